@@ -1,0 +1,189 @@
+"""Pins of the oracle's physical incremental cache (Sec. 3.1).
+
+* Each coded token's words and metadata, decoded by hand with numpy from the
+  documented image layout, equal the pinned group coder applied to that
+  token's values (catches wrong slots, transposed packing, wrong groups).
+* Appending is chunking-invariant: one call, token-by-token and ragged
+  chunks give byte-identical images (the state depends on tokens, not calls).
+* KIVI residual window: the newest tokens stay fp16 in the ring; with at
+  most 128 tokens nothing is coded.
+* Every reconstructed element meets the coder's s/2 bound against its input.
+* Capacity and format errors leave the cache untouched.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_04263_amd import configs, synth
+
+FMTS = {
+    "affine4_g32": configs.make_format(4, 4, k_group=32, v_group=32),
+    "affine4_g64": configs.make_format(4, 4, k_group=64, v_group=64),
+    "affine2_g64": configs.make_format(2, 2, k_group=64, v_group=64),
+    "kivi_k2v2": configs.WORKLOADS["llama8b_kivi"].fmt,
+    "had_k4v2": configs.make_format(4, 2, k_mode=1, v_mode=1, k_group=64, v_group=32, rotate=64),
+    "sym4_window": configs.make_format(4, 4, k_mode=1, v_mode=1, k_group=32, v_group=64,
+                                       residual=32, flush=32),
+}
+
+
+def f32(bits):
+    return synth.bf16_bits_to_f32(bits)
+
+
+def words(img, off, count):
+    return np.frombuffer(img[off:off + 4 * count].tobytes(), dtype=np.uint32)
+
+
+def floats(img, off, count):
+    return np.frombuffer(img[off:off + 4 * count].tobytes(), dtype=np.float32)
+
+
+def test_per_token_affine_slots_decode_by_hand():
+    f = FMTS["affine4_g32"]
+    B, H, D, T = 2, 3, 64, 40
+    K, V = synth.kv_tokens(11, B, 37, H, D)
+    c = oracle.Cache(f, B, H, D, T)
+    c.append(K[:, :20], V[:, :20])
+    c.append(K[:, 20:], V[:, 20:])
+    off, ln, _ = oracle.layout(f, B, H, D, T)
+    Ta = 64
+    kc = words(c.image, off[0], ln[0] // 4).reshape(B, H, Ta, D // 8)
+    ks = floats(c.image, off[1], ln[1] // 4).reshape(B, H, Ta, D // 32)
+    kz = floats(c.image, off[2], ln[2] // 4).reshape(B, H, Ta, D // 32)
+    vc = words(c.image, off[3], ln[3] // 4).reshape(B, H, Ta // 8, D)
+    vs = floats(c.image, off[4], ln[4] // 4).reshape(B, H, Ta, D // 32)
+    vz = floats(c.image, off[5], ln[5] // 4).reshape(B, H, Ta, D // 32)
+    for b in range(B):
+        for h in range(H):
+            for t in (0, 7, 8, 19, 20, 36):
+                x = f32(K[b, t, h])
+                y = f32(V[b, t, h])
+                for gi in range(2):
+                    codes, s, z = oracle.quant_affine(x[32 * gi:32 * gi + 32], 4)
+                    assert ks[b, h, t, gi] == s and kz[b, h, t, gi] == z
+                    for w in range(4):
+                        assert kc[b, h, t, 4 * gi + w] == oracle.pack_word(codes[8 * w:8 * w + 8], 4)
+                    vcodes, vs_, vz_ = oracle.quant_affine(y[32 * gi:32 * gi + 32], 4)
+                    assert vs[b, h, t, gi] == vs_ and vz[b, h, t, gi] == vz_
+                    for d in range(32):
+                        word = vc[b, h, t // 8, 32 * gi + d]
+                        assert (word >> (4 * (t % 8))) & 15 == vcodes[d]
+    # bits of tokens past n in the last partial V word are zero
+    last = vc[:, :, 36 // 8, :]
+    assert np.all(last >> (4 * (37 % 8)) == 0)
+
+
+def test_per_channel_keys_decode_by_hand():
+    f = FMTS["kivi_k2v2"]
+    B, H, D, T = 1, 2, 128, 256
+    K, V = synth.kv_tokens(12, B, 200, H, D)
+    c = oracle.Cache(f, B, H, D, T)
+    c.append(K, V)
+    assert c.n == 200 and c.n_coded == 64
+    off, ln, _ = oracle.layout(f, B, H, D, T)
+    kc = words(c.image, off[0], ln[0] // 4).reshape(B, H, T, D // 16)
+    ks = floats(c.image, off[1], ln[1] // 4).reshape(B, H, T // 32, D)
+    kz = floats(c.image, off[2], ln[2] // 4).reshape(B, H, T // 32, D)
+    for h in range(H):
+        for grp in range(2):
+            for d in (0, 5, 127):
+                col = np.array([oracle.f16_to_f32(oracle.f32_to_f16(f32(K[0, 32 * grp + i, h, d])))
+                                for i in range(32)], dtype=np.float32).reshape(-1)
+                codes, s, z = oracle.quant_affine(col, 2)
+                assert ks[0, h, grp, d] == s and kz[0, h, grp, d] == z
+                for i in range(32):
+                    word = kc[0, h, 32 * grp + i, d // 16]
+                    assert (word >> (2 * (d % 16))) & 3 == codes[i]
+    # the ring holds fp16 of the newest 160 tokens at slot t mod 160
+    kr = np.frombuffer(c.image[off[6]:off[6] + ln[6]].tobytes(), dtype=np.uint16).reshape(B, H, 160, D)
+    for t in (40, 100, 199):
+        assert np.array_equal(kr[0, 1, t % 160], oracle.f32_to_f16(f32(K[0, t, 1])))
+
+
+@pytest.mark.parametrize("name", list(FMTS))
+def test_chunking_invariance(name):
+    f = FMTS[name]
+    B, H, D = 2, 2, 64 if f["k_axis"] == 0 else 128
+    n = 230
+    K, V = synth.kv_tokens(13, B, n, H, D)
+    whole = oracle.Cache(f, B, H, D, 256)
+    whole.append(K, V)
+    single = oracle.Cache(f, B, H, D, 256)
+    for t in range(n):
+        single.append(K[:, t:t + 1], V[:, t:t + 1])
+    ragged = oracle.Cache(f, B, H, D, 256)
+    cuts = [0, 1, 31, 32, 77, 128, 129, 200, n]
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        ragged.append(K[:, a:b], V[:, a:b])
+    assert whole.n == single.n == ragged.n == n
+    assert np.array_equal(whole.image, single.image)
+    assert np.array_equal(whole.image, ragged.image)
+
+
+@pytest.mark.parametrize("name", list(FMTS))
+def test_reconstruction_error_bound(name):
+    f = FMTS[name]
+    B, H, D = 1, 2, 64 if f["k_axis"] == 0 else 128
+    n = 200
+    K, V = synth.kv_tokens(14, B, n, H, D)
+    c = oracle.Cache(f, B, H, D, n)
+    c.append(K, V)
+    kh, vh = c.dequant()
+    nq = c.n_coded
+    for X, Xh, bits, mode, axis, group in (
+            (K, kh, f["k_bits"], f["k_mode"], f["k_axis"], f["k_group"]),
+            (V, vh, f["v_bits"], f["v_mode"], f["v_axis"], f["v_group"])):
+        x = f32(X).transpose(0, 2, 1, 3).astype(np.float32)      # [B, H, n, D]
+        if f["rotate"]:
+            x = oracle.fwht_f32(x)
+        if f["flush"]:
+            x = oracle.f16_to_f32(oracle.f32_to_f16(x))
+        x = x.astype(np.float64)
+        # residual tokens are the fp16 values exactly
+        assert np.array_equal(Xh[:, :, nq:], x[:, :, nq:])
+        err = np.abs(Xh[:, :, :nq] - x[:, :, :nq])
+        if axis == 0:
+            xg = x[:, :, :nq].reshape(B, H, nq, D // group, group)
+            rng = xg.max(-1) - xg.min(-1)
+            amax = np.abs(xg).max(-1)
+            if mode == 0:
+                s = rng / (2 ** bits - 1)
+            else:
+                s = amax / (2 ** (bits - 1) - 1)
+            bound = np.repeat(np.maximum(s, 1e-8), group, axis=-1).reshape(err.shape)
+        else:
+            xg = x[:, :, :nq].reshape(B, H, nq // 32, 32, D)
+            s = (xg.max(3) - xg.min(3)) / (2 ** bits - 1)
+            bound = np.repeat(np.maximum(s, 1e-8)[:, :, :, None, :], 32, axis=3).reshape(err.shape)
+        assert np.all(err <= bound / 2 * (1 + 1e-6) + 1e-6 * np.abs(x[:, :, :nq]))
+
+
+def test_kivi_short_context_codes_nothing():
+    f = FMTS["kivi_k2v2"]
+    K, V = synth.kv_tokens(15, 1, 128, 2, 128)
+    c = oracle.Cache(f, 1, 2, 128, 300)
+    c.append(K, V)
+    assert c.n_coded == 0
+    off, ln, _ = oracle.layout(f, 1, 2, 128, 300)
+    assert not c.image[:off[6]].any()       # no codes or metadata written
+
+
+def test_capacity_and_errors_leave_state_untouched():
+    f = FMTS["affine4_g64"]
+    K, V = synth.kv_tokens(16, 1, 10, 1, 64)
+    c = oracle.Cache(f, 1, 1, 64, 12)
+    c.append(K[:, :8], V[:, :8])
+    before = c.image.copy()
+    with pytest.raises(oracle.OracleError) as e:
+        c.append(K[:, :5], V[:, :5])
+    assert e.value.status == 3
+    assert c.n == 8 and np.array_equal(c.image, before)
+    bad = K.copy()
+    bad[0, 0, 0, 0] = 0x7FC0                # bf16 NaN
+    with pytest.raises(oracle.OracleError) as e:
+        c.append(bad[:, :1], V[:, :1])
+    assert e.value.status == 4
+    assert c.n == 8 and np.array_equal(c.image, before)
+    c.append(K[:, :0], V[:, :0])            # empty append is a no-op
+    assert c.n == 8 and np.array_equal(c.image, before)
