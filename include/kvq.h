@@ -1,0 +1,173 @@
+/*
+ * kvq.h -- C ABI of the MI355X (gfx950) packed low-bit KV-cache decode path.
+ *
+ * Hot path of "Quality Recovery for Quantized KV Caches via Low-Rank
+ * Attention Adaptation" (Abdellatif): the adapted Q/K/V projection
+ * (Sec. 3, Eq. (1)-(2)), quantize-and-pack append into a physically packed
+ * incremental cache (Sec. 3.1, Eq. (3)), and decode attention over the
+ * reconstruction (Sec. 3.1-3.2), each a hand-written HIP kernel.
+ *
+ * Conventions for every call:
+ *   - Tensor arguments are DEVICE pointers owned by the caller; the library
+ *     never allocates or frees device memory.  A cache handle is host memory.
+ *   - Work is enqueued on the caller's HIP stream (passed as void*, NULL =
+ *     the default stream) and runs asynchronously; the call returns once
+ *     enqueued.  Calls on one handle must be ordered by the caller (one
+ *     stream, or explicit events); a handle is not thread-safe.
+ *   - Every argument is checked on the host before anything is enqueued; a
+ *     call that returns an error has changed no state and launched nothing.
+ *     KVQ_ERR_DEVICE reports a HIP launch error (state is then undefined).
+ *   - Device pointers must be 16-byte aligned.  bf16 and fp16 tensors are
+ *     16-bit IEEE-style storage (bfloat16 / binary16).
+ *   - Non-finite inputs are outside the contract (results are undefined).
+ */
+#ifndef KVQ_H
+#define KVQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    KVQ_OK = 0,
+    KVQ_ERR_ARG = 1,       /* null/misaligned pointer, bad size or shape, empty cache */
+    KVQ_ERR_FORMAT = 2,    /* unsupported format, or format differs from the cache's */
+    KVQ_ERR_CAPACITY = 3,  /* append would exceed T_max tokens */
+    KVQ_ERR_WORKSPACE = 4, /* workspace smaller than the *_workspace_bytes query */
+    KVQ_ERR_DEVICE = 5     /* HIP runtime/launch error */
+} kvq_status;
+
+enum { KVQ_AFFINE = 0, KVQ_SYMMETRIC = 1 };
+enum { KVQ_PER_TOKEN = 0, KVQ_PER_CHANNEL = 1 };
+
+/* Cache format (Sec. 3.1).
+ *   *_bits   2 or 4: code width.
+ *   *_mode   KVQ_AFFINE: Eq. (3), s = max((max-min)/(2^b-1), 1e-8),
+ *            c = clip(round_half_even((x-min)/s), 0, 2^b-1), offset = min.
+ *            KVQ_SYMMETRIC (the symmetric control, "max-magnitude scale, no
+ *            offset"; formula is this library's reading): s = max(max|x| /
+ *            (2^(b-1)-1), 1e-8), q = clip(round(x/s), -(2^(b-1)-1), ...),
+ *            stored code q + 2^(b-1).
+ *   *_axis   KVQ_PER_TOKEN: groups of *_group consecutive head_dim elements
+ *            of one token.  KVQ_PER_CHANNEL (keys only, KIVI): groups of 32
+ *            consecutive tokens of one channel (k_group must be 32).
+ *   *_group  32..head_dim, power of two (per token); 32 (per channel).
+ *   residual, flush   fp16 window (KIVI, Sec. 3.1): with flush F > 0, the
+ *            newest tokens stay fp16 and tokens are coded F at a time; the
+ *            number coded at length n is floor(max(0, n - residual)/F) * F.
+ *            F must be a multiple of 32; both 0 = no window.
+ *   rotate   0, or head_dim: apply the fixed normalized Hadamard transform
+ *            (KVarN, Sec. 3.1) to K and V before coding, to queries before
+ *            attention and to outputs after it.
+ * Scales and offsets are stored as fp32. */
+typedef struct {
+    int32_t k_bits, v_bits;
+    int32_t k_mode, v_mode;
+    int32_t k_axis, v_axis;
+    int32_t k_group, v_group;
+    int32_t residual, flush;
+    int32_t rotate;
+} kvq_format;
+
+/* Opaque host handle: format, dimensions, storage pointer, token count. */
+typedef struct kvq_cache kvq_cache;
+
+/* Bytes of cache storage for B sequences, H_kv heads of size D (64, 128 or
+ * 256) and up to T_max tokens.  The storage image has eight sections, each
+ * starting at a multiple of 256 bytes (T_alloc = T_max rounded up to 32):
+ *   0 Kc u32 [B][H_kv][T_alloc][D*k_bits/32]  K codes, packed along head_dim
+ *   1 Ks f32 [B][H_kv][T_alloc][D/k_group]    (per channel: [T_alloc/32][D])
+ *   2 Kz f32, like Ks; affine keys only (else 0 bytes)
+ *   3 Vc u32 [B][H_kv][T_alloc*v_bits/32][D]  V codes, packed along tokens
+ *   4 Vs f32 [B][H_kv][T_alloc][D/v_group]
+ *   5 Vz f32, like Vs; affine values only
+ *   6 Kr f16 [B][H_kv][residual+flush][D]     fp16 window, slot t mod (R+F)
+ *   7 Vr f16, like Kr
+ * In a packed word, element j of its run of 32/bits codes occupies bits
+ * [bits*j, bits*j + bits). */
+kvq_status kvq_cache_bytes(const kvq_format* fmt, int B, int H_kv, int D, int T_max, size_t* bytes);
+
+/* Create a handle over caller storage (at least kvq_cache_bytes bytes,
+ * 256-byte aligned, ZERO-FILLED by the caller).  Host-only: enqueues nothing.
+ * The cache starts empty (n = 0). */
+kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_max, void* storage,
+                          size_t bytes, kvq_cache** out);
+
+/* Byte offset and length of storage section 0..7 (see kvq_cache_bytes). */
+kvq_status kvq_cache_section(const kvq_cache* cache, int index, size_t* offset, size_t* length);
+
+/* n = 0: start a new window (the paper resets the cache per evaluation
+ * window, Sec. 4).  Storage is not cleared; slots at or past n are dead. */
+kvq_status kvq_cache_reset(kvq_cache* cache);
+
+/* Tokens cached (n) and tokens held as codes (n_coded <= n). */
+kvq_status kvq_cache_len(const kvq_cache* cache, int* n, int* n_coded);
+
+/* Shrink n to n_new <= n without touching storage.  Valid only for formats
+ * without an fp16 window (flush == 0), where the first n_new tokens' bytes
+ * are unchanged by later appends; otherwise KVQ_ERR_FORMAT. */
+kvq_status kvq_cache_rewind(kvq_cache* cache, int n_new);
+
+/* Free the host handle (not the storage). */
+void kvq_cache_destroy(kvq_cache* cache);
+
+/* Workspace bytes kvq_project_qkv needs for M rows and adapter rank r
+ * (the fp32 adapter activations (alpha/r) A h, M x 3r). */
+kvq_status kvq_project_workspace_bytes(int M, int rank, size_t* bytes);
+
+/* Adapted Q/K/V projection, Eq. (1)-(2) with the explicit adapter branch of
+ * Sec. 3.4: for each row h of H and projection p in {Q, K, V},
+ *     y_p = W_p h + lora_scale * B_p (A_p h),   lora_scale = alpha / r.
+ *   H  bf16 [M][d_in]             (M = tokens; d_in a multiple of 64)
+ *   W  bf16 [d_q + 2 d_kv][d_in]  rows of W_Q, then W_K, then W_V
+ *   A  bf16 [3 rank][d_in]        A_Q, A_K, A_V (ignored when rank == 0)
+ *   Bm bf16 [d_q + 2 d_kv][rank]  B_Q, B_K, B_V rows aligned with W's rows
+ *   Q  bf16 [M][d_q], K and V bf16 [M][d_kv]: outputs, fp32 accumulation,
+ *      rounded once to bf16 (round to nearest even).
+ * rank 0 disables the adapter.  rank <= 64.  d_q, d_kv multiples of 16. */
+kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_q, int d_kv,
+                           const void* A, const void* Bm, int rank, float lora_scale, void* Q,
+                           void* K, void* V, void* workspace, size_t ws_bytes, void* stream);
+
+/* Append n_new tokens per sequence (Sec. 3.1: new states are coded, packed
+ * and appended; the cache keeps no unquantized copy beyond the fp16 window).
+ *   K, V  bf16 [B][n_new][H_kv][D] (the natural view of the projection's
+ *         [B * n_new][d_kv] output).
+ *   fmt   must equal the cache's format (KVQ_ERR_FORMAT otherwise).
+ * The resulting storage bytes depend only on the tokens appended since the
+ * last reset, not on how they were split into calls.  Codes and metadata
+ * are bit-exact functions of the input (IEEE fp32, fixed operation order).
+ * n + n_new > T_max returns KVQ_ERR_CAPACITY.  n_new == 0 is a no-op. */
+kvq_status kvq_append(kvq_cache* cache, const void* K, const void* V, int n_new,
+                      const kvq_format* fmt, void* stream);
+
+/* Workspace bytes kvq_decode_attn needs for H_q query heads at any length
+ * up to the cache's T_max: split-K partial results plus one arrival counter
+ * per KV head.  The workspace must be ZERO-FILLED before its first use and
+ * left untouched by the caller between calls: every call returns the
+ * counters to zero.  Calls that share a workspace must not overlap. */
+kvq_status kvq_decode_workspace_bytes(const kvq_cache* cache, int H_q, size_t* bytes);
+
+/* Decode attention for one new query per sequence over the reconstructed
+ * cache (Sec. 3.1-3.2: attention sees the stored reconstruction).
+ *   Q  bf16 [B][H_q][D]; query head h reads KV head h / (H_q / H_kv);
+ *      H_q a multiple of H_kv with H_q / H_kv <= 16.
+ *   O  fp32 [B][H_q][D]: sum_t softmax_t(sm_scale * q . k_t) v_t over all n
+ *      cached tokens (coded tokens reconstructed in-kernel, window tokens
+ *      from fp16).  With a rotating format q is rotated first and the
+ *      output rotated back.
+ * An empty cache (n == 0) returns KVQ_ERR_ARG. */
+kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
+                           void* workspace, size_t ws_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* kvq_strerror(kvq_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVQ_H */

@@ -1,0 +1,310 @@
+// Quantize-and-pack append into the physically packed incremental cache
+// (Sec. 3.1 of the paper: new key/value states are coded with Eq. (3) or the
+// symmetric control, bit-packed and appended; KIVI keeps an fp16 window).
+//
+// Bit-exactness: codes and metadata must equal the CPU reference bit for
+// bit, so this file is compiled with -ffp-contract=off and the coder uses
+// exactly one IEEE binary32 operation per step: subtract, correctly rounded
+// divide, round-half-even (v_rndne_f32), clamp.  Min/max are exact.
+//
+// One workgroup (256 threads) codes one aligned block of 32 tokens of one
+// (sequence, KV head): the block's K rows are staged in LDS as fp32 (rotated
+// by the fixed Hadamard butterflies when the format rotates, rounded to fp16
+// when a window exists), group statistics are reduced per (token, group) or
+// per channel, and every output word is assembled by one thread.  V rows
+// follow through the same LDS buffer.  V codes are packed along tokens: a
+// word shared with tokens outside the block range keeps earlier tokens' bits
+// and clears later ones, so the image is independent of call boundaries.
+
+#include "kvq_device.h"
+#include "kvq_internal.h"
+
+namespace kvq {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kBlockTok = 32;
+
+__device__ __forceinline__ uint32_t code_affine(float x, float mn, float s, float top)
+{
+    float c = __builtin_rintf((x - mn) / s);
+    c = fminf(fmaxf(c, 0.0f), top);
+    return (uint32_t)c;
+}
+
+__device__ __forceinline__ uint32_t code_sym(float x, float s, float qmax, float half)
+{
+    float q = __builtin_rintf(x / s);
+    q = fminf(fmaxf(q, -qmax), qmax);
+    return (uint32_t)(int)(q + half);
+}
+
+// Scale (and offset) of one group, Eq. (3) / symmetric control.
+__device__ __forceinline__ void group_stats(const float* x, int stride, int g, int mode, int bits,
+                                            float* s_out, float* z_out)
+{
+    if (mode == KVQ_AFFINE) {
+        float mn = x[0], mx = x[0];
+        for (int i = 1; i < g; ++i) {
+            float v = x[i * stride];
+            mn = fminf(mn, v);
+            mx = fmaxf(mx, v);
+        }
+        const float top = (float)((1 << bits) - 1);
+        float s = (mx - mn) / top;
+        if (!(s >= 1e-8f))
+            s = 1e-8f;
+        *s_out = s;
+        *z_out = mn + 0.0f;  // canonical +0 for a signed-zero minimum
+    } else {
+        float ma = 0.0f;
+        for (int i = 0; i < g; ++i)
+            ma = fmaxf(ma, fabsf(x[i * stride]));
+        const float qmax = (float)((1 << (bits - 1)) - 1);
+        float s = ma / qmax;
+        if (!(s >= 1e-8f))
+            s = 1e-8f;
+        *s_out = s;
+        *z_out = 0.0f;
+    }
+}
+
+__device__ __forceinline__ uint32_t code_one(float x, float s, float z, int mode, int bits)
+{
+    if (mode == KVQ_AFFINE)
+        return code_affine(x, z, s, (float)((1 << bits) - 1));
+    return code_sym(x, s, (float)((1 << (bits - 1)) - 1), (float)(1 << (bits - 1)));
+}
+
+// Fixed normalized Hadamard transform of `rows` rows of D fp32 values in LDS:
+// butterflies with half-width 1, 2, ..., D/2 then one multiply by c.  Rows
+// with use[row] == 0 are left untouched.
+template <int D>
+__device__ void fwht_rows(float* xs, int rows, const int* use, float c)
+{
+    for (int h = 1; h < D; h <<= 1) {
+        for (int idx = threadIdx.x; idx < rows * (D / 2); idx += kThreads) {
+            int row = idx / (D / 2), k = idx % (D / 2);
+            if (!use[row])
+                continue;
+            int j = (k / h) * 2 * h + (k % h);
+            float a = xs[row * D + j], b = xs[row * D + j + h];
+            xs[row * D + j] = a + b;
+            xs[row * D + j + h] = a - b;
+        }
+        __syncthreads();
+    }
+    for (int idx = threadIdx.x; idx < rows * D; idx += kThreads)
+        if (use[idx / D])
+            xs[idx] = xs[idx] * c;
+    __syncthreads();
+}
+
+// Stage the block's rows of K (which = 0) or V (which = 1) as the coder sees
+// them.  Row i is token tb + i; rows outside [q0, q1) are zero.
+template <int D>
+__device__ void stage_rows(const AppendParams& p, int which, int b, int h, int tb, float* xs, int* from_input)
+{
+    const uint16_t* in = which ? p.vin : p.kin;
+    const uint16_t* ring = which ? p.vr : p.kr;
+    for (int idx = threadIdx.x; idx < kBlockTok * D; idx += kThreads) {
+        int i = idx / D, d = idx % D, t = tb + i;
+        float v = 0.0f;
+        if (t >= p.q0 && t < p.q1) {
+            if (t >= p.n0)
+                v = bf16_to_f32(in[(((size_t)b * p.n_new + (t - p.n0)) * p.H + h) * D + d]);
+            else
+                v = f16_bits_to_f32(ring[(((size_t)b * p.H + h) * p.ring + t % p.ring) * D + d]);
+        }
+        xs[idx] = v;
+    }
+    if (threadIdx.x < kBlockTok) {
+        int t = tb + threadIdx.x;
+        from_input[threadIdx.x] = (t >= p.q0 && t < p.q1 && t >= p.n0) ? 1 : 0;
+    }
+    __syncthreads();
+    if (p.rotate)
+        fwht_rows<D>(xs, kBlockTok, from_input, p.rot_c);
+    if (p.ring) {
+        for (int idx = threadIdx.x; idx < kBlockTok * D; idx += kThreads)
+            if (from_input[idx / D])
+                xs[idx] = f16_bits_to_f32(f32_to_f16_bits(xs[idx]));
+        __syncthreads();
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
+{
+    __shared__ float xs[kBlockTok * D];
+    __shared__ float ms[kBlockTok * 8 > D ? kBlockTok * 8 : D];
+    __shared__ float mz[kBlockTok * 8 > D ? kBlockTok * 8 : D];
+    __shared__ int from_input[kBlockTok];
+
+    const int unit = blockIdx.y;
+    const int b = unit / p.H, h = unit % p.H;
+    const int tb = (p.q0 / kBlockTok + (int)blockIdx.x) * kBlockTok;
+    const int lo = max(p.q0, tb), hi = min(p.q1, tb + kBlockTok);
+    const size_t bh = (size_t)unit;
+
+    // ------------------------------------------------------------ keys
+    stage_rows<D>(p, 0, b, h, tb, xs, from_input);
+    const int kb = p.k_bits, kpw = 32 / kb, kwpt = D / kpw;
+    if (p.k_axis == KVQ_PER_TOKEN) {
+        const int ng = D / p.k_group;
+        for (int idx = threadIdx.x; idx < kBlockTok * ng; idx += kThreads) {
+            int i = idx / ng, gi = idx % ng, t = tb + i;
+            if (t < lo || t >= hi)
+                continue;
+            float s, z;
+            group_stats(xs + i * D + gi * p.k_group, 1, p.k_group, p.k_mode, kb, &s, &z);
+            ms[idx] = s;
+            mz[idx] = z;
+            size_t mi = (bh * p.T + t) * ng + gi;
+            p.ks[mi] = s;
+            if (p.k_mode == KVQ_AFFINE)
+                p.kz[mi] = z;
+        }
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < kBlockTok * kwpt; idx += kThreads) {
+            int i = idx / kwpt, w = idx % kwpt, t = tb + i;
+            if (t < lo || t >= hi)
+                continue;
+            int gi = (w * kpw) / p.k_group;
+            float s = ms[i * ng + gi], z = mz[i * ng + gi];
+            uint32_t word = 0;
+            for (int e = 0; e < kpw; ++e)
+                word |= code_one(xs[i * D + w * kpw + e], s, z, p.k_mode, kb) << (kb * e);
+            p.kc[(bh * p.T + t) * kwpt + w] = word;
+        }
+    } else {
+        // Per-channel keys: the block is one whole 32-token group.
+        for (int d = threadIdx.x; d < D; d += kThreads) {
+            float s, z;
+            group_stats(xs + d, D, kBlockTok, p.k_mode, kb, &s, &z);
+            ms[d] = s;
+            mz[d] = z;
+            size_t mi = (bh * (p.T / kBlockTok) + tb / kBlockTok) * D + d;
+            p.ks[mi] = s;
+            if (p.k_mode == KVQ_AFFINE)
+                p.kz[mi] = z;
+        }
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < kBlockTok * kwpt; idx += kThreads) {
+            int i = idx / kwpt, w = idx % kwpt, t = tb + i;
+            uint32_t word = 0;
+            for (int e = 0; e < kpw; ++e) {
+                int d = w * kpw + e;
+                word |= code_one(xs[i * D + d], ms[d], mz[d], p.k_mode, kb) << (kb * e);
+            }
+            p.kc[(bh * p.T + t) * kwpt + w] = word;
+        }
+    }
+    __syncthreads();
+
+    // ---------------------------------------------------------- values
+    stage_rows<D>(p, 1, b, h, tb, xs, from_input);
+    const int vb = p.v_bits, vpw = 32 / vb, ng = D / p.v_group;
+    for (int idx = threadIdx.x; idx < kBlockTok * ng; idx += kThreads) {
+        int i = idx / ng, gi = idx % ng, t = tb + i;
+        if (t < lo || t >= hi)
+            continue;
+        float s, z;
+        group_stats(xs + i * D + gi * p.v_group, 1, p.v_group, p.v_mode, vb, &s, &z);
+        ms[idx] = s;
+        mz[idx] = z;
+        size_t mi = (bh * p.T + t) * ng + gi;
+        p.vs[mi] = s;
+        if (p.v_mode == KVQ_AFFINE)
+            p.vz[mi] = z;
+    }
+    __syncthreads();
+    const int words_per_col = kBlockTok / vpw;  // words along tokens in this block
+    const size_t tw_all = (size_t)p.T / vpw;
+    for (int idx = threadIdx.x; idx < words_per_col * D; idx += kThreads) {
+        int tw = idx / D, d = idx % D;
+        int tfirst = tb + tw * vpw;
+        if (tfirst + vpw <= lo || tfirst >= hi)
+            continue;
+        uint32_t* dst = p.vc + (bh * tw_all + tfirst / vpw) * D + d;
+        uint32_t word = 0;
+        if (tfirst < lo) {  // keep the bits of tokens appended earlier
+            int keep_n = lo - tfirst;
+            word = *dst & ((1u << (vb * keep_n)) - 1u);
+        }
+        int gi = d / p.v_group;
+        for (int e = 0; e < vpw; ++e) {
+            int t = tfirst + e;
+            if (t < lo || t >= hi)
+                continue;
+            int i = t - tb;
+            word |= code_one(xs[i * D + d], ms[i * ng + gi], mz[i * ng + gi], p.v_mode, vb) << (vb * e);
+        }
+        *dst = word;
+    }
+}
+
+// fp16 window: slot t mod (R + F) <- fp16 of token t (rotated first when
+// the format rotates), for t in [ring_lo, n0 + n_new).  Runs after the coder
+// of the same call, which may still read the slots being replaced.
+template <int D>
+__global__ __launch_bounds__(kThreads) void append_ring_kernel(AppendParams p)
+{
+    __shared__ float xs[2 * D];
+    __shared__ int use[2];
+    const int unit = blockIdx.y;
+    const int b = unit / p.H, h = unit % p.H;
+    const int t = p.ring_lo + (int)blockIdx.x;
+    for (int idx = threadIdx.x; idx < 2 * D; idx += kThreads) {
+        int which = idx / D, d = idx % D;
+        const uint16_t* in = which ? p.vin : p.kin;
+        xs[idx] = bf16_to_f32(in[(((size_t)b * p.n_new + (t - p.n0)) * p.H + h) * D + d]);
+    }
+    if (threadIdx.x < 2)
+        use[threadIdx.x] = 1;
+    __syncthreads();
+    if (p.rotate)
+        fwht_rows<D>(xs, 2, use, p.rot_c);
+    for (int idx = threadIdx.x; idx < 2 * D; idx += kThreads) {
+        int which = idx / D, d = idx % D;
+        uint16_t* ring = which ? p.vr : p.kr;
+        ring[(((size_t)b * p.H + h) * p.ring + t % p.ring) * D + d] = f32_to_f16_bits(xs[idx]);
+    }
+}
+
+template <int D>
+hipError_t launch_append_d(const AppendParams& p, hipStream_t stream)
+{
+    const int units = p.B * p.H;
+    if (p.q1 > p.q0) {
+        int nblk = (p.q1 + kBlockTok - 1) / kBlockTok - p.q0 / kBlockTok;
+        hipLaunchKernelGGL(append_code_kernel<D>, dim3(nblk, units), dim3(kThreads), 0, stream, p);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
+    int n1 = p.n0 + p.n_new;
+    if (p.ring && n1 > p.ring_lo) {
+        hipLaunchKernelGGL(append_ring_kernel<D>, dim3(n1 - p.ring_lo, units), dim3(kThreads), 0, stream, p);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_append(const AppendParams& p, int D, hipStream_t stream)
+{
+    switch (D) {
+    case 64:
+        return launch_append_d<64>(p, stream);
+    case 128:
+        return launch_append_d<128>(p, stream);
+    case 256:
+        return launch_append_d<256>(p, stream);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace kvq

@@ -1,0 +1,396 @@
+// Host side of the C ABI declared in include/kvq.h: format validation, the
+// storage layout, argument checks (all before any launch, so an error
+// changes nothing) and kernel dispatch on the caller's stream.
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "kvq_internal.h"
+
+namespace {
+
+bool pow2_in(int v, int lo, int hi)
+{
+    return v >= lo && v <= hi && (v & (v - 1)) == 0;
+}
+
+kvq_status check_format(const kvq_format* f, int D)
+{
+    if (!f)
+        return KVQ_ERR_ARG;
+    if (D != 64 && D != 128 && D != 256)
+        return KVQ_ERR_FORMAT;
+    if ((f->k_bits != 2 && f->k_bits != 4) || (f->v_bits != 2 && f->v_bits != 4))
+        return KVQ_ERR_FORMAT;
+    if ((f->k_mode != KVQ_AFFINE && f->k_mode != KVQ_SYMMETRIC) ||
+        (f->v_mode != KVQ_AFFINE && f->v_mode != KVQ_SYMMETRIC))
+        return KVQ_ERR_FORMAT;
+    if ((f->k_axis != KVQ_PER_TOKEN && f->k_axis != KVQ_PER_CHANNEL) || f->v_axis != KVQ_PER_TOKEN)
+        return KVQ_ERR_FORMAT;
+    if (f->residual < 0 || f->flush < 0 || (f->flush == 0 && f->residual != 0) || f->flush % 32 != 0)
+        return KVQ_ERR_FORMAT;
+    if (f->rotate != 0 && f->rotate != D)
+        return KVQ_ERR_FORMAT;
+    if (f->k_axis == KVQ_PER_TOKEN ? !pow2_in(f->k_group, 32, D) : (f->k_group != 32 || f->flush == 0))
+        return KVQ_ERR_FORMAT;
+    if (!pow2_in(f->v_group, 32, D))
+        return KVQ_ERR_FORMAT;
+    return KVQ_OK;
+}
+
+size_t round_up(size_t v, size_t a)
+{
+    return (v + a - 1) / a * a;
+}
+
+kvq_status layout(const kvq_format* f, int B, int H, int D, int T_max, size_t off[8], size_t len[8], size_t* total)
+{
+    kvq_status st = check_format(f, D);
+    if (st != KVQ_OK)
+        return st;
+    if (B < 1 || H < 1 || T_max < 1)
+        return KVQ_ERR_ARG;
+    const size_t bh = (size_t)B * H, T = round_up((size_t)T_max, 32);
+    const size_t ring = (size_t)(f->residual + f->flush);
+    len[0] = bh * T * (size_t)(D * f->k_bits / 32) * 4;
+    len[1] = f->k_axis == KVQ_PER_TOKEN ? bh * T * (size_t)(D / f->k_group) * 4 : bh * (T / 32) * (size_t)D * 4;
+    len[2] = f->k_mode == KVQ_AFFINE ? len[1] : 0;
+    len[3] = bh * (T * f->v_bits / 32) * (size_t)D * 4;
+    len[4] = bh * T * (size_t)(D / f->v_group) * 4;
+    len[5] = f->v_mode == KVQ_AFFINE ? len[4] : 0;
+    len[6] = f->flush ? bh * ring * (size_t)D * 2 : 0;
+    len[7] = len[6];
+    size_t o = 0;
+    for (int i = 0; i < 8; ++i) {
+        off[i] = o;
+        o = round_up(o + len[i], 256);
+    }
+    *total = o;
+    return KVQ_OK;
+}
+
+bool aligned16(const void* p)
+{
+    return ((uintptr_t)p & 15u) == 0;
+}
+
+bool same_format(const kvq_format& a, const kvq_format& b)
+{
+    return memcmp(&a, &b, sizeof(kvq_format)) == 0;
+}
+
+float rotation_constant(int D)
+{
+    return (float)(1.0 / sqrt((double)D));  // binary32 value nearest D^(-1/2)
+}
+
+// Decode workspace: partial outputs fp32 [B*H_q][S][D], partial (max, sum)
+// fp32 [B*H_q][S][2], then one arrival counter per KV head (u32 [B*H]).
+// The counters sit at a fixed offset for a given cache and head count,
+// so the split count S of a call never moves them.
+size_t decode_workspace_layout(const kvq_cache* c, int H_q, int S, size_t* off_ml, size_t* off_cnt)
+{
+    int S_max = kvq::decode_split_bound(c->B, c->H, kvq::num_coded(c->fmt, c->T_max)) + (c->fmt.flush ? 1 : 0);
+    (void)S;
+    size_t rows = (size_t)c->B * H_q;
+    size_t o_ml = round_up(rows * S_max * c->D * sizeof(float), 256);
+    size_t o_cnt = round_up(o_ml + rows * S_max * 2 * sizeof(float), 256);
+    if (off_ml)
+        *off_ml = o_ml;
+    if (off_cnt)
+        *off_cnt = o_cnt;
+    return o_cnt + (size_t)c->B * c->H * sizeof(unsigned);
+}
+
+template <typename T>
+T* at(const kvq_cache* c, int section)
+{
+    return (T*)(c->base + c->off[section]);
+}
+
+}  // namespace
+
+namespace kvq {
+
+int num_coded(const kvq_format& f, int n)
+{
+    if (f.flush == 0)
+        return n;
+    int over = n - f.residual;
+    return over <= 0 ? 0 : over / f.flush * f.flush;
+}
+
+}  // namespace kvq
+
+extern "C" {
+
+const char* kvq_strerror(kvq_status s)
+{
+    switch (s) {
+    case KVQ_OK:
+        return "ok";
+    case KVQ_ERR_ARG:
+        return "invalid argument";
+    case KVQ_ERR_FORMAT:
+        return "unsupported or mismatched cache format";
+    case KVQ_ERR_CAPACITY:
+        return "cache capacity exceeded";
+    case KVQ_ERR_WORKSPACE:
+        return "workspace too small";
+    case KVQ_ERR_DEVICE:
+        return "HIP device error";
+    }
+    return "unknown status";
+}
+
+kvq_status kvq_cache_bytes(const kvq_format* fmt, int B, int H_kv, int D, int T_max, size_t* bytes)
+{
+    if (!bytes)
+        return KVQ_ERR_ARG;
+    size_t off[8], len[8];
+    return layout(fmt, B, H_kv, D, T_max, off, len, bytes);
+}
+
+kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_max, void* storage, size_t bytes,
+                          kvq_cache** out)
+{
+    if (!out || !storage || ((uintptr_t)storage & 255u))
+        return KVQ_ERR_ARG;
+    size_t off[8], len[8], total;
+    kvq_status st = layout(fmt, B, H_kv, D, T_max, off, len, &total);
+    if (st != KVQ_OK)
+        return st;
+    if (bytes < total)
+        return KVQ_ERR_ARG;
+    kvq_cache* c = (kvq_cache*)calloc(1, sizeof(kvq_cache));
+    if (!c)
+        return KVQ_ERR_ARG;
+    c->fmt = *fmt;
+    c->B = B;
+    c->H = H_kv;
+    c->D = D;
+    c->T_max = T_max;
+    c->T_alloc = (int)round_up((size_t)T_max, 32);
+    c->base = (uint8_t*)storage;
+    c->bytes = bytes;
+    memcpy(c->off, off, sizeof(off));
+    memcpy(c->len, len, sizeof(len));
+    c->n = 0;
+    *out = c;
+    return KVQ_OK;
+}
+
+kvq_status kvq_cache_section(const kvq_cache* c, int index, size_t* offset, size_t* length)
+{
+    if (!c || index < 0 || index > 7 || !offset || !length)
+        return KVQ_ERR_ARG;
+    *offset = c->off[index];
+    *length = c->len[index];
+    return KVQ_OK;
+}
+
+kvq_status kvq_cache_reset(kvq_cache* c)
+{
+    if (!c)
+        return KVQ_ERR_ARG;
+    c->n = 0;
+    return KVQ_OK;
+}
+
+kvq_status kvq_cache_len(const kvq_cache* c, int* n, int* n_coded)
+{
+    if (!c || !n || !n_coded)
+        return KVQ_ERR_ARG;
+    *n = c->n;
+    *n_coded = kvq::num_coded(c->fmt, c->n);
+    return KVQ_OK;
+}
+
+kvq_status kvq_cache_rewind(kvq_cache* c, int n_new)
+{
+    if (!c || n_new < 0 || n_new > c->n)
+        return KVQ_ERR_ARG;
+    if (c->fmt.flush != 0)
+        return KVQ_ERR_FORMAT;
+    c->n = n_new;
+    return KVQ_OK;
+}
+
+void kvq_cache_destroy(kvq_cache* c)
+{
+    free(c);
+}
+
+kvq_status kvq_project_workspace_bytes(int M, int rank, size_t* bytes)
+{
+    if (!bytes || M < 0 || rank < 0 || rank > 64)
+        return KVQ_ERR_ARG;
+    *bytes = (size_t)M * 3 * rank * sizeof(float);
+    return KVQ_OK;
+}
+
+kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_q, int d_kv, const void* A,
+                           const void* Bm, int rank, float lora_scale, void* Q, void* K, void* V, void* workspace,
+                           size_t ws_bytes, void* stream)
+{
+    if (M < 0 || d_in < 64 || d_in % 64 != 0 || d_q < 16 || d_kv < 16 || d_q % 16 != 0 || d_kv % 16 != 0)
+        return KVQ_ERR_ARG;
+    if (rank < 0 || rank > 64 || !isfinite(lora_scale))
+        return KVQ_ERR_ARG;
+    if (M == 0)
+        return KVQ_OK;
+    if (!H || !W || !Q || !K || !V || !aligned16(H) || !aligned16(W) || !aligned16(Q) || !aligned16(K) ||
+        !aligned16(V))
+        return KVQ_ERR_ARG;
+    if (rank > 0) {
+        if (!A || !Bm || !aligned16(A) || !aligned16(Bm) || !workspace || !aligned16(workspace))
+            return KVQ_ERR_ARG;
+        if (ws_bytes < (size_t)M * 3 * rank * sizeof(float))
+            return KVQ_ERR_WORKSPACE;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const int N = d_q + 2 * d_kv;
+    if (rank > 0) {
+        kvq::ProjParams a = {};
+        a.x = (const uint16_t*)H;
+        a.w = (const uint16_t*)A;
+        a.yf = (float*)workspace;
+        a.M = M;
+        a.K = d_in;
+        a.N = 3 * rank;
+        a.n1 = a.n2 = 3 * rank;
+        a.rank = 0;
+        a.scale = lora_scale;
+        if (kvq::launch_project(a, s) != hipSuccess)
+            return KVQ_ERR_DEVICE;
+    }
+    kvq::ProjParams p = {};
+    p.x = (const uint16_t*)H;
+    p.w = (const uint16_t*)W;
+    p.bm = (const uint16_t*)Bm;
+    p.t = (const float*)workspace;
+    p.y0 = (uint16_t*)Q;
+    p.y1 = (uint16_t*)K;
+    p.y2 = (uint16_t*)V;
+    p.M = M;
+    p.K = d_in;
+    p.N = N;
+    p.n1 = d_q;
+    p.n2 = d_q + d_kv;
+    p.rank = rank;
+    p.scale = 1.0f;
+    return kvq::launch_project(p, s) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+}
+
+kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int n_new, const kvq_format* fmt, void* stream)
+{
+    if (!c || !fmt || n_new < 0)
+        return KVQ_ERR_ARG;
+    if (!same_format(c->fmt, *fmt))
+        return KVQ_ERR_FORMAT;
+    if (n_new == 0)
+        return KVQ_OK;
+    if (!K || !V || !aligned16(K) || !aligned16(V))
+        return KVQ_ERR_ARG;
+    if ((long long)c->n + n_new > c->T_max)
+        return KVQ_ERR_CAPACITY;
+    const kvq_format& f = c->fmt;
+    kvq::AppendParams p = {};
+    p.kc = at<uint32_t>(c, 0);
+    p.ks = at<float>(c, 1);
+    p.kz = at<float>(c, 2);
+    p.vc = at<uint32_t>(c, 3);
+    p.vs = at<float>(c, 4);
+    p.vz = at<float>(c, 5);
+    p.kr = at<uint16_t>(c, 6);
+    p.vr = at<uint16_t>(c, 7);
+    p.kin = (const uint16_t*)K;
+    p.vin = (const uint16_t*)V;
+    p.B = c->B;
+    p.H = c->H;
+    p.T = c->T_alloc;
+    p.n0 = c->n;
+    p.n_new = n_new;
+    p.q0 = kvq::num_coded(f, c->n);
+    p.q1 = kvq::num_coded(f, c->n + n_new);
+    p.ring = f.residual + f.flush;
+    int n1 = c->n + n_new;
+    p.ring_lo = p.ring ? (n1 - p.ring > c->n ? n1 - p.ring : c->n) : n1;
+    p.k_bits = f.k_bits;
+    p.v_bits = f.v_bits;
+    p.k_mode = f.k_mode;
+    p.v_mode = f.v_mode;
+    p.k_axis = f.k_axis;
+    p.k_group = f.k_group;
+    p.v_group = f.v_group;
+    p.rotate = f.rotate;
+    p.rot_c = rotation_constant(c->D);
+    if (kvq::launch_append(p, c->D, (hipStream_t)stream) != hipSuccess)
+        return KVQ_ERR_DEVICE;
+    c->n = n1;
+    return KVQ_OK;
+}
+
+kvq_status kvq_decode_workspace_bytes(const kvq_cache* c, int H_q, size_t* bytes)
+{
+    if (!c || !bytes || H_q < c->H || H_q % c->H != 0 || H_q / c->H > 16)
+        return KVQ_ERR_ARG;
+    // Splits never exceed the bound at the largest coded-token count.
+    int S_tot = kvq::decode_split_bound(c->B, c->H, kvq::num_coded(c->fmt, c->T_max)) + (c->fmt.flush ? 1 : 0);
+    *bytes = decode_workspace_layout(c, H_q, S_tot, nullptr, nullptr);
+    return KVQ_OK;
+}
+
+kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_scale, void* O, void* workspace,
+                           size_t ws_bytes, void* stream)
+{
+    if (!c || !Q || !O || !workspace || !aligned16(Q) || !aligned16(O) || !aligned16(workspace))
+        return KVQ_ERR_ARG;
+    if (H_q < c->H || H_q % c->H != 0 || H_q / c->H > 16 || !isfinite(sm_scale))
+        return KVQ_ERR_ARG;
+    if (c->n < 1)
+        return KVQ_ERR_ARG;
+    const kvq_format& f = c->fmt;
+    kvq::AttnParams p = {};
+    p.nq = kvq::num_coded(f, c->n);
+    kvq::decode_plan(c->B, c->H, p.nq, &p.S_q, &p.bps);
+    p.S_tot = p.S_q + (f.flush ? 1 : 0);
+    size_t off_ml, off_cnt;
+    const size_t need = decode_workspace_layout(c, H_q, p.S_tot, &off_ml, &off_cnt);
+    if (ws_bytes < need)
+        return KVQ_ERR_WORKSPACE;
+    p.kc = at<uint32_t>(c, 0);
+    p.ks = at<float>(c, 1);
+    p.kz = at<float>(c, 2);
+    p.vc = at<uint32_t>(c, 3);
+    p.vs = at<float>(c, 4);
+    p.vz = at<float>(c, 5);
+    p.kr = at<uint16_t>(c, 6);
+    p.vr = at<uint16_t>(c, 7);
+    p.q = (const uint16_t*)Q;
+    p.part_o = (float*)workspace;
+    p.part_ml = (float*)((uint8_t*)workspace + off_ml);
+    p.counters = (unsigned*)((uint8_t*)workspace + off_cnt);
+    p.out = (float*)O;
+    p.B = c->B;
+    p.H = c->H;
+    p.H_q = H_q;
+    p.G = H_q / c->H;
+    p.T = c->T_alloc;
+    p.n = c->n;
+    p.ring = f.residual + f.flush;
+    p.k_bits = f.k_bits;
+    p.v_bits = f.v_bits;
+    p.k_mode = f.k_mode;
+    p.v_mode = f.v_mode;
+    p.k_axis = f.k_axis;
+    p.k_group = f.k_group;
+    p.v_group = f.v_group;
+    p.rotate = f.rotate;
+    p.sm_log2 = sm_scale * 1.4426950408889634f;
+    p.rot_c = rotation_constant(c->D);
+    return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+}
+
+}  // extern "C"

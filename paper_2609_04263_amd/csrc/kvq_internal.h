@@ -1,0 +1,98 @@
+// Internal declarations shared by the host API and the HIP kernels of libkvq.
+// Nothing here is part of the public C ABI (include/kvq.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/kvq.h"
+
+// Host handle behind the opaque kvq_cache.
+struct kvq_cache {
+    kvq_format fmt;
+    int B, H, D, T_max, T_alloc;
+    uint8_t* base;
+    size_t bytes;
+    size_t off[8], len[8];
+    int n;
+};
+
+namespace kvq {
+
+// Tokens held as codes at length n (floor(max(0, n - R)/F) * F with a window).
+int num_coded(const kvq_format& f, int n);
+
+// ---------------------------------------------------------------- append
+struct AppendParams {
+    uint32_t* kc;
+    float* ks;
+    float* kz;
+    uint32_t* vc;
+    float* vs;
+    float* vz;
+    uint16_t* kr;
+    uint16_t* vr;
+    const uint16_t* kin;  // bf16 [B][n_new][H][D]
+    const uint16_t* vin;
+    int B, H, T;          // T = T_alloc
+    int n0, n_new;        // length before the call, tokens appended
+    int q0, q1;           // coded-token range written by this call
+    int ring;             // R + F (0 = no window)
+    int ring_lo;          // first token written to the ring by this call
+    int k_bits, v_bits, k_mode, v_mode, k_axis, k_group, v_group;
+    int rotate;           // 0 or D
+    float rot_c;          // binary32 value nearest D^(-1/2)
+};
+hipError_t launch_append(const AppendParams& p, int D, hipStream_t stream);
+
+// ------------------------------------------------------------- projection
+struct ProjParams {
+    const uint16_t* x;    // bf16 [M][K]  (hidden states)
+    const uint16_t* w;    // bf16 [N][K]  (weight rows)
+    const uint16_t* bm;   // bf16 [N][rank] adapter up-projection rows (rank > 0)
+    const float* t;       // fp32 [M][3 rank] scaled adapter activations (rank > 0)
+    uint16_t* y0;         // bf16 outputs: columns [0, n1) -> y0, [n1, n2) -> y1, [n2, N) -> y2
+    uint16_t* y1;
+    uint16_t* y2;
+    float* yf;            // fp32 output [M][N] (activation pass), else null
+    int M, K, N;
+    int n1, n2;           // column split points (d_q, d_q + d_kv)
+    int rank;
+    float scale;          // multiplies the fp32 output (activation pass)
+};
+hipError_t launch_project(const ProjParams& p, hipStream_t stream);
+
+// ---------------------------------------------------------------- decode
+struct AttnParams {
+    const uint32_t* kc;
+    const float* ks;
+    const float* kz;
+    const uint32_t* vc;
+    const float* vs;
+    const float* vz;
+    const uint16_t* kr;
+    const uint16_t* vr;
+    const uint16_t* q;    // bf16 [B][H_q][D]
+    float* part_o;        // fp32 [B*H_q][S_tot][D]  unnormalized partial outputs
+    float* part_ml;       // fp32 [B*H_q][S_tot][2]  (running max in log2 units, sum)
+    float* out;           // fp32 [B][H_q][D]
+    unsigned* counters;   // [B*H] arrival counters, zero between calls
+    int B, H, H_q, G, T;  // T = T_alloc
+    int n, nq;
+    int ring;
+    int S_q;              // splits over coded tokens
+    int S_tot;            // S_q (+1 when a window exists)
+    int bps;              // 32-token blocks per split
+    int k_bits, v_bits, k_mode, v_mode, k_axis, k_group, v_group;
+    int rotate;
+    float sm_log2;        // softmax scale * log2(e)
+    float rot_c;
+};
+// Split count over coded tokens for a cache of (B, H) units with nq coded tokens.
+void decode_plan(int B, int H, int nq, int* S_q, int* bps);
+// Upper bound of S_q over every coded-token count up to nq.
+int decode_split_bound(int B, int H, int nq);
+hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
+
+}  // namespace kvq

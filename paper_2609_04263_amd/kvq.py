@@ -1,0 +1,194 @@
+"""Thin ctypes binding of libkvq.so (the C ABI in include/kvq.h).
+
+Argument marshalling only: torch tensors provide device memory and the HIP
+stream; every step of the path runs in the library's HIP kernels.  Importing
+this module loads ``libkvq.so`` and raises if it is missing or cannot load
+(there is no CPU fallback).  Names follow the C ABI without the ``kvq_``
+prefix.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvq.so")
+
+FORMAT_FIELDS = ("k_bits", "v_bits", "k_mode", "v_mode", "k_axis", "v_axis",
+                 "k_group", "v_group", "residual", "flush", "rotate")
+
+OK, ERR_ARG, ERR_FORMAT, ERR_CAPACITY, ERR_WORKSPACE, ERR_DEVICE = range(6)
+
+
+class KvqError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {_lib.kvq_strerror(status).decode()} (status {status})")
+        self.status = status
+
+
+class Format(C.Structure):
+    _fields_ = [(name, C.c_int32) for name in FORMAT_FIELDS]
+
+    @classmethod
+    def of(cls, fmt) -> "Format":
+        if isinstance(fmt, Format):
+            return fmt
+        return cls(*[int(fmt[name]) for name in FORMAT_FIELDS])
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "(the HIP library is required, there is no fallback)")
+    L = C.CDLL(LIB_PATH)
+    P, I, S = C.c_void_p, C.c_int, C.c_size_t
+    Fp = C.POINTER(Format)
+    L.kvq_strerror.argtypes = [I]
+    L.kvq_strerror.restype = C.c_char_p
+    L.kvq_cache_bytes.argtypes = [Fp, I, I, I, I, C.POINTER(S)]
+    L.kvq_cache_init.argtypes = [Fp, I, I, I, I, P, S, C.POINTER(P)]
+    L.kvq_cache_section.argtypes = [P, I, C.POINTER(S), C.POINTER(S)]
+    L.kvq_cache_reset.argtypes = [P]
+    L.kvq_cache_len.argtypes = [P, C.POINTER(I), C.POINTER(I)]
+    L.kvq_cache_rewind.argtypes = [P, I]
+    L.kvq_cache_destroy.argtypes = [P]
+    L.kvq_cache_destroy.restype = None
+    L.kvq_project_workspace_bytes.argtypes = [I, I, C.POINTER(S)]
+    L.kvq_project_qkv.argtypes = [P, I, I, P, I, I, P, P, I, C.c_float, P, P, P, P, S, P]
+    L.kvq_append.argtypes = [P, P, P, I, Fp, P]
+    L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
+    L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
+    for name in ("kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section", "kvq_cache_reset",
+                 "kvq_cache_len", "kvq_cache_rewind", "kvq_project_workspace_bytes",
+                 "kvq_project_qkv", "kvq_append", "kvq_decode_workspace_bytes", "kvq_decode_attn"):
+        getattr(L, name).restype = I
+    return L
+
+
+_lib = _load()
+EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
+            "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_destroy",
+            "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_append",
+            "kvq_decode_workspace_bytes", "kvq_decode_attn")
+
+
+def lib() -> C.CDLL:
+    return _lib
+
+
+def _check(status: int, what: str) -> None:
+    if status != OK:
+        raise KvqError(status, what)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ------------------------------------------------------------------ cache
+
+def cache_bytes(fmt, B: int, H_kv: int, D: int, T_max: int) -> int:
+    out = C.c_size_t()
+    _check(_lib.kvq_cache_bytes(C.byref(Format.of(fmt)), B, H_kv, D, T_max, C.byref(out)), "cache_bytes")
+    return out.value
+
+
+class Cache:
+    """A packed cache: caller-owned device storage (a zero-filled uint8 torch
+    tensor) plus the library's host handle."""
+
+    def __init__(self, fmt, B: int, H_kv: int, D: int, T_max: int, device="cuda", storage=None):
+        self.fmt = Format.of(fmt)
+        self.B, self.H, self.D, self.T_max = B, H_kv, D, T_max
+        nbytes = cache_bytes(self.fmt, B, H_kv, D, T_max)
+        if storage is None:
+            storage = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+        self.storage = storage
+        h = C.c_void_p()
+        _check(_lib.kvq_cache_init(C.byref(self.fmt), B, H_kv, D, T_max, C.c_void_p(_ptr(storage)),
+                                   storage.numel() * storage.element_size(), C.byref(h)), "cache_init")
+        self.handle = h
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value and _lib is not None:
+            _lib.kvq_cache_destroy(h)
+            self.handle = None
+
+    def section(self, index: int):
+        off, ln = C.c_size_t(), C.c_size_t()
+        _check(_lib.kvq_cache_section(self.handle, index, C.byref(off), C.byref(ln)), "cache_section")
+        return off.value, ln.value
+
+    def reset(self) -> None:
+        _check(_lib.kvq_cache_reset(self.handle), "cache_reset")
+
+    def rewind(self, n: int) -> None:
+        _check(_lib.kvq_cache_rewind(self.handle, n), "cache_rewind")
+
+    def length(self):
+        n, nc = C.c_int(), C.c_int()
+        _check(_lib.kvq_cache_len(self.handle, C.byref(n), C.byref(nc)), "cache_len")
+        return n.value, nc.value
+
+    @property
+    def n(self) -> int:
+        return self.length()[0]
+
+    def append(self, K, V, n_new: int | None = None, fmt=None, stream=None) -> None:
+        """Append bf16 K, V [B, n_new, H_kv, D] (device tensors)."""
+        if n_new is None:
+            n_new = K.shape[1] if K.dim() == 4 else 1
+        f = self.fmt if fmt is None else Format.of(fmt)
+        _check(_lib.kvq_append(self.handle, C.c_void_p(_ptr(K)), C.c_void_p(_ptr(V)), n_new, C.byref(f),
+                               C.c_void_p(_stream(stream))), "append")
+
+    def decode_workspace_bytes(self, H_q: int) -> int:
+        out = C.c_size_t()
+        _check(_lib.kvq_decode_workspace_bytes(self.handle, H_q, C.byref(out)), "decode_workspace_bytes")
+        return out.value
+
+    def decode_workspace(self, H_q: int, device="cuda"):
+        """A zero-filled workspace of the required size (reuse it across calls)."""
+        return torch.zeros(self.decode_workspace_bytes(H_q), dtype=torch.uint8, device=device)
+
+    def decode_attn(self, Q, H_q: int, sm_scale: float, O, workspace, stream=None) -> None:
+        """O[B, H_q, D] (fp32) <- attention of bf16 Q[B, H_q, D] over the cache."""
+        nbytes = workspace.numel() * workspace.element_size()
+        _check(_lib.kvq_decode_attn(self.handle, C.c_void_p(_ptr(Q)), H_q, C.c_float(sm_scale),
+                                    C.c_void_p(_ptr(O)), C.c_void_p(_ptr(workspace)), nbytes,
+                                    C.c_void_p(_stream(stream))), "decode_attn")
+
+
+# ------------------------------------------------------------- projection
+
+def project_workspace_bytes(M: int, rank: int) -> int:
+    out = C.c_size_t()
+    _check(_lib.kvq_project_workspace_bytes(M, rank, C.byref(out)), "project_workspace_bytes")
+    return out.value
+
+
+def project_qkv(H, W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, Q, K, V, workspace,
+                stream=None) -> None:
+    """Q/K/V (bf16) <- H W^T + lora_scale * (H A_p^T) B_p^T per projection."""
+    M, d_in = H.shape[0], H.shape[-1]
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.kvq_project_qkv(C.c_void_p(_ptr(H)), M, d_in, C.c_void_p(_ptr(W)), d_q, d_kv,
+                                C.c_void_p(_ptr(A)), C.c_void_p(_ptr(Bm)), rank, C.c_float(lora_scale),
+                                C.c_void_p(_ptr(Q)), C.c_void_p(_ptr(K)), C.c_void_p(_ptr(V)),
+                                C.c_void_p(_ptr(workspace)), nbytes, C.c_void_p(_stream(stream))),
+           "project_qkv")

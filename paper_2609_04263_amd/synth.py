@@ -97,3 +97,16 @@ def kv_tokens(seed: int, B: int, n: int, H: int, D: int, outlier=("scale", 4, 20
 
 def queries(seed: int, B: int, H_q: int, D: int, name="q") -> np.ndarray:
     return normal_bf16(seed, ("q", name), (B, H_q, D))
+
+
+def normal_bf16_device(seed: int, name, shape, device="cuda", std: float = 1.0):
+    """Large ~N(0, std^2) bf16 tensors drawn directly on the device (torch's
+    Philox generator, seeded from the same SeedSequence keys); used for
+    benchmark inputs that the oracle never consumes."""
+    key = int(stream(seed, "device", name).integers(0, 2 ** 62))
+    g = torch.Generator(device=device)
+    g.manual_seed(key)
+    x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    if std != 1.0:
+        x *= std
+    return x.to(torch.bfloat16)

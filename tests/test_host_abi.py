@@ -1,0 +1,151 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+* libkvq.so loads and exports every function include/kvq.h declares;
+* the storage layout (total size and section offsets) matches the oracle's
+  for every workload and a spread of formats;
+* argument errors are reported before anything is enqueued and leave the
+  cache handle unchanged (fake, never-dereferenced device addresses).
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2609_04263_amd import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 1 << 32          # 256-aligned address that host code never dereferences
+
+
+@pytest.fixture(scope="module")
+def kvq():
+    from paper_2609_04263_amd import kvq as mod
+    return mod
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "kvq.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:kvq_status|void|const char\*)\s+(kvq_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(kvq):
+    names = declared_functions()
+    assert len(names) >= 13
+    for name in names:
+        assert hasattr(kvq.lib(), name), name
+    assert set(names) == set(kvq.EXPORTED)
+
+
+FORMATS = [wl.fmt for wl in configs.WORKLOADS.values()] + [
+    configs.make_format(2, 4, k_mode=1, k_group=32, v_group=128),
+    configs.make_format(4, 2, k_axis=1, k_group=32, v_group=64, residual=64, flush=64),
+    configs.make_format(4, 4, k_group=256, v_group=256),
+]
+
+
+@pytest.mark.parametrize("fi", range(len(FORMATS)))
+@pytest.mark.parametrize("dims", [(1, 1, 64, 1), (3, 2, 128, 77), (2, 5, 256, 300)])
+def test_layout_matches_oracle(kvq, fi, dims):
+    f = FORMATS[fi]
+    B, H, D, T = dims
+    if oracle.check_format(f, D) != 0:
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.cache_bytes(f, B, H, D, T)
+        assert e.value.status == kvq.ERR_FORMAT
+        return
+    off, ln, total = oracle.layout(f, B, H, D, T)
+    assert kvq.cache_bytes(f, B, H, D, T) == total
+    c = kvq.Cache(f, B, H, D, T, storage=FakeStorage(total))
+    for i in range(8):
+        assert c.section(i) == (off[i], ln[i])
+
+
+class FakeStorage:
+    """Stands in for a device tensor on hosts without a GPU."""
+
+    def __init__(self, nbytes, addr=FAKE):
+        self.nbytes, self.addr = nbytes, addr
+
+    def data_ptr(self):
+        return self.addr
+
+    def numel(self):
+        return self.nbytes
+
+    def element_size(self):
+        return 1
+
+
+def test_errors_leave_cache_unchanged(kvq):
+    f = configs.make_format(4, 4, k_group=64, v_group=64)
+    B, H, D, T = 2, 2, 64, 40
+    c = kvq.Cache(f, B, H, D, T, storage=FakeStorage(kvq.cache_bytes(f, B, H, D, T)))
+    assert c.length() == (0, 0)
+    fake_k = FakeStorage(0, FAKE + (1 << 30))
+    # capacity
+    with pytest.raises(kvq.KvqError) as e:
+        c.append(fake_k, fake_k, n_new=41, stream=0)
+    assert e.value.status == kvq.ERR_CAPACITY and c.length() == (0, 0)
+    # format mismatch
+    with pytest.raises(kvq.KvqError) as e:
+        c.append(fake_k, fake_k, n_new=1, fmt=dict(f, k_bits=2), stream=0)
+    assert e.value.status == kvq.ERR_FORMAT and c.length() == (0, 0)
+    # misaligned input
+    with pytest.raises(kvq.KvqError) as e:
+        c.append(FakeStorage(0, FAKE + 8), fake_k, n_new=1, stream=0)
+    assert e.value.status == kvq.ERR_ARG and c.length() == (0, 0)
+    # empty append is a no-op
+    c.append(fake_k, fake_k, n_new=0, stream=0)
+    assert c.length() == (0, 0)
+    # empty cache cannot be attended
+    with pytest.raises(kvq.KvqError) as e:
+        c.decode_attn(fake_k, 8, 0.125, fake_k, FakeStorage(1 << 20), stream=0)
+    assert e.value.status == kvq.ERR_ARG
+    # bad head grouping
+    assert c.decode_workspace_bytes(8) > 0
+    for bad in (3, 2 * 17 + 1, 2 * 17):
+        with pytest.raises(kvq.KvqError):
+            c.decode_workspace_bytes(bad)
+
+
+def test_rewind_only_without_window(kvq):
+    f = configs.WORKLOADS["llama8b_kivi"].fmt
+    c = kvq.Cache(f, 1, 1, 128, 64, storage=FakeStorage(kvq.cache_bytes(f, 1, 1, 128, 64)))
+    with pytest.raises(kvq.KvqError) as e:
+        c.rewind(0)
+    assert e.value.status == kvq.ERR_FORMAT
+
+
+def test_init_rejects_small_or_misaligned_storage(kvq):
+    f = configs.make_format()
+    n = kvq.cache_bytes(f, 1, 1, 64, 32)
+    with pytest.raises(kvq.KvqError):
+        kvq.Cache(f, 1, 1, 64, 32, storage=FakeStorage(n - 1))
+    with pytest.raises(kvq.KvqError):
+        kvq.Cache(f, 1, 1, 64, 32, storage=FakeStorage(n, FAKE + 128))
+
+
+def test_projection_argument_checks(kvq):
+    p = FakeStorage(0, FAKE)
+    ws_small = FakeStorage(4, FAKE)
+    # d_in must be a multiple of 64
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.project_qkv(_Shape(4, 96), p, p, p, 8, 2.0, 64, 64, p, p, p, ws_small, stream=0)
+    assert e.value.status == kvq.ERR_ARG
+    # rank above 64
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.project_qkv(_Shape(4, 128), p, p, p, 65, 2.0, 64, 64, p, p, p, ws_small, stream=0)
+    assert e.value.status == kvq.ERR_ARG
+    # workspace too small for M x 3r fp32
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.project_qkv(_Shape(4, 128), p, p, p, 8, 2.0, 64, 64, p, p, p, ws_small, stream=0)
+    assert e.value.status == kvq.ERR_WORKSPACE
+    assert kvq.project_workspace_bytes(4, 8) == 4 * 24 * 4
+
+
+class _Shape(FakeStorage):
+    def __init__(self, M, d_in):
+        super().__init__(0, FAKE)
+        self.shape = (M, d_in)
