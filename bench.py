@@ -1,0 +1,282 @@
+"""Benchmark of the packed low-bit KV-cache decode path on one MI355X.
+
+One step = one decode token per sequence through the whole hot path:
+  1. adapted Q/K/V projection of the B new hidden states (Eq. (1)-(2)),
+  2. quantize-and-pack append of the new K/V into the packed cache,
+  3. decode attention over the in-kernel reconstruction of all cached tokens
+     (Hadamard rotation of q and the output where the format rotates).
+The cache is first filled to the workload's context with the same kernels
+(prefill projection in chunks, then append).  Inputs are synthetic, seeded
+and resident in HBM before the timed region.
+
+Output: one JSON line.  ``value`` is decoded tokens per second (B tokens per
+step).  ``roofline`` reports the decode-attention kernel: algorithmic bytes
+per launch (packed codes + fp32 metadata + fp16 window + bf16 q + fp32 o)
+over its mean duration, measured with HIP events around each launch inside
+the timed region, against MI355X's 8 TB/s HBM peak.  ``cpu_baseline`` times
+the CPU oracle (single thread) on a bounded sample of decode steps.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+  python bench.py --phase prefill [--workload gqa12b_b8]   (projection GEMM, MFMA roofline)
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "packed-cache decode attn tokens/s + achieved HBM GB/s (% peak) per config"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+DEFAULT_WORKLOAD = "tiny_b16"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's decode steps)")
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--phase", choices=["decode", "prefill"], default="decode")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=None)
+    return ap.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("attn.hip", "kvq_device.h", "kvq_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_04263_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the decode-attention kernel from the committed
+    rocprofv3 counter summary, or None when it is missing or was taken on a
+    different version of the kernel source."""
+    path = os.path.join(ROOT, "profiles", f"decode_attn_{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    src = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not src or not val or src.group(1) != kernel_source_hash():
+        return None
+    return float(val.group(1))
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "the decode path shards over (sequence, KV head) units with no exchange; "
+              "multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import __graft_entry__
+    __graft_entry__._ensure_built()
+    from paper_2609_04263_amd import configs, kvq, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    wl = configs.WORKLOADS[args.workload]
+    B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
+
+    def bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    W, A, Bm = (bf16(x) for x in synth.layer_weights(wl))
+
+    def alloc_proj(M):
+        return (torch.empty((M, wl.d_q), dtype=torch.bfloat16, device=dev),
+                torch.empty((M, wl.d_kv), dtype=torch.bfloat16, device=dev),
+                torch.empty((M, wl.d_kv), dtype=torch.bfloat16, device=dev),
+                torch.empty(max(16, kvq.project_workspace_bytes(M, wl.rank)), dtype=torch.uint8, device=dev))
+
+    if args.phase == "prefill":
+        return bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch)
+
+    # ---------------------------------------------------------------- setup
+    T_max = wl.context + wl.decode_steps
+    cache = kvq.Cache(wl.fmt, B, Hkv, D, T_max, device=dev)
+    chunk = min(wl.chunk, wl.context)
+    Qp, Kp, Vp, wsp = alloc_proj(B * chunk)
+    done = 0
+    while done < wl.context:
+        c = min(chunk, wl.context - done)
+        Hc = synth.normal_bf16_device(wl.seed, ("prefill", done), (B * c, wl.d_in), device=dev)
+        kvq.project_qkv(Hc, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv,
+                        Qp[:B * c], Kp[:B * c], Vp[:B * c], wsp)
+        cache.append(Kp[:B * c].view(B, c, Hkv, D), Vp[:B * c].view(B, c, Hkv, D))
+        done += c
+    del Qp, Kp, Vp, wsp
+    snapshot = cache.storage.clone() if wl.fmt["flush"] else None
+    Hdec = synth.normal_bf16_device(wl.seed, "decode", (wl.decode_steps, B, wl.d_in), device=dev)
+    Qd, Kd, Vd, wsd = alloc_proj(B)
+    O = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    wsa = cache.decode_workspace(Hq, device=dev)
+    sm = 1.0 / float(np.sqrt(D))
+    torch.cuda.synchronize()
+
+    def restart(timed=False):
+        if snapshot is None:
+            cache.rewind(wl.context)          # host-only: no GPU work
+        elif timed:
+            raise RuntimeError("windowed formats restart only outside the timed region")
+        else:
+            cache.storage.copy_(snapshot)
+            cache.restore(wl.context)
+
+    def step(i, ev=None):
+        kvq.project_qkv(Hdec[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
+        cache.append(Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D))
+        if ev is not None:
+            ev[0].record()
+        cache.decode_attn(Qd.view(B, Hq, D), Hq, sm, O, wsa)
+        if ev is not None:
+            ev[1].record()
+
+    steps = args.steps if args.steps is not None else wl.decode_steps
+    if snapshot is not None and steps > wl.decode_steps:
+        steps = wl.decode_steps  # the fp16 window cannot be rewound in place
+    for i in range(args.warmup):
+        if i % wl.decode_steps == 0 and i:
+            restart()
+        step(i % wl.decode_steps)
+    torch.cuda.synchronize()
+    if snapshot is not None:
+        cache.storage.copy_(snapshot)
+        cache.restore(wl.context)
+    else:
+        cache.rewind(wl.context)
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    n_at = []
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        j = i % wl.decode_steps
+        if j == 0 and i:
+            restart(timed=True)
+        n_at.append(wl.context + j + 1)
+        step(j, events[i])
+    t1.record()
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    attn_ms = np.array([a.elapsed_time(b) for a, b in events])
+    bytes_launch = np.array([configs.attention_bytes(wl, n) for n in n_at], dtype=np.float64)
+    achieved = bytes_launch.mean() / (attn_ms.mean() * 1e-3) / 1e9
+    traffic = measured_traffic(wl.name)
+
+    result = {
+        "metric": METRIC,
+        "value": B * steps / (total_ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u%d/f16" % wl.fmt["k_bits"],
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "H_q": Hq, "H_kv": Hkv, "head_dim": D, "d_in": wl.d_in,
+                   "rank": wl.rank, "context": wl.context, "decode_steps": wl.decode_steps,
+                   "format": wl.fmt, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "kernel": "decode attention", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "bytes_per_launch": float(bytes_launch.mean()),
+                     "us_per_launch": float(attn_ms.mean() * 1e3)},
+        "attention_us_per_step": float(attn_ms.mean() * 1e3),
+    }
+    if not args.no_cpu_baseline:
+        if snapshot is None:
+            cache.rewind(wl.context)
+            torch.cuda.synchronize()
+            image = cache.storage.cpu().numpy()
+        else:
+            image = snapshot.cpu().numpy()
+        result["cpu_baseline"] = cpu_baseline(wl, image, args, np, synth)
+    print(json.dumps(result))
+
+
+def cpu_baseline(wl, image, args, np, synth):
+    """The oracle (single-threaded C) on a bounded sample of the same
+    workload: starting from the GPU-filled cache image at the context length,
+    it runs S decode steps (projection of the B new tokens, append, attention
+    over all cached tokens), timed end to end.  S is chosen from a first
+    timed step so the sample takes about 15 s."""
+    import oracle
+
+    W, A, Bm = synth.layer_weights(wl)
+    ref = oracle.Cache(wl.fmt, wl.B, wl.H_kv, wl.D, wl.T_max)
+    ref.image[:] = image
+    ref.n = wl.context
+
+    def one(i):
+        H = synth.hidden(wl, ("cpu-sample", i), wl.B)
+        _, yb = oracle.project(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv)
+        q = yb[:, :wl.d_q].reshape(wl.B, wl.H_q, wl.D)
+        k = yb[:, wl.d_q:wl.d_q + wl.d_kv].reshape(wl.B, 1, wl.H_kv, wl.D)
+        v = yb[:, wl.d_q + wl.d_kv:].reshape(wl.B, 1, wl.H_kv, wl.D)
+        ref.append(k, v)
+        ref.decode_attn(q, 1.0 / np.sqrt(wl.D))
+
+    t = time.perf_counter()
+    one(0)
+    first = time.perf_counter() - t
+    S = args.cpu_sample_steps or int(min(max(15.0 / max(first, 1e-3), 2), wl.decode_steps))
+    t = time.perf_counter()
+    for i in range(1, S + 1):
+        one(i)
+    el = time.perf_counter() - t
+    return {"value": wl.B * S / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{S} decode steps of {wl.name} (B={wl.B}, from context {wl.context}): oracle projection, "
+                      f"append and fp64 attention, single thread, {el:.1f} s"}
+
+
+def bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch):
+    """Projection GEMM at the prefill chunk (M = B * chunk rows): MFMA roofline."""
+    M = wl.B * wl.chunk
+    Q, K, V, ws = alloc_proj(M)
+    H = synth.normal_bf16_device(wl.seed, "prefill-bench", (M, wl.d_in), device=dev)
+    for _ in range(args.warmup):
+        kvq.project_qkv(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Q, K, V, ws)
+    steps = args.steps or 20
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        kvq.project_qkv(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Q, K, V, ws)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    flops = configs.projection_flops(M, wl.d_in, wl.d_q, wl.d_kv, wl.rank)
+    tflops = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "adapted QKV projection (prefill chunk) TFLOP/s", "value": tflops, "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "M": M, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / BF16_PEAK_TFLOPS, "traffic": None},
+    }))
+
+
+if __name__ == "__main__":
+    main()

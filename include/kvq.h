@@ -111,6 +111,13 @@ kvq_status kvq_cache_len(const kvq_cache* cache, int* n, int* n_coded);
  * are unchanged by later appends; otherwise KVQ_ERR_FORMAT. */
 kvq_status kvq_cache_rewind(kvq_cache* cache, int n_new);
 
+/* Set the length to n (0 <= n <= T_max) after the caller has made the
+ * storage hold the image this cache had at length n, for example by copying
+ * back a snapshot of the storage taken then (the fp16 window of formats that
+ * have one is only consistent with such a snapshot).  The bytes are not
+ * checked.  Host-only. */
+kvq_status kvq_cache_restore(kvq_cache* cache, int n);
+
 /* Free the host handle (not the storage). */
 void kvq_cache_destroy(kvq_cache* cache);
 
@@ -145,10 +152,8 @@ kvq_status kvq_append(kvq_cache* cache, const void* K, const void* V, int n_new,
                       const kvq_format* fmt, void* stream);
 
 /* Workspace bytes kvq_decode_attn needs for H_q query heads at any length
- * up to the cache's T_max: split-K partial results plus one arrival counter
- * per KV head.  The workspace must be ZERO-FILLED before its first use and
- * left untouched by the caller between calls: every call returns the
- * counters to zero.  Calls that share a workspace must not overlap. */
+ * up to the cache's T_max (split-K partial results; contents need no
+ * initialization).  Calls that share a workspace must not overlap. */
 kvq_status kvq_decode_workspace_bytes(const kvq_cache* cache, int H_q, size_t* bytes);
 
 /* Decode attention for one new query per sequence over the reconstructed

@@ -20,11 +20,11 @@
 // packed fp16 subtract, so every product in the MFMAs is exact and the
 // accumulation is fp32.  Tokens of the fp16 window (KIVI) are handled by one
 // extra split per KV head that feeds the fp16 values to the same MFMAs.  Each
-// split writes an unnormalized partial (m, l, o) to the workspace and counts
-// itself in a per-KV-head counter; the last split to arrive merges the
-// partials, divides by the softmax sum, applies the inverse rotation, writes
-// the outputs and resets the counter.  With a single split the partial is
-// skipped.
+// split writes an unnormalized partial (m, l, o) to the workspace and a
+// second kernel merges them (a kernel boundary instead of an in-kernel
+// cross-workgroup handoff, whose agent-scope fences write back and
+// invalidate the whole L2 on gfx950).  With a single split the first kernel
+// writes the outputs itself.
 
 #include "kvq_device.h"
 #include "kvq_internal.h"
@@ -46,16 +46,106 @@ __device__ __forceinline__ uint32_t key_code_word(const uint32_t* row, int kb, i
 }
 
 template <int BITS>
-__device__ __forceinline__ uint32_t value_code_word(const uint32_t* vc_unit, int T, int D, int t8, int d)
+__device__ __forceinline__ uint32_t value_code_word(const uint32_t* vc, int D, int t8, int d)
 {
-    // Eight codes along tokens: t = t8 .. t8 + 7 (t8 a multiple of 8), channel d.
+    // Eight codes along tokens: t = t8 .. t8 + 7 (t8 a multiple of 8, relative
+    // to a 32-token-aligned base), channel d.
     if (BITS == 4)
-        return vc_unit[(size_t)(t8 >> 3) * D + d];
-    return vc_unit[(size_t)(t8 >> 4) * D + d] >> (16 * ((t8 >> 3) & 1));
+        return vc[(t8 >> 3) * D + d];
+    return vc[(t8 >> 4) * D + d] >> (16 * ((t8 >> 3) & 1));
+}
+
+// Bytes one 32-token block of coded tokens occupies in the LDS stage:
+// key codes, key scales (+ offsets), value codes, value scales (+ offsets).
+struct BlockBytes {
+    int kc, ks, kz, vc, vs, vz;
+    __host__ __device__ int total() const { return kc + ks + kz + vc + vs + vz; }
+};
+
+__host__ __device__ inline BlockBytes block_bytes(int D, int k_bits, int v_bits, int k_axis, int k_group,
+                                                  int v_group, int k_mode, int v_mode)
+{
+    BlockBytes r;
+    r.kc = 32 * (D * k_bits / 32) * 4;
+    r.ks = k_axis == KVQ_PER_TOKEN ? 32 * (D / k_group) * 4 : D * 4;
+    r.kz = k_mode == KVQ_AFFINE ? r.ks : 0;
+    r.vc = v_bits * D * 4;
+    r.vs = 32 * (D / v_group) * 4;
+    r.vz = v_mode == KVQ_AFFINE ? r.vs : 0;
+    return r;
+}
+
+// Up to six contiguous 16-byte-aligned chunks copied from global memory
+// into LDS by the whole workgroup: chunk k has n_k 16-byte units read from
+// src_k and written consecutively from LDS 16-byte index o_k = n_0 + ... +
+// n_(k-1).  issue() starts every load of a thread (kStageLoads 16-byte
+// loads, enough for kStageBytes) before any is used, so a split pays one
+// memory round trip; commit() writes them to LDS.
+constexpr int kStageBytes = 64 * 1024;
+constexpr int kStageLoads = kStageBytes / (16 * kThreads);
+
+struct Chunks {
+    const u32x4* src[6];
+    int end[6];  // cumulative 16-byte counts
+};
+
+struct Stager {
+    u32x4 r[kStageLoads];
+
+    __device__ __forceinline__ void issue(const Chunks& c)
+    {
+#pragma unroll
+        for (int u = 0; u < kStageLoads; ++u) {
+            const int idx = u * kThreads + (int)threadIdx.x;
+            if (idx < c.end[5]) {
+                const u32x4* src;
+                int off;
+                if (idx < c.end[0]) { src = c.src[0]; off = idx; }
+                else if (idx < c.end[1]) { src = c.src[1]; off = idx - c.end[0]; }
+                else if (idx < c.end[2]) { src = c.src[2]; off = idx - c.end[1]; }
+                else if (idx < c.end[3]) { src = c.src[3]; off = idx - c.end[2]; }
+                else if (idx < c.end[4]) { src = c.src[4]; off = idx - c.end[3]; }
+                else { src = c.src[5]; off = idx - c.end[4]; }
+                r[u] = src[off];
+            }
+        }
+    }
+
+    __device__ __forceinline__ void commit(const Chunks& c, u32x4* lds16)
+    {
+#pragma unroll
+        for (int u = 0; u < kStageLoads; ++u) {
+            const int idx = u * kThreads + (int)threadIdx.x;
+            if (idx < c.end[5])
+                lds16[idx] = r[u];
+        }
+    }
+};
+
+// Inverse rotation (the normalized transform is its own inverse) of G rows
+// of D outputs staged in LDS, then the store to O.
+template <int D>
+__device__ __forceinline__ void finish_rows(const AttnParams& p, float* xo, size_t row0, int G)
+{
+    if (p.rotate) {
+        for (int h = 1; h < D; h <<= 1) {
+            for (int idx = threadIdx.x; idx < G * (D / 2); idx += kThreads) {
+                int r = idx / (D / 2), k = idx % (D / 2);
+                int jj = (k / h) * 2 * h + (k % h);
+                float a = xo[r * D + jj], c = xo[r * D + jj + h];
+                xo[r * D + jj] = a + c;
+                xo[r * D + jj + h] = a - c;
+            }
+            __syncthreads();
+        }
+    }
+    const float post = p.rotate ? p.rot_c : 1.0f;
+    for (int idx = threadIdx.x; idx < G * D; idx += kThreads)
+        p.out[row0 * D + idx] = xo[idx] * post;
 }
 
 template <int D, int KBITS, int VBITS, bool PERCH>
-__device__ void run_split(const AttnParams& p, float* lds)
+__device__ __forceinline__ void run_split(const AttnParams& p, float* lds)
 {
     constexpr int NKB = D / 32;   // 32-wide K-blocks of the score MFMA
     constexpr int NMB = D / 16;   // 16-row M-blocks of the value MFMA
@@ -65,64 +155,7 @@ __device__ void run_split(const AttnParams& p, float* lds)
     const int b = unit / p.H, j = unit % p.H;
     const bool ring_split = p.ring && split == p.S_q;
 
-    // ---- queries: stage [16][D] fp32 (heads >= G zero), rotate if needed
-    for (int idx = threadIdx.x; idx < 16 * D; idx += kThreads) {
-        int h = idx / D, d = idx % D;
-        float v = 0.0f;
-        if (h < p.G)
-            v = bf16_to_f32(p.q[((size_t)b * p.H_q + (size_t)j * p.G + h) * D + d]);
-        lds[idx] = v;
-    }
-    __syncthreads();
-    if (p.rotate) {
-        for (int h = 1; h < D; h <<= 1) {
-            for (int idx = threadIdx.x; idx < 16 * (D / 2); idx += kThreads) {
-                int row = idx / (D / 2), k = idx % (D / 2);
-                int jj = (k / h) * 2 * h + (k % h);
-                float a = lds[row * D + jj], c = lds[row * D + jj + h];
-                lds[row * D + jj] = a + c;
-                lds[row * D + jj + h] = a - c;
-            }
-            __syncthreads();
-        }
-        for (int idx = threadIdx.x; idx < 16 * D; idx += kThreads)
-            lds[idx] *= p.rot_c;
-        __syncthreads();
-    }
-    // Query operand per K-block: fp16 hi part (exact for bf16 queries) and,
-    // when the query is not bf16 (rotated), the fp16 remainder as a lo part.
-    const bool qlo = p.rotate != 0;
-    float qf[NKB][8];      // fp32 query elements of this lane, operand order
-    half8 qhi[NKB], qlop[NKB];
-    float qsum[NKB];       // sum of the 32 query elements of K-block kb (head hh)
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-        float part = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            qf[kb][e] = lds[hh * D + 32 * kb + 8 * qg + perm4(e)];
-            part += qf[kb][e];
-        }
-        split_half8(qf[kb], &qhi[kb], &qlop[kb]);
-        qsum[kb] = xor_sum16_32(part);
-    }
-    __syncthreads();  // lds is reused below
-
-    const int T = p.T;
-    const uint32_t* kc_unit = p.kc + (size_t)unit * T * (D * KBITS / 32);
-    const uint32_t* vc_unit = p.vc + (size_t)unit * (T * VBITS / 32) * D;
-    const int kng = D / p.k_group, vng = D / p.v_group;
-    const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
-    const _Float16 kb16 = (_Float16)(1024 + (kaff ? 0 : (1 << (KBITS - 1))));
-    const _Float16 vb16 = (_Float16)(1024 + (vaff ? 0 : (1 << (VBITS - 1))));
-    const half2_t kbias = {kb16, kb16}, vbias = {vb16, vb16};
-
-    float m = kNegInf, lsum = 0.0f;
-    floatx4 oacc[NMB];
-#pragma unroll
-    for (int mb = 0; mb < NMB; ++mb)
-        oacc[mb] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-
+    // ---- split range
     int t_begin, t_end, blk_begin, blk_end;
     if (ring_split) {
         t_begin = p.nq;
@@ -136,6 +169,113 @@ __device__ void run_split(const AttnParams& p, float* lds)
         blk_begin = split * p.bps;
         blk_end = min(nblk, blk_begin + p.bps);
     }
+    const int T = p.T;
+    constexpr int WPT = D * KBITS / 32;  // key code words per token
+    const int kng = D / p.k_group, vng = D / p.v_group;
+    const int ta = 32 * blk_begin;  // first token of the split
+
+    // ---- LDS: [stage of the split's coded tokens][queries fp32 16 x D]
+    const BlockBytes bb = block_bytes(D, KBITS, VBITS, PERCH ? KVQ_PER_CHANNEL : KVQ_PER_TOKEN, p.k_group,
+                                      p.v_group, p.k_mode, p.v_mode);
+    const int nb = ring_split ? 0 : blk_end - blk_begin;
+    uint8_t* stage = (uint8_t*)lds;
+    const uint32_t* lkc = (const uint32_t*)stage;
+    const float* lks = (const float*)(stage + nb * bb.kc);
+    const float* lkz = (const float*)(stage + nb * (bb.kc + bb.ks));
+    const uint32_t* lvc = (const uint32_t*)(stage + nb * (bb.kc + bb.ks + bb.kz));
+    const float* lvs = (const float*)(stage + nb * (bb.kc + bb.ks + bb.kz + bb.vc));
+    const float* lvz = (const float*)(stage + nb * (bb.kc + bb.ks + bb.kz + bb.vc + bb.vs));
+    float* lq = (float*)(stage + p.q_lds_offset);
+
+    // ---- one round of loads: queries (8 bf16 per 16-byte load) + the stage
+    constexpr int QPIECES = 16 * D / 8;
+    constexpr int QLOADS = (QPIECES + kThreads - 1) / kThreads;
+    u32x4 qraw[QLOADS];
+#pragma unroll
+    for (int u = 0; u < QLOADS; ++u) {
+        const int piece = u * kThreads + (int)threadIdx.x, row = piece / (D / 8);
+        qraw[u] = u32x4{0u, 0u, 0u, 0u};
+        if (piece < QPIECES && row < p.G)
+            qraw[u] = *(const u32x4*)(p.q + ((size_t)b * p.H_q + (size_t)j * p.G + row) * D + (piece % (D / 8)) * 8);
+    }
+    Stager st;
+    Chunks ch;
+    if (!ring_split) {
+        const size_t kmeta = PERCH ? ((size_t)unit * (T / 32) + blk_begin) * D : ((size_t)unit * T + ta) * kng;
+        ch.src[0] = (const u32x4*)(p.kc + ((size_t)unit * T + ta) * WPT);
+        ch.src[1] = (const u32x4*)(p.ks + kmeta);
+        ch.src[2] = (const u32x4*)(p.kz + kmeta);
+        ch.src[3] = (const u32x4*)(p.vc + ((size_t)unit * (T * VBITS / 32) + ta * VBITS / 32) * D);
+        ch.src[4] = (const u32x4*)(p.vs + ((size_t)unit * T + ta) * vng);
+        ch.src[5] = (const u32x4*)(p.vz + ((size_t)unit * T + ta) * vng);
+        ch.end[0] = nb * bb.kc / 16;
+        ch.end[1] = ch.end[0] + nb * bb.ks / 16;
+        ch.end[2] = ch.end[1] + nb * bb.kz / 16;
+        ch.end[3] = ch.end[2] + nb * bb.vc / 16;
+        ch.end[4] = ch.end[3] + nb * bb.vs / 16;
+        ch.end[5] = ch.end[4] + nb * bb.vz / 16;
+        st.issue(ch);
+    }
+#pragma unroll
+    for (int u = 0; u < QLOADS; ++u) {
+        const int piece = u * kThreads + (int)threadIdx.x;
+        if (piece < QPIECES) {
+            const uint32_t w[4] = {qraw[u].x, qraw[u].y, qraw[u].z, qraw[u].w};
+            float* dst = lq + piece * 8;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                dst[2 * e] = __uint_as_float(w[e] << 16);
+                dst[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+            }
+        }
+    }
+    if (!ring_split)
+        st.commit(ch, (u32x4*)stage);
+    __syncthreads();
+    if (p.rotate) {
+        for (int h = 1; h < D; h <<= 1) {
+            for (int idx = threadIdx.x; idx < 16 * (D / 2); idx += kThreads) {
+                int row = idx / (D / 2), k = idx % (D / 2);
+                int jj = (k / h) * 2 * h + (k % h);
+                float a = lq[row * D + jj], c = lq[row * D + jj + h];
+                lq[row * D + jj] = a + c;
+                lq[row * D + jj + h] = a - c;
+            }
+            __syncthreads();
+        }
+        for (int idx = threadIdx.x; idx < 16 * D; idx += kThreads)
+            lq[idx] *= p.rot_c;
+        __syncthreads();
+    }
+    // Query operand per K-block: fp16 hi part (exact for bf16 queries) and,
+    // when the query is not bf16 (rotated), the fp16 remainder as a lo part.
+    const bool qlo = p.rotate != 0;
+    float qf[NKB][8];      // fp32 query elements of this lane, operand order
+    half8 qhi[NKB], qlop[NKB];
+    float qsum[NKB];       // sum of the 32 query elements of K-block kb (head hh)
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+        float part = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            qf[kb][e] = lq[hh * D + 32 * kb + 8 * qg + perm4(e)];
+            part += qf[kb][e];
+        }
+        split_half8(qf[kb], &qhi[kb], &qlop[kb]);
+        qsum[kb] = xor_sum16_32(part);
+    }
+
+    const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
+    const _Float16 kb16 = (_Float16)(1024 + (kaff ? 0 : (1 << (KBITS - 1))));
+    const _Float16 vb16 = (_Float16)(1024 + (vaff ? 0 : (1 << (VBITS - 1))));
+    const half2_t kbias = {kb16, kb16}, vbias = {vb16, vb16};
+
+    float m = kNegInf, lsum = 0.0f;
+    floatx4 oacc[NMB];
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb)
+        oacc[mb] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
 
     for (int blk = blk_begin + wave; blk < blk_end; blk += kWaves) {
         const int t0 = t_begin + 32 * blk;
@@ -169,8 +309,8 @@ __device__ void run_split(const AttnParams& p, float* lds)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 int tA = t0 + 8 * (hh >> 2) + 4 * h2 + (hh & 3);
-                const uint32_t* krow = kc_unit + (size_t)tA * (D * KBITS / 32);
-                const int tS = t0 + 8 * qg + 4 * h2;  // tokens of this lane's outputs: tS + i
+                const uint32_t* krow = lkc + (tA - ta) * WPT;
+                const int tS = t0 + 8 * qg + 4 * h2 - ta;  // split-relative tokens of this lane's outputs: tS + i
                 floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
                 floatx4 Sacc = {0.0f, 0.0f, 0.0f, 0.0f};
                 float qs = 0.0f;
@@ -185,11 +325,11 @@ __device__ void run_split(const AttnParams& p, float* lds)
                         int g = (32 * kb) / p.k_group;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
-                            size_t mi = ((size_t)unit * T + tS + i) * kng + g;
-                            float s = p.ks[mi];
+                            int mi = (tS + i) * kng + g;
+                            float s = lks[mi];
                             Sacc[i] += s * acc[i];
                             if (kaff)
-                                Sacc[i] += p.kz[mi] * qs;
+                                Sacc[i] += lkz[mi] * qs;
                         }
                         acc = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
                         qs = 0.0f;
@@ -201,7 +341,7 @@ __device__ void run_split(const AttnParams& p, float* lds)
             // Per-channel keys: one 32-token group per block; the channel
             // scale folds into the query operand (hi + lo fp16 parts) and the
             // offsets give one constant per head: sum_d q_d z_d.
-            const size_t meta = ((size_t)unit * (T / 32) + (size_t)(t0 / 32)) * D;
+            const int meta = (blk - blk_begin) * D;
             half8 qkh[NKB], qkl[NKB];
             float c2 = 0.0f;
 #pragma unroll
@@ -210,9 +350,9 @@ __device__ void run_split(const AttnParams& p, float* lds)
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     int d = 32 * kb + 8 * qg + perm4(e);
-                    qs[e] = qf[kb][e] * p.ks[meta + d];
+                    qs[e] = qf[kb][e] * lks[meta + d];
                     if (kaff)
-                        c2 += qf[kb][e] * p.kz[meta + d];
+                        c2 += qf[kb][e] * lkz[meta + d];
                 }
                 split_half8(qs, &qkh[kb], &qkl[kb]);
             }
@@ -220,7 +360,7 @@ __device__ void run_split(const AttnParams& p, float* lds)
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 int tA = t0 + 8 * (hh >> 2) + 4 * h2 + (hh & 3);
-                const uint32_t* krow = kc_unit + (size_t)tA * (D * KBITS / 32);
+                const uint32_t* krow = lkc + (tA - ta) * WPT;
                 floatx4 acc = {zq, zq, zq, zq};
 #pragma unroll
                 for (int kb = 0; kb < NKB; ++kb) {
@@ -284,7 +424,7 @@ __device__ void run_split(const AttnParams& p, float* lds)
             }
         } else {
             // O^T[d][h] += sum_t c[t][d] (p_t s_t) + sum_t p_t z_t, per V group.
-            const int t8 = t0 + 8 * qg;
+            const int t8 = t0 + 8 * qg - ta;  // split-relative
             half8 ph, pl;
             float zp = 0.0f;
 #pragma unroll
@@ -295,10 +435,10 @@ __device__ void run_split(const AttnParams& p, float* lds)
                     float c2 = 0.0f;
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        size_t mi = ((size_t)unit * T + t8 + k) * vng + g;
-                        pv[k] = pr[k] * p.vs[mi];
+                        int mi = (t8 + k) * vng + g;
+                        pv[k] = pr[k] * lvs[mi];
                         if (vaff)
-                            c2 += pr[k] * p.vz[mi];
+                            c2 += pr[k] * lvz[mi];
                     }
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
@@ -307,7 +447,7 @@ __device__ void run_split(const AttnParams& p, float* lds)
                     zp = vaff ? xor_sum16_32(c2) : 0.0f;
                 }
                 int d = 16 * mb + hh;
-                half8 a = codes_to_half8<VBITS>(value_code_word<VBITS>(vc_unit, T, D, t8, d), vbias);
+                half8 a = codes_to_half8<VBITS>(value_code_word<VBITS>(lvc, D, t8, d), vbias);
                 oacc[mb] = mfma16(a, ph, oacc[mb]);
                 oacc[mb] = mfma16(a, pl, oacc[mb]);
                 if (vaff)
@@ -325,8 +465,7 @@ __device__ void run_split(const AttnParams& p, float* lds)
     float* lm = lds;                       // [4][16] running max per wave and head
     float* ll = lds + kWaves * 16;         // [4][16] softmax sums
     float* lo = lds + 2 * kWaves * 16;     // [4][G][D] unnormalized outputs
-    float* xo = lo + (size_t)kWaves * G * D;  // [G][D] this workgroup's result
-    int* flag = (int*)(xo + (size_t)G * D);
+    float* xo = lo;  // [G][D] result: element idx is written after its own four reads
     if (qg == 0) {
         lm[wave * 16 + hh] = m;
         ll[wave * 16 + hh] = lsum;
@@ -365,57 +504,10 @@ __device__ void run_split(const AttnParams& p, float* lds)
             }
         }
     }
-    if (!single) {
-        // Publish this split's partial; the last split of the KV head to
-        // arrive merges all of them (no workgroup ever waits for another).
-        __threadfence();
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            unsigned prev = atomicAdd(&p.counters[unit], 1u);
-            *flag = prev == (unsigned)(p.S_tot - 1);
-        }
-        __syncthreads();
-        if (!*flag)
-            return;
-        __threadfence();
-        for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
-            int h = idx / D, d = idx % D;
-            size_t row = row0 + h;
-            const float* ml = p.part_ml + row * p.S_tot * 2;
-            float M = kNegInf;
-            for (int s = 0; s < p.S_tot; ++s)
-                M = fmaxf(M, ml[2 * s]);
-            float acc = 0.0f, L = 0.0f;
-            for (int s = 0; s < p.S_tot; ++s) {
-                float ms = ml[2 * s];
-                if (ms == kNegInf)
-                    continue;
-                float sc = fast_exp2(ms - M);
-                L += sc * ml[2 * s + 1];
-                acc += sc * p.part_o[(row * p.S_tot + s) * D + d];
-            }
-            xo[idx] = acc / L;
-        }
-        if (threadIdx.x == 0)
-            p.counters[unit] = 0u;  // ready for the next call
-    }
+    if (!single)
+        return;  // the merge kernel finishes
     __syncthreads();
-    // ---- inverse rotation (the normalized transform is its own inverse)
-    if (p.rotate) {
-        for (int h = 1; h < D; h <<= 1) {
-            for (int idx = threadIdx.x; idx < G * (D / 2); idx += kThreads) {
-                int r = idx / (D / 2), k = idx % (D / 2);
-                int jj = (k / h) * 2 * h + (k % h);
-                float a = xo[r * D + jj], c = xo[r * D + jj + h];
-                xo[r * D + jj] = a + c;
-                xo[r * D + jj + h] = a - c;
-            }
-            __syncthreads();
-        }
-    }
-    const float post = p.rotate ? p.rot_c : 1.0f;
-    for (int idx = threadIdx.x; idx < G * D; idx += kThreads)
-        p.out[row0 * D + idx] = xo[idx] * post;
+    finish_rows<D>(p, xo, row0, G);
 }
 
 template <int D, int KBITS, int VBITS, bool PERCH>
@@ -425,15 +517,63 @@ __global__ __launch_bounds__(kThreads) void decode_split_kernel(AttnParams p)
     run_split<D, KBITS, VBITS, PERCH>(p, lds);
 }
 
+// Merge the S_tot split partials of one (sequence, KV head): per head, the
+// weights w_s = 2^(m_s - M) / sum_s' 2^(m_s' - M) l_s' go to LDS, then every
+// output is a weighted sum over splits of coalesced partial rows; finally
+// rotate back and store.
+template <int D>
+__global__ __launch_bounds__(kThreads) void decode_merge_kernel(AttnParams p)
+{
+    extern __shared__ float sm[];
+    const int unit = blockIdx.x;
+    const int b = unit / p.H, j = unit % p.H, G = p.G, S = p.S_tot;
+    const size_t row0 = (size_t)b * p.H_q + (size_t)j * G;
+    float* w = sm;                    // [G][S]: (max, sum) pairs, then weights
+    float* xo = sm + 2 * G * S;       // [G][D]
+    const float* ml = p.part_ml + row0 * S * 2;
+    for (int idx = threadIdx.x; idx < 2 * G * S; idx += kThreads)
+        w[idx] = ml[idx];
+    __syncthreads();
+    if (threadIdx.x < (unsigned)G) {
+        float* r = w + 2 * S * threadIdx.x;
+        float M = kNegInf;
+        for (int s = 0; s < S; ++s)
+            M = fmaxf(M, r[2 * s]);
+        float L = 0.0f;
+        for (int s = 0; s < S; ++s)
+            L += r[2 * s] == kNegInf ? 0.0f : fast_exp2(r[2 * s] - M) * r[2 * s + 1];
+        const float inv = 1.0f / L;
+        for (int s = 0; s < S; ++s) {
+            float m = r[2 * s];
+            r[2 * s] = m == kNegInf ? 0.0f : fast_exp2(m - M) * inv;  // weights overwrite maxima
+        }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+        const int h = idx / D, d = idx % D;
+        const float* o = p.part_o + ((row0 + h) * S) * D + d;
+        const float* wr = w + 2 * S * h;
+        float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
+        int s = 0;
+        for (; s + 4 <= S; s += 4) {
+            acc0 += wr[2 * s] * o[(size_t)s * D];
+            acc1 += wr[2 * s + 2] * o[(size_t)(s + 1) * D];
+            acc2 += wr[2 * s + 4] * o[(size_t)(s + 2) * D];
+            acc3 += wr[2 * s + 6] * o[(size_t)(s + 3) * D];
+        }
+        for (; s < S; ++s)
+            acc0 += wr[2 * s] * o[(size_t)s * D];
+        xo[idx] = (acc0 + acc1) + (acc2 + acc3);
+    }
+    __syncthreads();
+    finish_rows<D>(p, xo, row0, G);
+}
+
 template <int D, int KBITS, int VBITS, bool PERCH>
 hipError_t launch_split(const AttnParams& p, hipStream_t stream)
 {
-    size_t lds_floats = 16 * D;
-    size_t merge = 2 * kWaves * 16 + (size_t)(kWaves + 1) * p.G * D + 1;
-    if (merge > lds_floats)
-        lds_floats = merge;
     hipLaunchKernelGGL((decode_split_kernel<D, KBITS, VBITS, PERCH>), dim3(p.S_tot, p.B * p.H), dim3(kThreads),
-                       lds_floats * sizeof(float), stream, p);
+                       p.lds_bytes, stream, p);
     return hipGetLastError();
 }
 
@@ -458,36 +598,64 @@ hipError_t launch_decode_d(const AttnParams& p, hipStream_t stream)
         e = launch_split<D, 2, 4, true>(p, stream);
     else
         e = launch_split<D, 2, 2, true>(p, stream);
-    return e;
+    if (e != hipSuccess || p.S_tot == 1)
+        return e;
+    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3(p.B * p.H), dim3(kThreads),
+                       (size_t)(2 * p.S_tot + D) * p.G * sizeof(float), stream, p);
+    return hipGetLastError();
 }
 
 }  // namespace
 
-// Aim for about 2048 workgroups over the 256 compute units, with at least
-// two 32-token blocks per wave (8 per split) so the loop can pipeline.
-static int split_target(int B, int H, int nblk)
+// Split planning.  A split stages all its coded tokens in LDS, so its size
+// is capped by kStageBytes; within that cap, aim for about kTargetGroups
+// workgroups over the 256 compute units so several are resident per CU and
+// one's loads overlap another's arithmetic.
+constexpr int kTargetGroups = 512;
+
+static int max_blocks_per_split(int D, const kvq_format& f)
 {
-    const int units = B * H;
-    int want = (2048 + units - 1) / units;
-    int max_splits = (nblk + 7) / 8;
-    int s = want < max_splits ? want : max_splits;
-    return s < 1 ? 1 : s;
+    BlockBytes bb = block_bytes(D, f.k_bits, f.v_bits, f.k_axis, f.k_group, f.v_group, f.k_mode, f.v_mode);
+    int m = kStageBytes / bb.total();
+    return m < 1 ? 1 : m;
 }
 
-int decode_split_bound(int B, int H, int nq)
-{
-    return split_target(B, H, (nq + 31) / 32);  // non-decreasing in nq
-}
-
-void decode_plan(int B, int H, int nq, int* S_q, int* bps)
+void decode_plan(int B, int H, int D, const kvq_format& f, int nq, int* S_q, int* bps)
 {
     const int nblk = (nq + 31) / 32;
-    const int s = split_target(B, H, nblk);
-    int per = (nblk + s - 1) / s;
+    const int units = B * H;
+    const int s_want = (kTargetGroups + units - 1) / units;
+    int per = (nblk + s_want - 1) / s_want;
+    const int cap = max_blocks_per_split(D, f);
+    if (per > cap)
+        per = cap;
     if (per < 1)
         per = 1;
     *bps = per;
     *S_q = nblk == 0 ? 0 : (nblk + per - 1) / per;
+}
+
+int decode_split_bound(int B, int H, int D, const kvq_format& f, int nq)
+{
+    // S_q <= max(s_want, ceil(nblk / cap)) for every coded count up to nq.
+    const int nblk = (nq + 31) / 32;
+    const int units = B * H;
+    const int s_want = (kTargetGroups + units - 1) / units;
+    const int cap = max_blocks_per_split(D, f);
+    const int by_cap = (nblk + cap - 1) / cap;
+    int s = s_want > by_cap ? s_want : by_cap;
+    return s < 1 ? 1 : s;
+}
+
+size_t decode_lds_bytes(int D, const kvq_format& f, int bps, int G, int* q_offset)
+{
+    // [stage of bps blocks][fp32 queries 16 x D]; the merge area reuses the front.
+    BlockBytes bb = block_bytes(D, f.k_bits, f.v_bits, f.k_axis, f.k_group, f.v_group, f.k_mode, f.v_mode);
+    size_t stage = ((size_t)bps * bb.total() + 15) / 16 * 16;
+    *q_offset = (int)stage;
+    size_t total = stage + 16 * (size_t)D * sizeof(float);
+    size_t merge = (2 * kWaves * 16 + (size_t)kWaves * G * D) * sizeof(float);
+    return total > merge ? total : merge;
 }
 
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream)

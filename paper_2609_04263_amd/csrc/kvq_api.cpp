@@ -85,22 +85,17 @@ float rotation_constant(int D)
     return (float)(1.0 / sqrt((double)D));  // binary32 value nearest D^(-1/2)
 }
 
-// Decode workspace: partial outputs fp32 [B*H_q][S][D], partial (max, sum)
-// fp32 [B*H_q][S][2], then one arrival counter per KV head (u32 [B*H]).
-// The counters sit at a fixed offset for a given cache and head count,
-// so the split count S of a call never moves them.
-size_t decode_workspace_layout(const kvq_cache* c, int H_q, int S, size_t* off_ml, size_t* off_cnt)
+// Decode workspace: partial outputs fp32 [B*H_q][S][D], then partial
+// (max, sum) fp32 [B*H_q][S][2], sized for the largest split count S the
+// cache can need (the split count of a call never exceeds it).
+size_t decode_workspace_layout(const kvq_cache* c, int H_q, size_t* off_ml)
 {
-    int S_max = kvq::decode_split_bound(c->B, c->H, kvq::num_coded(c->fmt, c->T_max)) + (c->fmt.flush ? 1 : 0);
-    (void)S;
+    int S_max = kvq::decode_split_bound(c->B, c->H, c->D, c->fmt, kvq::num_coded(c->fmt, c->T_max)) + (c->fmt.flush ? 1 : 0);
     size_t rows = (size_t)c->B * H_q;
     size_t o_ml = round_up(rows * S_max * c->D * sizeof(float), 256);
-    size_t o_cnt = round_up(o_ml + rows * S_max * 2 * sizeof(float), 256);
     if (off_ml)
         *off_ml = o_ml;
-    if (off_cnt)
-        *off_cnt = o_cnt;
-    return o_cnt + (size_t)c->B * c->H * sizeof(unsigned);
+    return o_ml + rows * S_max * 2 * sizeof(float);
 }
 
 template <typename T>
@@ -214,6 +209,14 @@ kvq_status kvq_cache_rewind(kvq_cache* c, int n_new)
     if (c->fmt.flush != 0)
         return KVQ_ERR_FORMAT;
     c->n = n_new;
+    return KVQ_OK;
+}
+
+kvq_status kvq_cache_restore(kvq_cache* c, int n)
+{
+    if (!c || n < 0 || n > c->T_max)
+        return KVQ_ERR_ARG;
+    c->n = n;
     return KVQ_OK;
 }
 
@@ -337,8 +340,7 @@ kvq_status kvq_decode_workspace_bytes(const kvq_cache* c, int H_q, size_t* bytes
     if (!c || !bytes || H_q < c->H || H_q % c->H != 0 || H_q / c->H > 16)
         return KVQ_ERR_ARG;
     // Splits never exceed the bound at the largest coded-token count.
-    int S_tot = kvq::decode_split_bound(c->B, c->H, kvq::num_coded(c->fmt, c->T_max)) + (c->fmt.flush ? 1 : 0);
-    *bytes = decode_workspace_layout(c, H_q, S_tot, nullptr, nullptr);
+    *bytes = decode_workspace_layout(c, H_q, nullptr);
     return KVQ_OK;
 }
 
@@ -354,10 +356,10 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     const kvq_format& f = c->fmt;
     kvq::AttnParams p = {};
     p.nq = kvq::num_coded(f, c->n);
-    kvq::decode_plan(c->B, c->H, p.nq, &p.S_q, &p.bps);
+    kvq::decode_plan(c->B, c->H, c->D, f, p.nq, &p.S_q, &p.bps);
     p.S_tot = p.S_q + (f.flush ? 1 : 0);
-    size_t off_ml, off_cnt;
-    const size_t need = decode_workspace_layout(c, H_q, p.S_tot, &off_ml, &off_cnt);
+    size_t off_ml;
+    const size_t need = decode_workspace_layout(c, H_q, &off_ml);
     if (ws_bytes < need)
         return KVQ_ERR_WORKSPACE;
     p.kc = at<uint32_t>(c, 0);
@@ -371,7 +373,6 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.q = (const uint16_t*)Q;
     p.part_o = (float*)workspace;
     p.part_ml = (float*)((uint8_t*)workspace + off_ml);
-    p.counters = (unsigned*)((uint8_t*)workspace + off_cnt);
     p.out = (float*)O;
     p.B = c->B;
     p.H = c->H;
@@ -390,6 +391,7 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.rotate = f.rotate;
     p.sm_log2 = sm_scale * 1.4426950408889634f;
     p.rot_c = rotation_constant(c->D);
+    p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.bps, p.G, &p.q_lds_offset);
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 

@@ -77,7 +77,6 @@ struct AttnParams {
     float* part_o;        // fp32 [B*H_q][S_tot][D]  unnormalized partial outputs
     float* part_ml;       // fp32 [B*H_q][S_tot][2]  (running max in log2 units, sum)
     float* out;           // fp32 [B][H_q][D]
-    unsigned* counters;   // [B*H] arrival counters, zero between calls
     int B, H, H_q, G, T;  // T = T_alloc
     int n, nq;
     int ring;
@@ -88,11 +87,15 @@ struct AttnParams {
     int rotate;
     float sm_log2;        // softmax scale * log2(e)
     float rot_c;
+    size_t lds_bytes;     // dynamic LDS of the split kernel
+    int q_lds_offset;     // byte offset of the fp32 query rows in that LDS
 };
-// Split count over coded tokens for a cache of (B, H) units with nq coded tokens.
-void decode_plan(int B, int H, int nq, int* S_q, int* bps);
+// Split count and 32-token blocks per split over nq coded tokens.
+void decode_plan(int B, int H, int D, const kvq_format& f, int nq, int* S_q, int* bps);
 // Upper bound of S_q over every coded-token count up to nq.
-int decode_split_bound(int B, int H, int nq);
+int decode_split_bound(int B, int H, int D, const kvq_format& f, int nq);
+// Dynamic LDS of the split kernel.
+size_t decode_lds_bytes(int D, const kvq_format& f, int bps, int G, int* q_offset);
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
 
 }  // namespace kvq

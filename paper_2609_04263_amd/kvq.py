@@ -53,6 +53,7 @@ def _load() -> C.CDLL:
     L.kvq_cache_reset.argtypes = [P]
     L.kvq_cache_len.argtypes = [P, C.POINTER(I), C.POINTER(I)]
     L.kvq_cache_rewind.argtypes = [P, I]
+    L.kvq_cache_restore.argtypes = [P, I]
     L.kvq_cache_destroy.argtypes = [P]
     L.kvq_cache_destroy.restype = None
     L.kvq_project_workspace_bytes.argtypes = [I, I, C.POINTER(S)]
@@ -61,7 +62,7 @@ def _load() -> C.CDLL:
     L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
     for name in ("kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section", "kvq_cache_reset",
-                 "kvq_cache_len", "kvq_cache_rewind", "kvq_project_workspace_bytes",
+                 "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_project_workspace_bytes",
                  "kvq_project_qkv", "kvq_append", "kvq_decode_workspace_bytes", "kvq_decode_attn"):
         getattr(L, name).restype = I
     return L
@@ -69,7 +70,7 @@ def _load() -> C.CDLL:
 
 _lib = _load()
 EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
-            "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_destroy",
+            "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
             "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_append",
             "kvq_decode_workspace_bytes", "kvq_decode_attn")
 
@@ -140,6 +141,10 @@ class Cache:
     def rewind(self, n: int) -> None:
         _check(_lib.kvq_cache_rewind(self.handle, n), "cache_rewind")
 
+    def restore(self, n: int) -> None:
+        """Length n after the storage was restored from a snapshot taken at n."""
+        _check(_lib.kvq_cache_restore(self.handle, n), "cache_restore")
+
     def length(self):
         n, nc = C.c_int(), C.c_int()
         _check(_lib.kvq_cache_len(self.handle, C.byref(n), C.byref(nc)), "cache_len")
@@ -163,8 +168,8 @@ class Cache:
         return out.value
 
     def decode_workspace(self, H_q: int, device="cuda"):
-        """A zero-filled workspace of the required size (reuse it across calls)."""
-        return torch.zeros(self.decode_workspace_bytes(H_q), dtype=torch.uint8, device=device)
+        """A workspace of the required size (reuse it across calls)."""
+        return torch.empty(self.decode_workspace_bytes(H_q), dtype=torch.uint8, device=device)
 
     def decode_attn(self, Q, H_q: int, sm_scale: float, O, workspace, stream=None) -> None:
         """O[B, H_q, D] (fp32) <- attention of bf16 Q[B, H_q, D] over the cache."""
