@@ -26,17 +26,32 @@
  *
  * Storage image (the byte layout the GPU library must reproduce exactly):
  * sections Kc, Ks, Kz, Vc, Vs, Vz, Kr, Vr, each starting at a multiple of
- * 256 bytes.  T_alloc = T_max rounded up to a multiple of 32.
- *   Kc  u32 [B][H][T_alloc][D*kb/32]   K codes packed along head_dim
- *   Ks  f32 [B][H][T_alloc][D/kg]      per-token K scale
- *       f32 [B][H][T_alloc/32][D]      per-channel K scale (32-token groups)
+ * 256 bytes.  T_alloc = T_max rounded up to a multiple of 32; NB = T_alloc/32
+ * blocks of 32 tokens per (b, h); u = b*H + h; token t is position
+ * tau = t % 32 of block beta = t / 32.
+ *
+ * Codes are stored in pieces of eight codes, code j of a piece at bits
+ * [bits*j, bits*j + bits) (a piece is a u32 for 4-bit codes, a u16 for
+ * 2-bit codes; piece i of a section starts at byte i * bits).  The pieces of
+ * a block are ordered for the consumer, a 64-lane MFMA layout: token tau has
+ * row r = 4*(tau/8) + tau%4 in half e = (tau/4)%2 of its block.
+ *   Kc  piece (t, P) = channels 8P..8P+7 of token t, P < D/8, at index
+ *       (((u*NB + beta)*2 + e)*64 + r + 16*(P%4)) * (D/32) + P/4
+ *   Vc  piece (o, d) = tokens 8o..8o+7 (octet o) of channel d, at index
+ *       ((u*NB + o/4)*64 + d%16 + 16*(o%4)) * (D/16) + d/16
+ *   Ks  f32 per-token K scale of group g (channels g*kg ..), at
+ *       ((u*NB + beta)*(D/kg) + g)*32 + tau
+ *       f32 per-channel K scale of (32-token group beta, channel d), at
+ *       (u*NB + beta)*D + d
  *   Kz  like Ks, affine K only (zero bytes for symmetric K)
- *   Vc  u32 [B][H][T_alloc*vb/32][D]   V codes packed along tokens
- *   Vs  f32 [B][H][T_alloc][D/vg]      per-token V scale
+ *   Vs  f32 per-token V scale of group g, at ((u*NB + beta)*(D/vg) + g)*32 + tau
  *   Vz  like Vs, affine V only
  *   Kr  f16 [B][H][R+F][D]             fp16 residual ring (F > 0 only)
  *   Vr  f16 [B][H][R+F][D]
- * In a packed word, element j of the run sits at bits [b*j, b*j + b).
+ * The paper fixes the codes, their width and the metadata (Sec. 3.1), not
+ * the order of the packed bytes; this order is the one the decode kernel
+ * reads, so the packed cache is streamed without rearrangement.
+ * orc_pack_word/orc_unpack_word pack a full 32-bit word (32/bits codes).
  */
 #include <math.h>
 #include <stddef.h>
@@ -387,35 +402,78 @@ static int view_init(image_view* v, const orc_format* f, int B, int H, int D, in
     return ORC_OK;
 }
 
-static uint32_t* kc_word(const image_view* v, int b, int h, int t, int w)
+static size_t unit_block(const image_view* v, int b, int h, int t)
 {
-    size_t wpt = (size_t)(v->D * v->f->k_bits / 32);
-    size_t i = (((size_t)b * v->H + h) * v->T + t) * wpt + w;
-    return (uint32_t*)(v->img + v->off[0]) + i;
+    return ((size_t)b * v->H + h) * (size_t)(v->T / 32) + (size_t)(t / 32);
+}
+
+/* Score-row of position tau in its half block, and the half. */
+static int row_of(int tau) { return 4 * (tau / 8) + tau % 4; }
+static int half_of(int tau) { return (tau / 4) % 2; }
+
+/* Byte address of K piece P (channels 8P..8P+7) of token t. */
+static uint8_t* kc_piece(const image_view* v, int b, int h, int t, int P)
+{
+    int tau = t % 32;
+    size_t lane = (size_t)row_of(tau) + 16 * (size_t)(P % 4);
+    size_t i = ((unit_block(v, b, h, t) * 2 + (size_t)half_of(tau)) * 64 + lane) * (size_t)(v->D / 32) + (size_t)(P / 4);
+    return v->img + v->off[0] + i * (size_t)v->f->k_bits;
+}
+
+/* Byte address of V piece (octet t / 8, channel d). */
+static uint8_t* vc_piece(const image_view* v, int b, int h, int t, int d)
+{
+    int o = (t % 32) / 8;
+    size_t lane = (size_t)(d % 16) + 16 * (size_t)o;
+    size_t i = (unit_block(v, b, h, t) * 64 + lane) * (size_t)(v->D / 16) + (size_t)(d / 16);
+    return v->img + v->off[3] + i * (size_t)v->f->v_bits;
+}
+
+/* A piece holds eight codes of `bits` bits: 32 bits for 4-bit codes, 16 for 2-bit. */
+static uint32_t piece_get(const uint8_t* p, int bits)
+{
+    if (bits == 4) {
+        uint32_t w;
+        memcpy(&w, p, 4);
+        return w;
+    }
+    uint16_t hw;
+    memcpy(&hw, p, 2);
+    return hw;
+}
+
+static void piece_put(uint8_t* p, int bits, uint32_t val)
+{
+    if (bits == 4) {
+        memcpy(p, &val, 4);
+    } else {
+        uint16_t hw = (uint16_t)val;
+        memcpy(p, &hw, 2);
+    }
+}
+
+static uint32_t pack8(const uint8_t* codes, int bits)
+{
+    uint32_t w = 0;
+    for (int j = 0; j < 8; ++j)
+        w |= (uint32_t)codes[j] << (bits * j);
+    return w;
 }
 
 /* Index of K metadata for (b, h, token t, head_dim element d). */
 static size_t kmeta_index(const image_view* v, int b, int h, int t, int d)
 {
-    size_t bh = (size_t)b * v->H + h;
     if (v->f->k_axis == 0) {
         size_t gpt = (size_t)(v->D / v->f->k_group);
-        return (bh * v->T + t) * gpt + d / v->f->k_group;
+        return (unit_block(v, b, h, t) * gpt + (size_t)(d / v->f->k_group)) * 32 + (size_t)(t % 32);
     }
-    return (bh * (v->T / 32) + t / 32) * v->D + d;
-}
-
-static uint32_t* vc_word(const image_view* v, int b, int h, int t, int d)
-{
-    size_t tw = (size_t)(v->T * v->f->v_bits / 32);
-    size_t i = (((size_t)b * v->H + h) * tw + t / (32 / v->f->v_bits)) * v->D + d;
-    return (uint32_t*)(v->img + v->off[3]) + i;
+    return unit_block(v, b, h, t) * v->D + d;
 }
 
 static size_t vmeta_index(const image_view* v, int b, int h, int t, int d)
 {
     size_t gpt = (size_t)(v->D / v->f->v_group);
-    return (((size_t)b * v->H + h) * v->T + t) * gpt + d / v->f->v_group;
+    return (unit_block(v, b, h, t) * gpt + (size_t)(d / v->f->v_group)) * 32 + (size_t)(t % 32);
 }
 
 static uint16_t* ring_entry(const image_view* v, int which, int b, int h, int t)
@@ -493,7 +551,6 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
 
     const int q0 = orc_num_coded(f, n0), q1 = orc_num_coded(f, n1);
     const int kb = f->k_bits, vb = f->v_bits;
-    const int kpw = 32 / kb, vpw = 32 / vb;
     float* x = (float*)malloc(sizeof(float) * (size_t)D * 32);
     uint8_t* codes = (uint8_t*)malloc((size_t)D * 32);
     if (!x || !codes) {
@@ -520,8 +577,8 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                         if (f->k_mode == 0)
                             Kz[mi] = z;
                     }
-                    for (int w = 0; w < D / kpw; ++w)
-                        *kc_word(&v, b, h, t, w) = orc_pack_word(codes + w * kpw, kb);
+                    for (int P = 0; P < D / 8; ++P)
+                        piece_put(kc_piece(&v, b, h, t, P), kb, pack8(codes + 8 * P, kb));
                 }
             } else {
                 /* K, groups of 32 tokens per channel (KIVI keys). */
@@ -543,12 +600,12 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                             codes[(size_t)i * D + d] = cc[i];
                     }
                     for (int i = 0; i < 32; ++i)
-                        for (int w = 0; w < D / kpw; ++w)
-                            *kc_word(&v, b, h, t0 + i, w) = orc_pack_word(codes + (size_t)i * D + w * kpw, kb);
+                        for (int P = 0; P < D / 8; ++P)
+                            piece_put(kc_piece(&v, b, h, t0 + i, P), kb, pack8(codes + (size_t)i * D + 8 * P, kb));
                 }
             }
             /* V, groups along head_dim; codes packed along tokens.  Writing
-             * token t keeps the bits of earlier tokens in the word and
+             * token t keeps the bits of earlier tokens in its piece and
              * clears those of t and later tokens before inserting t's code. */
             for (int t = q0; t < q1; ++t) {
                 token_values(&v, 1, V, n0, n_new, b, h, t, x);
@@ -560,11 +617,11 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                     if (f->v_mode == 0)
                         Vz[mi] = z;
                 }
-                int j = t % vpw;
+                int j = t % 8;
                 uint32_t keep = j == 0 ? 0u : ((1u << (vb * j)) - 1u);
                 for (int d = 0; d < D; ++d) {
-                    uint32_t* w = vc_word(&v, b, h, t, d);
-                    *w = (*w & keep) | ((uint32_t)codes[d] << (vb * j));
+                    uint8_t* pc = vc_piece(&v, b, h, t, d);
+                    piece_put(pc, vb, (piece_get(pc, vb) & keep) | ((uint32_t)codes[d] << (vb * j)));
                 }
             }
             /* fp16 residual ring: slot t mod (R + F) holds the newest token
@@ -616,12 +673,12 @@ static void reconstruct_bh(const image_view* v, int b, int h, int n, double* kha
         for (int d = 0; d < D; ++d) {
             double kv, vv;
             if (t < nq) {
-                uint32_t kw = *kc_word(v, b, h, t, d / (32 / kb));
-                uint32_t kc = (kw >> (kb * (d % (32 / kb)))) & ((1u << kb) - 1u);
+                uint32_t kw = piece_get(kc_piece(v, b, h, t, d / 8), kb);
+                uint32_t kc = (kw >> (kb * (d % 8))) & ((1u << kb) - 1u);
                 size_t km = kmeta_index(v, b, h, t, d);
                 kv = dequant_code(f->k_mode, kb, kc, Ks[km], f->k_mode == 0 ? Kz[km] : 0.0f);
-                uint32_t vw = *vc_word(v, b, h, t, d);
-                uint32_t vc = (vw >> (vb * (t % (32 / vb)))) & ((1u << vb) - 1u);
+                uint32_t vw = piece_get(vc_piece(v, b, h, t, d), vb);
+                uint32_t vc = (vw >> (vb * (t % 8))) & ((1u << vb) - 1u);
                 size_t vm = vmeta_index(v, b, h, t, d);
                 vv = dequant_code(f->v_mode, vb, vc, Vs[vm], f->v_mode == 0 ? Vz[vm] : 0.0f);
             } else {

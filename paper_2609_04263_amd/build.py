@@ -28,8 +28,13 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libkvq.so")
 ROOT = os.path.dirname(HERE)
 
-SOURCES = ["kvq_api.cpp", "append.hip", "attn.hip", "project.hip"]
-PER_FILE = {"append.hip": ["-ffp-contract=off"]}
+SOURCES = ["kvq_api.cpp", "append.hip", "attn.hip", "attn_d64.hip", "attn_d128.hip", "attn_d256.hip",
+           "project.hip"]
+# MFMA accumulators in VGPRs: the attention loop rescales them with VALU
+# instructions, and AGPR accumulators cost a copy each way per block.
+_VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+PER_FILE = {"append.hip": ["-ffp-contract=off"], "attn_d64.hip": _VGPR_MFMA, "attn_d128.hip": _VGPR_MFMA,
+            "attn_d256.hip": _VGPR_MFMA}
 
 
 def hipcc() -> str:

@@ -11,10 +11,17 @@
 // (sequence, KV head): the block's K rows are staged in LDS as fp32 (rotated
 // by the fixed Hadamard butterflies when the format rotates, rounded to fp16
 // when a window exists), group statistics are reduced per (token, group) or
-// per channel, and every output word is assembled by one thread.  V rows
-// follow through the same LDS buffer.  V codes are packed along tokens: a
-// word shared with tokens outside the block range keeps earlier tokens' bits
-// and clears later ones, so the image is independent of call boundaries.
+// per channel, and every output piece (eight codes) is assembled by one
+// thread.  V rows follow through the same LDS buffer.  V codes are packed
+// along tokens: a piece shared with tokens outside the block range keeps
+// earlier tokens' bits and clears later ones, so the image is independent of
+// call boundaries.
+//
+// Pieces are stored in the order the decode kernel consumes them (per
+// 32-token block, a 64-lane MFMA layout; see include/kvq.h): token tau of a
+// block is row 4 (tau / 8) + tau % 4 of half (tau / 4) % 2, and the lane of
+// key piece P is row + 16 (P % 4); value piece (octet o, channel d) belongs
+// to lane d % 16 + 16 o.
 
 #include "kvq_device.h"
 #include "kvq_internal.h"
@@ -24,6 +31,35 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kBlockTok = 32;
+
+// Index of key piece P (channels 8P..8P+7) of position tau in block `blk`
+// (blk counted over the whole section: unit * NB + block).
+template <int D>
+__device__ __forceinline__ size_t key_piece(size_t blk, int tau, int P)
+{
+    const int row = 4 * (tau >> 3) + (tau & 3), half = (tau >> 2) & 1;
+    return ((blk * 2 + half) * 64 + row + 16 * (P & 3)) * (D / 32) + (P >> 2);
+}
+
+// Index of value piece (octet o of the block, channel d).
+template <int D>
+__device__ __forceinline__ size_t value_piece(size_t blk, int o, int d)
+{
+    return (blk * 64 + (d & 15) + 16 * o) * (D / 16) + (d >> 4);
+}
+
+__device__ __forceinline__ void store_piece(void* base, size_t i, int bits, uint32_t v)
+{
+    if (bits == 4)
+        ((uint32_t*)base)[i] = v;
+    else
+        ((uint16_t*)base)[i] = (uint16_t)v;
+}
+
+__device__ __forceinline__ uint32_t load_piece(const void* base, size_t i, int bits)
+{
+    return bits == 4 ? ((const uint32_t*)base)[i] : ((const uint16_t*)base)[i];
+}
 
 __device__ __forceinline__ uint32_t code_affine(float x, float mn, float s, float top)
 {
@@ -148,8 +184,10 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
     const size_t bh = (size_t)unit;
 
     // ------------------------------------------------------------ keys
+    const size_t blk = bh * (size_t)(p.T / kBlockTok) + (size_t)(tb / kBlockTok);
     stage_rows<D>(p, 0, b, h, tb, xs, from_input);
-    const int kb = p.k_bits, kpw = 32 / kb, kwpt = D / kpw;
+    const int kb = p.k_bits;
+    constexpr int PPT = D / 8;  // pieces per token
     if (p.k_axis == KVQ_PER_TOKEN) {
         const int ng = D / p.k_group;
         for (int idx = threadIdx.x; idx < kBlockTok * ng; idx += kThreads) {
@@ -160,22 +198,22 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
             group_stats(xs + i * D + gi * p.k_group, 1, p.k_group, p.k_mode, kb, &s, &z);
             ms[idx] = s;
             mz[idx] = z;
-            size_t mi = (bh * p.T + t) * ng + gi;
+            size_t mi = (blk * ng + gi) * kBlockTok + i;
             p.ks[mi] = s;
             if (p.k_mode == KVQ_AFFINE)
                 p.kz[mi] = z;
         }
         __syncthreads();
-        for (int idx = threadIdx.x; idx < kBlockTok * kwpt; idx += kThreads) {
-            int i = idx / kwpt, w = idx % kwpt, t = tb + i;
+        for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
+            int i = idx / PPT, P = idx % PPT, t = tb + i;
             if (t < lo || t >= hi)
                 continue;
-            int gi = (w * kpw) / p.k_group;
+            int gi = (8 * P) / p.k_group;
             float s = ms[i * ng + gi], z = mz[i * ng + gi];
             uint32_t word = 0;
-            for (int e = 0; e < kpw; ++e)
-                word |= code_one(xs[i * D + w * kpw + e], s, z, p.k_mode, kb) << (kb * e);
-            p.kc[(bh * p.T + t) * kwpt + w] = word;
+            for (int e = 0; e < 8; ++e)
+                word |= code_one(xs[i * D + 8 * P + e], s, z, p.k_mode, kb) << (kb * e);
+            store_piece(p.kc, key_piece<D>(blk, i, P), kb, word);
         }
     } else {
         // Per-channel keys: the block is one whole 32-token group.
@@ -184,27 +222,27 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
             group_stats(xs + d, D, kBlockTok, p.k_mode, kb, &s, &z);
             ms[d] = s;
             mz[d] = z;
-            size_t mi = (bh * (p.T / kBlockTok) + tb / kBlockTok) * D + d;
+            size_t mi = blk * D + d;
             p.ks[mi] = s;
             if (p.k_mode == KVQ_AFFINE)
                 p.kz[mi] = z;
         }
         __syncthreads();
-        for (int idx = threadIdx.x; idx < kBlockTok * kwpt; idx += kThreads) {
-            int i = idx / kwpt, w = idx % kwpt, t = tb + i;
+        for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
+            int i = idx / PPT, P = idx % PPT;
             uint32_t word = 0;
-            for (int e = 0; e < kpw; ++e) {
-                int d = w * kpw + e;
+            for (int e = 0; e < 8; ++e) {
+                int d = 8 * P + e;
                 word |= code_one(xs[i * D + d], ms[d], mz[d], p.k_mode, kb) << (kb * e);
             }
-            p.kc[(bh * p.T + t) * kwpt + w] = word;
+            store_piece(p.kc, key_piece<D>(blk, i, P), kb, word);
         }
     }
     __syncthreads();
 
     // ---------------------------------------------------------- values
     stage_rows<D>(p, 1, b, h, tb, xs, from_input);
-    const int vb = p.v_bits, vpw = 32 / vb, ng = D / p.v_group;
+    const int vb = p.v_bits, ng = D / p.v_group;
     for (int idx = threadIdx.x; idx < kBlockTok * ng; idx += kThreads) {
         int i = idx / ng, gi = idx % ng, t = tb + i;
         if (t < lo || t >= hi)
@@ -213,34 +251,32 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
         group_stats(xs + i * D + gi * p.v_group, 1, p.v_group, p.v_mode, vb, &s, &z);
         ms[idx] = s;
         mz[idx] = z;
-        size_t mi = (bh * p.T + t) * ng + gi;
+        size_t mi = (blk * ng + gi) * kBlockTok + i;
         p.vs[mi] = s;
         if (p.v_mode == KVQ_AFFINE)
             p.vz[mi] = z;
     }
     __syncthreads();
-    const int words_per_col = kBlockTok / vpw;  // words along tokens in this block
-    const size_t tw_all = (size_t)p.T / vpw;
-    for (int idx = threadIdx.x; idx < words_per_col * D; idx += kThreads) {
-        int tw = idx / D, d = idx % D;
-        int tfirst = tb + tw * vpw;
-        if (tfirst + vpw <= lo || tfirst >= hi)
+    for (int idx = threadIdx.x; idx < (kBlockTok / 8) * D; idx += kThreads) {
+        int o = idx / D, d = idx % D;
+        int tfirst = tb + 8 * o;
+        if (tfirst + 8 <= lo || tfirst >= hi)
             continue;
-        uint32_t* dst = p.vc + (bh * tw_all + tfirst / vpw) * D + d;
+        const size_t pi = value_piece<D>(blk, o, d);
         uint32_t word = 0;
         if (tfirst < lo) {  // keep the bits of tokens appended earlier
             int keep_n = lo - tfirst;
-            word = *dst & ((1u << (vb * keep_n)) - 1u);
+            word = load_piece(p.vc, pi, vb) & ((1u << (vb * keep_n)) - 1u);
         }
         int gi = d / p.v_group;
-        for (int e = 0; e < vpw; ++e) {
+        for (int e = 0; e < 8; ++e) {
             int t = tfirst + e;
             if (t < lo || t >= hi)
                 continue;
             int i = t - tb;
             word |= code_one(xs[i * D + d], ms[i * ng + gi], mz[i * ng + gi], p.v_mode, vb) << (vb * e);
         }
-        *dst = word;
+        store_piece(p.vc, pi, vb, word);
     }
 }
 

@@ -391,7 +391,7 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.rotate = f.rotate;
     p.sm_log2 = sm_scale * 1.4426950408889634f;
     p.rot_c = rotation_constant(c->D);
-    p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.bps, p.G, &p.q_lds_offset);
+    p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.G);
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 

@@ -88,14 +88,13 @@ struct AttnParams {
     float sm_log2;        // softmax scale * log2(e)
     float rot_c;
     size_t lds_bytes;     // dynamic LDS of the split kernel
-    int q_lds_offset;     // byte offset of the fp32 query rows in that LDS
 };
 // Split count and 32-token blocks per split over nq coded tokens.
 void decode_plan(int B, int H, int D, const kvq_format& f, int nq, int* S_q, int* bps);
 // Upper bound of S_q over every coded-token count up to nq.
 int decode_split_bound(int B, int H, int D, const kvq_format& f, int nq);
 // Dynamic LDS of the split kernel.
-size_t decode_lds_bytes(int D, const kvq_format& f, int bps, int G, int* q_offset);
+size_t decode_lds_bytes(int D, const kvq_format& f, int G);
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
 
 }  // namespace kvq

@@ -1,8 +1,9 @@
 """Pins of the oracle's physical incremental cache (Sec. 3.1).
 
-* Each coded token's words and metadata, decoded by hand with numpy from the
-  documented image layout, equal the pinned group coder applied to that
-  token's values (catches wrong slots, transposed packing, wrong groups).
+* Each coded token's pieces and metadata, decoded by hand with numpy from the
+  documented image layout (blocks of 32 tokens in the order of a 64-lane
+  MFMA layout), equal the pinned group coder applied to that token's values
+  (catches wrong slots, transposed packing, wrong groups).
 * Appending is chunking-invariant: one call, token-by-token and ragged
   chunks give byte-identical images (the state depends on tokens, not calls).
 * KIVI residual window: the newest tokens stay fp16 in the ring; with at
@@ -31,12 +32,29 @@ def f32(bits):
     return synth.bf16_bits_to_f32(bits)
 
 
-def words(img, off, count):
-    return np.frombuffer(img[off:off + 4 * count].tobytes(), dtype=np.uint32)
-
-
 def floats(img, off, count):
     return np.frombuffer(img[off:off + 4 * count].tobytes(), dtype=np.float32)
+
+
+def pieces(img, off, ln, bits):
+    """Section as an array of eight-code pieces (u32 for 4-bit, u16 for 2-bit)."""
+    dt = np.uint32 if bits == 4 else np.uint16
+    return np.frombuffer(img[off:off + ln].tobytes(), dtype=dt)
+
+
+def kc_index(b, h, t, P, H, NB, D):
+    u, beta, tau = b * H + h, t // 32, t % 32
+    row, half = 4 * (tau // 8) + tau % 4, (tau // 4) % 2
+    return (((u * NB + beta) * 2 + half) * 64 + row + 16 * (P % 4)) * (D // 32) + P // 4
+
+
+def vc_index(b, h, t, d, H, NB, D):
+    u, beta, o = b * H + h, t // 32, (t % 32) // 8
+    return ((u * NB + beta) * 64 + d % 16 + 16 * o) * (D // 16) + d // 16
+
+
+def meta_index(b, h, t, g, H, NB, groups):
+    return (((b * H + h) * NB + t // 32) * groups + g) * 32 + t % 32
 
 
 def test_per_token_affine_slots_decode_by_hand():
@@ -47,31 +65,56 @@ def test_per_token_affine_slots_decode_by_hand():
     c.append(K[:, :20], V[:, :20])
     c.append(K[:, 20:], V[:, 20:])
     off, ln, _ = oracle.layout(f, B, H, D, T)
-    Ta = 64
-    kc = words(c.image, off[0], ln[0] // 4).reshape(B, H, Ta, D // 8)
-    ks = floats(c.image, off[1], ln[1] // 4).reshape(B, H, Ta, D // 32)
-    kz = floats(c.image, off[2], ln[2] // 4).reshape(B, H, Ta, D // 32)
-    vc = words(c.image, off[3], ln[3] // 4).reshape(B, H, Ta // 8, D)
-    vs = floats(c.image, off[4], ln[4] // 4).reshape(B, H, Ta, D // 32)
-    vz = floats(c.image, off[5], ln[5] // 4).reshape(B, H, Ta, D // 32)
+    NB = 64 // 32
+    kc = pieces(c.image, off[0], ln[0], 4)
+    ks = floats(c.image, off[1], ln[1] // 4)
+    kz = floats(c.image, off[2], ln[2] // 4)
+    vc = pieces(c.image, off[3], ln[3], 4)
+    vs = floats(c.image, off[4], ln[4] // 4)
+    vz = floats(c.image, off[5], ln[5] // 4)
     for b in range(B):
         for h in range(H):
             for t in (0, 7, 8, 19, 20, 36):
                 x = f32(K[b, t, h])
                 y = f32(V[b, t, h])
                 for gi in range(2):
+                    mi = meta_index(b, h, t, gi, H, NB, 2)
                     codes, s, z = oracle.quant_affine(x[32 * gi:32 * gi + 32], 4)
-                    assert ks[b, h, t, gi] == s and kz[b, h, t, gi] == z
+                    assert ks[mi] == s and kz[mi] == z
                     for w in range(4):
-                        assert kc[b, h, t, 4 * gi + w] == oracle.pack_word(codes[8 * w:8 * w + 8], 4)
+                        P = 4 * gi + w
+                        assert kc[kc_index(b, h, t, P, H, NB, D)] == oracle.pack_word(codes[8 * w:8 * w + 8], 4)
                     vcodes, vs_, vz_ = oracle.quant_affine(y[32 * gi:32 * gi + 32], 4)
-                    assert vs[b, h, t, gi] == vs_ and vz[b, h, t, gi] == vz_
+                    assert vs[mi] == vs_ and vz[mi] == vz_
                     for d in range(32):
-                        word = vc[b, h, t // 8, 32 * gi + d]
+                        word = vc[vc_index(b, h, t, 32 * gi + d, H, NB, D)]
                         assert (word >> (4 * (t % 8))) & 15 == vcodes[d]
-    # bits of tokens past n in the last partial V word are zero
-    last = vc[:, :, 36 // 8, :]
-    assert np.all(last >> (4 * (37 % 8)) == 0)
+    # bits of tokens past n in the last partial V piece are zero
+    for b in range(B):
+        for h in range(H):
+            for d in range(D):
+                assert vc[vc_index(b, h, 36, d, H, NB, D)] >> (4 * (37 % 8)) == 0
+
+
+def test_two_bit_pieces_decode_by_hand():
+    f = FMTS["affine2_g64"]
+    B, H, D, T = 1, 2, 64, 64
+    K, V = synth.kv_tokens(14, B, 45, H, D)
+    c = oracle.Cache(f, B, H, D, T)
+    c.append(K, V)
+    off, ln, _ = oracle.layout(f, B, H, D, T)
+    NB = 2
+    kc = pieces(c.image, off[0], ln[0], 2)
+    vc = pieces(c.image, off[3], ln[3], 2)
+    for h in range(H):
+        for t in (0, 13, 31, 32, 44):
+            codes, _, _ = oracle.quant_affine(f32(K[0, t, h]), 2)
+            vcodes, _, _ = oracle.quant_affine(f32(V[0, t, h]), 2)
+            for P in range(D // 8):
+                piece = int(kc[kc_index(0, h, t, P, H, NB, D)])
+                assert [(piece >> (2 * j)) & 3 for j in range(8)] == list(codes[8 * P:8 * P + 8])
+            for d in range(D):
+                assert (int(vc[vc_index(0, h, t, d, H, NB, D)]) >> (2 * (t % 8))) & 3 == vcodes[d]
 
 
 def test_per_channel_keys_decode_by_hand():
@@ -82,7 +125,8 @@ def test_per_channel_keys_decode_by_hand():
     c.append(K, V)
     assert c.n == 200 and c.n_coded == 64
     off, ln, _ = oracle.layout(f, B, H, D, T)
-    kc = words(c.image, off[0], ln[0] // 4).reshape(B, H, T, D // 16)
+    NB = T // 32
+    kc = pieces(c.image, off[0], ln[0], 2)
     ks = floats(c.image, off[1], ln[1] // 4).reshape(B, H, T // 32, D)
     kz = floats(c.image, off[2], ln[2] // 4).reshape(B, H, T // 32, D)
     for h in range(H):
@@ -93,8 +137,8 @@ def test_per_channel_keys_decode_by_hand():
                 codes, s, z = oracle.quant_affine(col, 2)
                 assert ks[0, h, grp, d] == s and kz[0, h, grp, d] == z
                 for i in range(32):
-                    word = kc[0, h, 32 * grp + i, d // 16]
-                    assert (word >> (2 * (d % 16))) & 3 == codes[i]
+                    piece = int(kc[kc_index(0, h, 32 * grp + i, d // 8, H, NB, D)])
+                    assert (piece >> (2 * (d % 8))) & 3 == codes[i]
     # the ring holds fp16 of the newest 160 tokens at slot t mod 160
     kr = np.frombuffer(c.image[off[6]:off[6] + ln[6]].tobytes(), dtype=np.uint16).reshape(B, H, 160, D)
     for t in (40, 100, 199):
