@@ -4,33 +4,42 @@
 // it).  Included by one translation unit per head dimension.
 //
 // Work decomposition.  A workgroup of 4 waves handles one (split, sequence,
-// KV head).  The G <= 16 query heads of the KV head are the N = 16 columns
-// of v_mfma_f32_16x16x32_f16 (heads >= G are zero), so each code is read
-// from HBM once per KV head.  Each wave walks every fourth 32-token block of
-// the split:
+// KV head).  The MFMA v_mfma_f32_16x16x32_f16 has 16 columns; the G <= 16
+// query heads of the KV head take G of them, so every code is read from HBM
+// once per KV head.  When the value groups of a token times G fit in the 16
+// columns, each value group gets its own copy of the G head columns
+// (column r G + h: head h, value group r) and one pass of the value-side
+// arithmetic serves every group; otherwise groups are taken one per pass.
+// Each wave walks every fourth 32-token block of the split:
 //
 //   loads     the cache stores each block's code pieces in the order of
 //             this kernel's MFMA operands, so a lane reads its key and value
 //             pieces with a few 8- to 16-byte loads that are contiguous
-//             across the wave; the block's scales and offsets are read with
-//             one 16-byte load per lane into a per-wave LDS buffer, from
-//             which lanes read them broadcast.  The next block's loads are
-//             issued before the current block is computed;
-//   scores    per-token keys: S[t][h] = sum_g s_tg (sum_{d in g} c_td q_hd)
-//             + z_tg sum_{d in g} q_hd, one MFMA per 32 channels with the
-//             codes as exact fp16 A operands and the query as B (fp16 hi,
-//             plus an fp16 remainder when the query is rotated); per-channel
-//             keys fold the channel scale into the B operand (hi + lo fp16);
-//   softmax   online in base 2 (sm_scale * log2(e) is folded into the query);
+//             across the wave; the block's scales and offsets pass through a
+//             per-wave LDS buffer, from which lanes read them broadcast.  The
+//             next block's loads are issued before the current one is
+//             computed, and every lane issues the same loads, so the wait
+//             before a block only covers that block;
+//   codes     a piece of eight codes becomes an exact fp16 MFMA operand
+//             A = B0 + c with two bit operations per pair (the exponent of
+//             B0 = 16 for 4-bit, 4 for 2-bit codes gives the code bits unit
+//             weight); the bias is folded into a staged offset
+//             z' = z - B0 s (z = -2^(b-1) s for symmetric codes), so that
+//             every reconstructed element is A s + z';
+//   scores    per-token keys: S[t][h] = sum_g s_tg (sum_{d in g} A_td q_hd)
+//             + z'_tg sum_{d in g} q_hd, one MFMA per 32 channels with the
+//             query as B (fp16 hi, plus an fp16 remainder when the query is
+//             rotated); per-channel keys fold the channel scale into the B
+//             operand (hi + lo fp16) and sum_d z'_d q_d into the accumulator;
+//   softmax   online in base 2 (scales and offsets carry sm_scale log2(e));
 //             the running maximum is only raised when a block exceeds it by
 //             more than kTau, so the accumulators are rescaled a few times
 //             per split, not per block;
-//   values    O^T[d][h] += sum_t c_dt (p_t s_tg 2^-kTau) over 32 tokens per
-//             MFMA, with p s as hi + lo fp16 B operands, and the offset term
-//             sum_t p_t z_tg accumulated per lane in fp32.
+//   values    O^T[d][h] += sum_t A_dt (p_t s_tg 2^-kTau) over 32 tokens per
+//             MFMA, with p s as hi + lo fp16 B operands, plus the offset term
+//             sum_t p_t z'_tg accumulated per lane in fp32.
 //
-// Codes become exact fp16 operands with the 0x6400 exponent trick and one
-// packed fp16 subtract, so every MFMA product is exact and accumulation is
+// Every MFMA product is exact (fp16 x fp16 in fp32) and accumulation is
 // fp32.  Tokens of an fp16 window are handled by one extra split per KV head
 // that feeds the fp16 values to the same MFMAs.  Each split writes an
 // unnormalized partial (m, l, o) and a second kernel merges them (a kernel
@@ -38,6 +47,8 @@
 // agent-scope fences write back and invalidate the L2 on gfx950).  With a
 // single split the first kernel writes the outputs itself.
 #pragma once
+
+#include <atomic>
 
 #include "kvq_device.h"
 #include "kvq_internal.h"
@@ -48,16 +59,16 @@ namespace attn {
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
 constexpr float kNegInf = -__builtin_inff();
-constexpr float kTau = 4.0f;         // lazy rescale threshold, log2 units
-constexpr float kPScale = 0.0625f;   // 2^-kTau: keeps p s below the group scale
+constexpr float kTau = 4.0f;        // lazy rescale threshold, log2 units
+constexpr float kPScale = 0.0625f;  // 2^-kTau: keeps p s below the group scale
 
-// 16-byte loads per lane that read the largest metadata of one block (key
-// groups of 32; scales and offsets of keys and values).  The per-wave LDS
-// buffer holds 1 KiB per load.
-__host__ __device__ constexpr int meta_loads(int D, bool perch, int nvg)
+// 16-byte metadata chunk pairs (scale, offset) per lane that cover the
+// largest metadata of one block: key groups of 32 (or per-channel keys, D
+// floats each) and D / v_group value groups, 32 tokens each.  The per-wave
+// LDS buffer holds 2 KiB per pair.
+__host__ __device__ constexpr int meta_pairs(int D, int nvg)
 {
-    (void)perch;  // key metadata is at most 2 D floats either way
-    return ((2 * D + 2 * 32 * nvg) / 4 + 63) / 64;
+    return ((D + 32 * nvg) / 4 + 63) / 64;
 }
 
 // Compile-time shape of one kernel instance.
@@ -67,13 +78,12 @@ struct Cfg {
     static constexpr bool PERCH = PERCH_;
     static constexpr int NKB = D / 32;          // 32-channel K-blocks of the score MFMAs
     static constexpr int NMB = D / 16;          // 16-channel M-blocks of the value MFMAs
-    static constexpr int WPT = D * KBITS / 32;  // key code words per token in the cache
     static constexpr int KW = NKB * KBITS / 4;  // key code words per lane and half block
     static constexpr int VW = NMB * VBITS / 4;  // value code words per lane and block
     static constexpr int VG = 32 << VGS;        // value group size
     static constexpr int NVG = D / VG;          // value groups per token
     static constexpr int MBPG = VG / 16;        // value M-blocks per group
-    static constexpr int NMETA = meta_loads(D, PERCH, NVG);
+    static constexpr int NPAIR = meta_pairs(D, NVG);
     static_assert(NVG >= 1, "value group larger than head_dim");
 };
 
@@ -118,45 +128,100 @@ __device__ __forceinline__ void gload_words(const uint32_t* p, uint32_t* w)
     }
 }
 
-// Piece k (eight codes) of a lane's words: a word for 4-bit codes, a
-// halfword for 2-bit codes.
+// ------------------------------------------------------------ code operands
+
+// Operand bias B0 of a code width: A = B0 + c exactly in binary16.
 template <int BITS>
-__device__ __forceinline__ uint32_t piece(const uint32_t* w, int k)
+__device__ constexpr float code_bias()
 {
-    if (BITS == 4)
-        return w[k];
-    return w[k >> 1] >> (16 * (k & 1));
+    return BITS == 4 ? 16.0f : 4.0f;
 }
 
-// Row of the score MFMA A operand (and lane column hh) for token tb of a
-// block: tokens 8a + 4 h2 + b sit in row 4a + b of half h2, so the MFMA
-// output rows 4 qg + i of lane (hh, qg) are tokens 8 qg + 4 h2 + i, the same
-// tokens whose values that lane's B operand covers.
-__device__ __forceinline__ int score_row(int tb) { return 4 * (tb >> 3) + (tb & 3); }
-__device__ __forceinline__ int score_half(int tb) { return (tb >> 2) & 1; }
+// Bit constants of the conversion, kept in registers (a VOP3 operation
+// cannot take two literals on gfx950).
+struct CodeBits {
+    uint32_t mask, magic;
+};
+
+template <int BITS>
+__device__ __forceinline__ CodeBits code_bits()
+{
+    // 4-bit: code at mantissa bits 6..9 under exponent 2^4 (16 + c);
+    // 2-bit: code at mantissa bits 8..9 under exponent 2^2 (4 + c).
+    uint32_t mask = BITS == 4 ? 0x03C003C0u : 0x03000300u;
+    uint32_t magic = BITS == 4 ? 0x4C004C00u : 0x44004400u;
+    // opaque to constant folding, so both stay in registers
+    asm volatile("" : "+v"(mask), "+v"(magic));
+    return CodeBits{mask, magic};
+}
+
+// Piece k (eight codes, code j at bits BITS j) of a lane's words -> the
+// MFMA operand (B0 + c_j, B0 + c_{j+4}) in dword j, i.e. element e holds
+// code perm4(e).
+template <int BITS>
+__device__ __forceinline__ half8 biased_codes(const uint32_t* w, int k, const CodeBits& cb)
+{
+    u32x4 v;
+    if constexpr (BITS == 4) {
+        const uint32_t x = w[k];
+        v.x = ((x << 6) & cb.mask) | cb.magic;
+        v.y = ((x << 2) & cb.mask) | cb.magic;
+        v.z = ((x >> 2) & cb.mask) | cb.magic;
+        v.w = ((x >> 6) & cb.mask) | cb.magic;
+    } else {
+        // bytes (c0..c3) and (c4..c7) of the piece to bytes 0 and 2
+        const uint32_t z = __builtin_amdgcn_perm(0u, w[k >> 1], (k & 1) ? 0x0c030c02u : 0x0c010c00u);
+        v.x = ((z << 8) & cb.mask) | cb.magic;
+        v.y = ((z << 6) & cb.mask) | cb.magic;
+        v.z = ((z << 4) & cb.mask) | cb.magic;
+        v.w = ((z << 2) & cb.mask) | cb.magic;
+    }
+    return __builtin_bit_cast(half8, v);
+}
+
+// fp32 -> fp16 hi + lo: hi is v with its binary32 mantissa cut to binary16
+// width (so v - hi is exact in binary32) and lo is that remainder, both
+// converted to nearest.  An MFMA pair over (hi, lo) carries about 22
+// significant bits; where lo falls below the binary16 normal range its
+// rounding error (at most 2^-25 absolute) is unbiased, which matters because
+// the value-side sum of biased codes times p s cancels against the offset
+// term.
+__device__ __forceinline__ void split_pairs(const float* v, half8* hi, half8* lo)
+{
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float a = __uint_as_float(__float_as_uint(v[e]) & 0xFFFFE000u);
+        (*hi)[e] = (_Float16)a;
+        (*lo)[e] = (_Float16)(v[e] - a);
+    }
+}
 
 // ------------------------------------------------------------ block loads
 
-// The metadata sections of one block, in the order they are concatenated in
-// a wave's LDS buffer: key scales, key offsets, value scales, value offsets
-// (absent offset sections have no chunks).  Fields are scalars, not arrays,
-// so that selecting a section never indexes memory.
+// Metadata of one block: nk key floats (scales; offsets alike) and nv value
+// floats, taken as nk / 4 + nv / 4 chunk pairs (scale chunk, offset chunk).
+// In the wave's LDS buffer: key scales, key offsets z', value scales, value
+// offsets z' (float4 offsets in coded_block).
 struct MetaMap {
-    const float *ks, *kz, *vs, *vz;  // section starts in the cache
-    int nks, nkz, nvs;               // floats per block (offsets absent: nkz = 0 / no vz chunks)
-    int e0, e1, e2, e3;              // cumulative 16-byte chunk counts
-    float kmul, vmul;                // factors applied when staging key and value scales
-    int l0, l1, l2, l3;              // float4 offsets in the wave buffer (absent: alias the scales)
+    const float* ks;     // key scales; the other sections are at float offsets from it
+    long dkz, dvs, dvz;  // kz - ks (0 for symmetric keys), vs - ks, vz - ks (vs - ks when symmetric)
+    int nk, nv;          // floats per block
+    int kp, np;          // key chunk pairs, all chunk pairs
+    float kmul, vmul;    // sm_scale log2(e) for keys, 2^-kTau for value scales
+    float kz0, kzs;      // key z' = kz0 z + kzs s: z - B0 s (affine) or -(2^(b-1) + B0) s (symmetric)
+    float vz0, vzs;      // value z' alike
 };
 
 template <class C>
 struct BlockRegs {
-    uint32_t k[2][C::KW];  // key pieces of the two half blocks
-    uint32_t v[C::VW];     // value pieces
-    u32x4 meta[C::NMETA];  // 16-byte metadata chunks lane + 64 u
+    uint32_t k[2][C::KW];              // key pieces of the two half blocks
+    uint32_t v[C::VW];                 // value pieces
+    u32x4 ms[C::NPAIR], mz[C::NPAIR];  // metadata chunk pairs lane + 64 u
 };
 
-// Issue every load of block `ub` (unit * NB + block) of a lane.
+// Issue every load of block `ub` (unit * NB + block) of a lane.  Every lane
+// issues the same loads whatever the format (surplus lanes re-read the last
+// chunk pair), so the number of loads in flight is fixed.
 template <class C>
 __device__ __forceinline__ void load_block(BlockRegs<C>& r, const AttnParams& p, const MetaMap& mm, size_t ub,
                                            int lane)
@@ -166,20 +231,14 @@ __device__ __forceinline__ void load_block(BlockRegs<C>& r, const AttnParams& p,
     gload_words<C::KW>(kc + 64 * C::KW, r.k[1]);
     gload_words<C::VW>(p.vc + ub * (64 * C::VW) + lane * C::VW, r.v);
 #pragma unroll
-    for (int u = 0; u < C::NMETA; ++u) {
-        const int c = lane + 64 * u;
-        if (c < mm.e3) {
-            const float* src;
-            if (c < mm.e0)
-                src = mm.ks + ub * (size_t)mm.nks + 4 * c;
-            else if (c < mm.e1)
-                src = mm.kz + ub * (size_t)mm.nkz + 4 * (c - mm.e0);
-            else if (c < mm.e2)
-                src = mm.vs + ub * (size_t)mm.nvs + 4 * (c - mm.e1);
-            else
-                src = mm.vz + ub * (size_t)mm.nvs + 4 * (c - mm.e2);
-            r.meta[u] = __builtin_nontemporal_load((const u32x4*)src);
-        }
+    for (int u = 0; u < C::NPAIR; ++u) {
+        const int c = min(lane + 64 * u, mm.np - 1);
+        const bool key = c < mm.kp;
+        // one base pointer and selected offsets keep the loads global ones
+        const long s_off = key ? (long)ub * mm.nk + 4 * c : mm.dvs + (long)ub * mm.nv + 4 * (c - mm.kp);
+        const long z_off = s_off + (key ? mm.dkz : mm.dvz - mm.dvs);
+        r.ms[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + s_off));
+        r.mz[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + z_off));
     }
 }
 
@@ -192,7 +251,7 @@ struct Split {
     float qsum[C::PERCH ? 1 : NKB];                          // sum of the 32 query channels of K-block kb
     float qf[C::PERCH ? NKB : 1][8];                         // fp32 query, operand order (per-channel keys)
     float m, lsum;                                           // running max (log2 units), lane partial sum
-    float zl[NVG];                                           // lane partials of sum_t p_t z_tg
+    float zl[NVG];                                           // lane partials of sum_t p_t z'_tg
     floatx4 oacc[NMB];
 
     __device__ __forceinline__ void init()
@@ -235,29 +294,41 @@ struct Split {
     }
 
     // One coded 32-token block whose loads are in `r`; tokens at or beyond
-    // `valid` are masked.  `wl` is the wave's metadata buffer.
+    // `valid` are masked.  `wl` is the wave's metadata buffer; `vg` the value
+    // group of this lane's column when every group has its own columns.
     __device__ __forceinline__ void coded_block(const BlockRegs<C>& r, float4* wl, const MetaMap& mm, int lane,
-                                                int lgk, bool qlo_on, half2_t kbias, half2_t vbias, int valid)
+                                                int lgk, bool qlo_on, bool rep, int vg, const CodeBits& kcb,
+                                                const CodeBits& vcb, int valid)
     {
         const int qg = lane >> 4;
-        // Stage the block's metadata in the wave's buffer: key scales and
-        // offsets times sm_scale log2(e), value scales times 2^-kTau.  LDS
-        // accesses of one wave are performed in order, so the reads below
-        // see these writes without a barrier.
+        // Stage the block's metadata: key scales and z' times sm_scale log2(e),
+        // value scales times 2^-kTau.  LDS accesses of one wave are performed
+        // in order, so the reads below see these writes without a barrier.
+        const int vp = mm.np - mm.kp;
 #pragma unroll
-        for (int u = 0; u < C::NMETA; ++u) {
+        for (int u = 0; u < C::NPAIR; ++u) {
             const int c = lane + 64 * u;
-            if (c < mm.e3) {
-                const float f = c < mm.e1 ? mm.kmul : c < mm.e2 ? mm.vmul : 1.0f;
-                const u32x4 w = r.meta[u];
-                wl[c] = float4{__uint_as_float(w.x) * f, __uint_as_float(w.y) * f, __uint_as_float(w.z) * f,
-                               __uint_as_float(w.w) * f};
+            if (c < mm.np) {
+                const bool key = c < mm.kp;
+                const float f = key ? mm.kmul : 1.0f;
+                const float fs = key ? mm.kmul : mm.vmul;
+                const float z0 = key ? mm.kz0 : mm.vz0, zs = key ? mm.kzs : mm.vzs;
+                const u32x4 s = r.ms[u], z = r.mz[u];
+                const float sv[4] = {__uint_as_float(s.x), __uint_as_float(s.y), __uint_as_float(s.z),
+                                     __uint_as_float(s.w)};
+                const float zv[4] = {__uint_as_float(z.x), __uint_as_float(z.y), __uint_as_float(z.z),
+                                     __uint_as_float(z.w)};
+                const int ds = key ? c : 2 * mm.kp + (c - mm.kp);
+                const int dz = key ? mm.kp + c : 2 * mm.kp + vp + (c - mm.kp);
+                wl[ds] = float4{sv[0] * fs, sv[1] * fs, sv[2] * fs, sv[3] * fs};
+                wl[dz] = float4{(z0 * zv[0] + zs * sv[0]) * f, (z0 * zv[1] + zs * sv[1]) * f,
+                                (z0 * zv[2] + zs * sv[2]) * f, (z0 * zv[3] + zs * sv[3]) * f};
             }
         }
-        const float4* ks = wl + mm.l0;
-        const float4* kz = wl + mm.l1;
-        const float4* vs = wl + mm.l2;
-        const float4* vz = wl + mm.l3;
+        const float4* ks = wl;
+        const float4* kz = wl + mm.kp;
+        const float4* vs = wl + 2 * mm.kp;
+        const float4* vz = wl + 2 * mm.kp + vp;
 
         // ---------------------------------------------------- scores
         float l[8];
@@ -268,7 +339,7 @@ struct Split {
                 floatx4 acc[NKB];
 #pragma unroll
                 for (int kb = 0; kb < NKB; ++kb) {
-                    a[kb] = codes_to_half8<C::KBITS>(piece<C::KBITS>(r.k[h2], kb), kbias);
+                    a[kb] = biased_codes<C::KBITS>(r.k[h2], kb, kcb);
                     acc[kb] = mfma16(a[kb], qhi[kb], floatx4{0.0f, 0.0f, 0.0f, 0.0f});
                 }
                 if (qlo_on) {
@@ -291,7 +362,7 @@ struct Split {
                     l[4 * h2 + i] = S[i];
             }
         } else {
-            // Per-channel keys: B = q * s_d (hi + lo), and sum_d q_d z_d per head.
+            // Per-channel keys: B = q * s_d (hi + lo), and sum_d q_d z'_d per head.
             half8 bh[NKB], bl[NKB];
             float zq = 0.0f;
 #pragma unroll
@@ -306,15 +377,15 @@ struct Split {
                     v[e] = qf[kb][e] * sn[perm4(e)];
                     zq += qf[kb][e] * zn[perm4(e)];
                 }
-                split_half8(v, &bh[kb], &bl[kb]);
+                split_pairs(v, &bh[kb], &bl[kb]);
             }
-            zq = sum_rows(zq) * qsum[0];  // qsum[0] is 1 for affine keys, 0 for symmetric keys
+            zq = sum_rows(zq);
 #pragma unroll
             for (int h2 = 0; h2 < 2; ++h2) {
                 floatx4 acc = {zq, zq, zq, zq};
 #pragma unroll
                 for (int kb = 0; kb < NKB; ++kb) {
-                    const half8 a = codes_to_half8<C::KBITS>(piece<C::KBITS>(r.k[h2], kb), kbias);
+                    const half8 a = biased_codes<C::KBITS>(r.k[h2], kb, kcb);
                     acc = mfma16(a, bh[kb], acc);
                     acc = mfma16(a, bl[kb], acc);
                 }
@@ -323,36 +394,42 @@ struct Split {
                     l[4 * h2 + i] = acc[i];
             }
         }
+        if (valid < 32) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k)
-            l[k] = 8 * qg + k < valid ? l[k] : kNegInf;
+            for (int k = 0; k < 8; ++k)
+                l[k] = 8 * qg + k < valid ? l[k] : kNegInf;
+        }
         softmax(l);  // l now holds p (<= 2^kTau), 0 for masked tokens
 
         // ---------------------------------------------------- values
         // Masked tokens have p = 0 and finite metadata (the storage starts
         // zero-filled and is only ever written with finite values), so their
-        // terms vanish without a select.
+        // terms vanish without a select.  With one column set per group the
+        // B operand built in the first pass holds every group.
+        half8 ph, pl;
 #pragma unroll
-        for (int g = 0; g < NVG; ++g) {
-            const float4 s0 = vs[8 * g + 2 * qg], s1 = vs[8 * g + 2 * qg + 1];
-            const float4 z0 = vz[8 * g + 2 * qg], z1 = vz[8 * g + 2 * qg + 1];
-            const float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-            const float zn[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-            float pv[8];
-            float zs = 0.0f;
+        for (int pass = 0; pass < NVG; ++pass) {
+            if (pass == 0 || !rep) {
+                const int g = rep ? vg : pass;
+                const float4 s0 = vs[8 * g + 2 * qg], s1 = vs[8 * g + 2 * qg + 1];
+                const float4 z0 = vz[8 * g + 2 * qg], z1 = vz[8 * g + 2 * qg + 1];
+                const float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+                const float zn[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+                float pv[8];
+                float zs = 0.0f;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int k = perm4(e);
-                pv[e] = l[k] * sn[k];
-                zs += l[k] * zn[k];
+                for (int e = 0; e < 8; ++e) {
+                    const int k = perm4(e);
+                    pv[e] = l[k] * sn[k];
+                    zs += l[k] * zn[k];
+                }
+                zl[pass] += zs;
+                split_pairs(pv, &ph, &pl);
             }
-            zl[g] += zs;
-            half8 ph, pl;
-            split_half8(pv, &ph, &pl);
 #pragma unroll
             for (int j = 0; j < C::MBPG; ++j) {
-                const int mb = g * C::MBPG + j;
-                const half8 a = codes_to_half8<C::VBITS>(piece<C::VBITS>(r.v, mb), vbias);
+                const int mb = pass * C::MBPG + j;
+                const half8 a = biased_codes<C::VBITS>(r.v, mb, vcb);
                 oacc[mb] = mfma16(a, ph, oacc[mb]);
                 oacc[mb] = mfma16(a, pl, oacc[mb]);
             }
@@ -372,25 +449,29 @@ struct Split {
         for (int h2 = 0; h2 < 2; ++h2) {
             const int tA = t0 + 8 * (hh >> 2) + 4 * h2 + (hh & 3);
             const uint16_t* krow = p.kr + (rbase + (size_t)(tA % ring)) * D;
-            floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            half8 a[NKB];
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) {
-                half8 a = {};
+                a[kb] = half8{};
                 if (tA < n) {
                     const half8 nat = __builtin_bit_cast(half8, *(const u32x4*)(krow + 32 * kb + 8 * qg));
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
-                        a[e] = nat[perm4(e)];
+                        a[kb][e] = nat[perm4(e)];
                 }
+            }
+            floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
                 if constexpr (C::PERCH) {
                     half8 bh, bl;
-                    split_half8(qf[kb], &bh, &bl);
-                    acc = mfma16(a, bh, acc);
-                    acc = mfma16(a, bl, acc);
+                    split_pairs(qf[kb], &bh, &bl);
+                    acc = mfma16(a[kb], bh, acc);
+                    acc = mfma16(a[kb], bl, acc);
                 } else {
-                    acc = mfma16(a, qhi[kb], acc);
+                    acc = mfma16(a[kb], qhi[kb], acc);
                     if (qlo_on)
-                        acc = mfma16(a, qlo[kb], acc);
+                        acc = mfma16(a[kb], qlo[kb], acc);
                 }
             }
 #pragma unroll
@@ -410,19 +491,22 @@ struct Split {
         for (int e = 0; e < 8; ++e)
             pv[e] = slot[perm4(e)] >= 0 ? l[perm4(e)] * kPScale : 0.0f;
         half8 ph, pl;
-        split_half8(pv, &ph, &pl);
+        split_pairs(pv, &ph, &pl);
+        half8 va[NMB];
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb) {
             const int d = 16 * mb + hh;
-            half8 a;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int sl = slot[perm4(e)];
                 const uint16_t raw = sl >= 0 ? p.vr[(rbase + (size_t)sl) * D + d] : (uint16_t)0;
-                a[e] = __builtin_bit_cast(_Float16, raw);
+                va[mb][e] = __builtin_bit_cast(_Float16, raw);
             }
-            oacc[mb] = mfma16(a, ph, oacc[mb]);
-            oacc[mb] = mfma16(a, pl, oacc[mb]);
+        }
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) {
+            oacc[mb] = mfma16(va[mb], ph, oacc[mb]);
+            oacc[mb] = mfma16(va[mb], pl, oacc[mb]);
         }
     }
 };
@@ -449,13 +533,6 @@ __device__ __forceinline__ void finish_rows(const AttnParams& p, float* xo, size
         p.out[row0 * D + idx] = xo[idx] * post;
 }
 
-// Floats of the per-wave metadata buffer.
-template <class C>
-constexpr int meta_floats()
-{
-    return 256 * C::NMETA;
-}
-
 template <class C>
 __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
 {
@@ -471,26 +548,33 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     const int NB = p.T >> 5;
     const int lgk = C::PERCH ? 0 : __builtin_ctz((unsigned)p.k_group >> 5);  // log2(key group / 32)
     const int kmeta = C::PERCH ? D : 32 * (D / p.k_group);                    // key scale floats per block
+    constexpr int vmeta = 32 * C::NVG;
+
+    // Column roles: with one column set per value group, column hh is head
+    // hh % G of value group hh / G; otherwise head hh.
+    const bool rep = G * C::NVG <= 16 && C::NVG > 1;
+    const int vg = rep ? hh / G : 0;
+    const int head = rep ? hh - vg * G : hh;
+    const bool active = rep ? vg < C::NVG : hh < G;
 
     MetaMap mm;
     mm.ks = p.ks;
-    mm.kz = p.kz;
-    mm.vs = p.vs;
-    mm.vz = p.vz;
-    mm.nks = kmeta;
-    mm.nkz = kaff ? kmeta : 0;
-    mm.nvs = 32 * C::NVG;
-    mm.e0 = kmeta / 4;
-    mm.e1 = mm.e0 + mm.nkz / 4;
-    mm.e2 = mm.e1 + mm.nvs / 4;
-    mm.e3 = mm.e2 + (vaff ? mm.nvs / 4 : 0);
+    mm.dkz = kaff ? p.kz - p.ks : 0;
+    mm.dvs = p.vs - p.ks;
+    mm.dvz = vaff ? p.vz - p.ks : mm.dvs;
+    mm.nk = kmeta;
+    mm.nv = vmeta;
+    mm.kp = kmeta / 4;
+    mm.np = mm.kp + vmeta / 4;
     mm.kmul = p.sm_log2;
     mm.vmul = kPScale;
-    // absent offset sections alias the scales (their terms get a zero weight)
-    mm.l0 = 0;
-    mm.l1 = kaff ? mm.e0 : 0;
-    mm.l2 = mm.e1;
-    mm.l3 = vaff ? mm.e2 : mm.e1;
+    {
+        const float kb0 = code_bias<C::KBITS>(), vb0 = code_bias<C::VBITS>();
+        mm.kz0 = kaff ? 1.0f : 0.0f;
+        mm.kzs = kaff ? -kb0 : -((float)(1 << (C::KBITS - 1)) + kb0);
+        mm.vz0 = vaff ? 1.0f : 0.0f;
+        mm.vzs = vaff ? -vb0 : -((float)(1 << (C::VBITS - 1)) + vb0);
+    }
 
     // ---- block range of this split
     const int nblk = (p.nq + 31) >> 5;
@@ -511,8 +595,8 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     }
     BlockRegs<C> ra, rb;
     int blk = blk_begin + wave;
-    if (blk < blk_end)
-        load_block<C>(ra, p, mm, ub0 + blk, lane);
+    if (blk_end > blk_begin)
+        load_block<C>(ra, p, mm, ub0 + min(blk, blk_end - 1), lane);
     float* lq = (float*)lds;
 #pragma unroll
     for (int u = 0; u < QLOADS; ++u) {
@@ -551,7 +635,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
         float part = 0.0f;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-            v[k] = lq[hh * D + 32 * kb + 8 * qg + perm4(k)];
+            v[k] = active ? lq[head * D + 32 * kb + 8 * qg + perm4(k)] : 0.0f;
             part += v[k];
         }
         if constexpr (C::PERCH) {
@@ -559,32 +643,26 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
             for (int k = 0; k < 8; ++k)
                 S.qf[kb][k] = v[k];
         } else {
-            split_half8(v, &S.qhi[kb], &S.qlo[kb]);
-            S.qsum[kb] = kaff ? sum_rows(part) : 0.0f;  // offset terms vanish for symmetric keys
+            split_pairs(v, &S.qhi[kb], &S.qlo[kb]);
+            S.qsum[kb] = sum_rows(part);
         }
     }
-    if constexpr (C::PERCH)
-        S.qsum[0] = kaff ? 1.0f : 0.0f;
     __syncthreads();  // the metadata buffers overwrite the query rows
 
-    const _Float16 kb16 = (_Float16)(1024 + (kaff ? 0 : (1 << (C::KBITS - 1))));
-    const _Float16 vb16 = (_Float16)(1024 + (vaff ? 0 : (1 << (C::VBITS - 1))));
-    const half2_t kbias = {kb16, kb16}, vbias = {vb16, vb16};
-
+    const CodeBits kcb = code_bits<C::KBITS>(), vcb = code_bits<C::VBITS>();
     if (!ring_split) {
-        float4* wl = (float4*)lds + wave * (meta_floats<C>() / 4);
+        float4* wl = (float4*)lds + wave * (128 * C::NPAIR);
         // Two register sets alternate: the next block's loads fly while
-        // this one is computed.
+        // this one is computed (past the end they re-read the last block).
+        const int last = blk_end - 1;
         while (blk < blk_end) {
-            if (blk + kWaves < blk_end)
-                load_block<C>(rb, p, mm, ub0 + blk + kWaves, lane);
-            S.coded_block(ra, wl, mm, lane, lgk, qlo_on, kbias, vbias, min(32, p.nq - 32 * blk));
+            load_block<C>(rb, p, mm, ub0 + min(blk + kWaves, last), lane);
+            S.coded_block(ra, wl, mm, lane, lgk, qlo_on, rep, vg, kcb, vcb, min(32, p.nq - 32 * blk));
             blk += kWaves;
             if (blk >= blk_end)
                 break;
-            if (blk + kWaves < blk_end)
-                load_block<C>(ra, p, mm, ub0 + blk + kWaves, lane);
-            S.coded_block(rb, wl, mm, lane, lgk, qlo_on, kbias, vbias, min(32, p.nq - 32 * blk));
+            load_block<C>(ra, p, mm, ub0 + min(blk + kWaves, last), lane);
+            S.coded_block(rb, wl, mm, lane, lgk, qlo_on, rep, vg, kcb, vcb, min(32, p.nq - 32 * blk));
             blk += kWaves;
         }
     } else {
@@ -598,23 +676,29 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     float zl[C::NVG];
 #pragma unroll
     for (int g = 0; g < C::NVG; ++g)
-        zl[g] = vaff ? sum_rows(S.zl[g]) : 0.0f;
+        zl[g] = sum_rows(S.zl[g]);
     __syncthreads();
     float* lm = (float*)lds;           // [4][16] running max per wave and head
     float* ll = lm + kWaves * 16;      // [4][16] softmax sums
     float* lo = lm + 2 * kWaves * 16;  // [4][G][D] unnormalized outputs
     float* xo = lo;  // [G][D] result: element idx is written after its own four reads
-    if (qg == 0) {
-        lm[wave * 16 + hh] = S.m;
-        ll[wave * 16 + hh] = lsum;
+    if (qg == 0 && vg == 0 && active) {
+        lm[wave * 16 + head] = S.m;
+        ll[wave * 16 + head] = lsum;
     }
-    if (hh < G) {
+    if (active) {
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb)
+        for (int mb = 0; mb < NMB; ++mb) {
+            const int g = mb / C::MBPG;
+            // with one column set per group, a column holds its own group's channels
+            if (!rep || g == vg) {
+                const float z = ring_split ? 0.0f : zl[rep ? 0 : g];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                lo[((size_t)wave * G + hh) * D + 16 * mb + 4 * qg + i] =
-                    S.oacc[mb][i] * (1.0f / kPScale) + zl[mb / C::MBPG];
+                for (int i = 0; i < 4; ++i)
+                    lo[((size_t)wave * G + head) * D + 16 * mb + 4 * qg + i] =
+                        S.oacc[mb][i] * (1.0f / kPScale) + z;
+            }
+        }
     }
     __syncthreads();
     const bool single = p.S_tot == 1;
@@ -649,8 +733,16 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     finish_rows<D>(p, xo, row0, G);
 }
 
+// Waves per SIMD the register allocation is held to: 3 at head_dim 64 (the
+// block state fits without spills), fewer for wider heads.
 template <class C>
-__global__ __launch_bounds__(kThreads) void decode_split_kernel(AttnParams p)
+constexpr int split_waves_per_simd()
+{
+    return C::D == 64 ? 3 : C::D == 128 ? 2 : 1;
+}
+
+template <class C>
+__global__ __launch_bounds__(kThreads, split_waves_per_simd<C>()) void decode_split_kernel(AttnParams p)
 {
     extern __shared__ float lds_f[];
     split_body<C>(p, (uint8_t*)lds_f);
@@ -708,6 +800,26 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(AttnParams p)
     finish_rows<D>(p, xo, row0, G);
 }
 
+// Workgroups of the split kernel instance for `p` that fit on one compute
+// unit at once (occupancy from its registers and LDS).  The answer is cached
+// per instance, keyed by the LDS size.
+template <class C>
+int resident_per_cu(const AttnParams& p)
+{
+    static std::atomic<unsigned long long> cache{0};  // (lds_bytes << 32) | count, 0 = empty
+    const unsigned long long lds = (unsigned long long)p.lds_bytes;
+    const unsigned long long hit = cache.load(std::memory_order_relaxed);
+    if (hit != 0 && (hit >> 32) == lds)
+        return (int)(hit & 0xFFFFFFFFu);
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_split_kernel<C>, kThreads, p.lds_bytes) != hipSuccess)
+        n = 1;
+    if (n < 1)
+        n = 1;
+    cache.store((lds << 32) | (unsigned)n, std::memory_order_relaxed);
+    return n;
+}
+
 template <class C>
 hipError_t launch_split(const AttnParams& p, hipStream_t stream)
 {
@@ -715,31 +827,52 @@ hipError_t launch_split(const AttnParams& p, hipStream_t stream)
     return hipGetLastError();
 }
 
-template <int D, int KB, int VB, bool PC, int VGS = 0>
-hipError_t launch_groups(const AttnParams& p, hipStream_t stream)
+// Calls F<Cfg<...>>::run(p, args...) for the instance that serves p.
+template <template <class> class F, int D, int KB, int VB, bool PC, int VGS = 0, class... A>
+auto by_groups(const AttnParams& p, A... args)
 {
-    if constexpr ((32 << VGS) > D) {
-        return hipErrorInvalidValue;
+    if constexpr ((32 << VGS) >= D) {
+        return F<Cfg<D, KB, VB, PC, VGS>>::run(p, args...);
     } else {
         if (p.v_group == (32 << VGS))
-            return launch_split<Cfg<D, KB, VB, PC, VGS>>(p, stream);
-        return launch_groups<D, KB, VB, PC, VGS + 1>(p, stream);
+            return F<Cfg<D, KB, VB, PC, VGS>>::run(p, args...);
+        return by_groups<F, D, KB, VB, PC, VGS + 1>(p, args...);
     }
+}
+
+template <template <class> class F, int D, class... A>
+auto by_format(const AttnParams& p, A... args)
+{
+    const bool pc = p.k_axis == KVQ_PER_CHANNEL;
+    if (p.k_bits == 4 && p.v_bits == 4)
+        return pc ? by_groups<F, D, 4, 4, true>(p, args...) : by_groups<F, D, 4, 4, false>(p, args...);
+    if (p.k_bits == 4 && p.v_bits == 2)
+        return pc ? by_groups<F, D, 4, 2, true>(p, args...) : by_groups<F, D, 4, 2, false>(p, args...);
+    if (p.k_bits == 2 && p.v_bits == 4)
+        return pc ? by_groups<F, D, 2, 4, true>(p, args...) : by_groups<F, D, 2, 4, false>(p, args...);
+    return pc ? by_groups<F, D, 2, 2, true>(p, args...) : by_groups<F, D, 2, 2, false>(p, args...);
+}
+
+template <class C>
+struct LaunchSplit {
+    static hipError_t run(const AttnParams& p, hipStream_t stream) { return launch_split<C>(p, stream); }
+};
+
+template <class C>
+struct Resident {
+    static int run(const AttnParams& p) { return resident_per_cu<C>(p); }
+};
+
+template <int D>
+int resident_d(const AttnParams& p)
+{
+    return by_format<Resident, D>(p);
 }
 
 template <int D>
 hipError_t launch_decode_d(const AttnParams& p, hipStream_t stream)
 {
-    hipError_t e;
-    const bool pc = p.k_axis == KVQ_PER_CHANNEL;
-    if (p.k_bits == 4 && p.v_bits == 4)
-        e = pc ? launch_groups<D, 4, 4, true>(p, stream) : launch_groups<D, 4, 4, false>(p, stream);
-    else if (p.k_bits == 4 && p.v_bits == 2)
-        e = pc ? launch_groups<D, 4, 2, true>(p, stream) : launch_groups<D, 4, 2, false>(p, stream);
-    else if (p.k_bits == 2 && p.v_bits == 4)
-        e = pc ? launch_groups<D, 2, 4, true>(p, stream) : launch_groups<D, 2, 4, false>(p, stream);
-    else
-        e = pc ? launch_groups<D, 2, 2, true>(p, stream) : launch_groups<D, 2, 2, false>(p, stream);
+    const hipError_t e = by_format<LaunchSplit, D>(p, stream);
     if (e != hipSuccess || p.S_tot == 1)
         return e;
     hipLaunchKernelGGL(decode_merge_kernel<D>, dim3(p.B * p.H), dim3(kThreads),

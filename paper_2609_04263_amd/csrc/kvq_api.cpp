@@ -90,7 +90,7 @@ float rotation_constant(int D)
 // cache can need (the split count of a call never exceeds it).
 size_t decode_workspace_layout(const kvq_cache* c, int H_q, size_t* off_ml)
 {
-    int S_max = kvq::decode_split_bound(c->B, c->H, c->D, c->fmt, kvq::num_coded(c->fmt, c->T_max)) + (c->fmt.flush ? 1 : 0);
+    int S_max = kvq::decode_split_bound(c->B, c->H) + (c->fmt.flush ? 1 : 0);
     size_t rows = (size_t)c->B * H_q;
     size_t o_ml = round_up(rows * S_max * c->D * sizeof(float), 256);
     if (off_ml)
@@ -356,8 +356,6 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     const kvq_format& f = c->fmt;
     kvq::AttnParams p = {};
     p.nq = kvq::num_coded(f, c->n);
-    kvq::decode_plan(c->B, c->H, c->D, f, p.nq, &p.S_q, &p.bps);
-    p.S_tot = p.S_q + (f.flush ? 1 : 0);
     size_t off_ml;
     const size_t need = decode_workspace_layout(c, H_q, &off_ml);
     if (ws_bytes < need)
@@ -392,6 +390,8 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.sm_log2 = sm_scale * 1.4426950408889634f;
     p.rot_c = rotation_constant(c->D);
     p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.G);
+    kvq::decode_plan(c->B, c->H, kvq::decode_target_groups(p, c->D), p.nq, &p.S_q, &p.bps);
+    p.S_tot = p.S_q + (f.flush ? 1 : 0);
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 

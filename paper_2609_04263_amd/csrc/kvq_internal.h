@@ -89,10 +89,14 @@ struct AttnParams {
     float rot_c;
     size_t lds_bytes;     // dynamic LDS of the split kernel
 };
-// Split count and 32-token blocks per split over nq coded tokens.
-void decode_plan(int B, int H, int D, const kvq_format& f, int nq, int* S_q, int* bps);
-// Upper bound of S_q over every coded-token count up to nq.
-int decode_split_bound(int B, int H, int D, const kvq_format& f, int nq);
+// Workgroups of the split kernel that fit the device at once (all fields of p
+// that select the kernel instance and its LDS must be set).
+int decode_target_groups(const AttnParams& p, int D);
+// Split count and 32-token blocks per split over nq coded tokens for a
+// target number of workgroups.
+void decode_plan(int B, int H, int groups, int nq, int* S_q, int* bps);
+// Upper bound of S_q for any coded-token count and target.
+int decode_split_bound(int B, int H);
 // Dynamic LDS of the split kernel.
 size_t decode_lds_bytes(int D, const kvq_format& f, int G);
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
