@@ -748,56 +748,79 @@ __global__ __launch_bounds__(kThreads, split_waves_per_simd<C>()) void decode_sp
     split_body<C>(p, (uint8_t*)lds_f);
 }
 
-// Merge the S_tot split partials of one (sequence, KV head): per head, the
-// weights w_s = 2^(m_s - M) / sum_s' 2^(m_s' - M) l_s' go to LDS, then every
-// output is a weighted sum over splits of coalesced partial rows; finally
-// rotate back and store.
+// Merge the S_tot split partials: one thread per output element (row, d),
+// 256 / D rows per workgroup.  A thread reads the partials of its row in
+// chunks of kMergeChunk splits, all loads of a chunk in flight together,
+// and combines them online: O = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
+// The rows are then rotated back when the format rotates, and stored.
+constexpr int kMergeChunk = 16;
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void decode_merge_kernel(AttnParams p)
 {
-    extern __shared__ float sm[];
-    const int unit = blockIdx.x;
-    const int b = unit / p.H, j = unit % p.H, G = p.G, S = p.S_tot;
-    const size_t row0 = (size_t)b * p.H_q + (size_t)j * G;
-    float* w = sm;               // [G][S]: (max, sum) pairs, then weights
-    float* xo = sm + 2 * G * S;  // [G][D]
-    const float* ml = p.part_ml + row0 * S * 2;
-    for (int idx = threadIdx.x; idx < 2 * G * S; idx += kThreads)
-        w[idx] = ml[idx];
-    __syncthreads();
-    if (threadIdx.x < (unsigned)G) {
-        float* r = w + 2 * S * threadIdx.x;
-        float M = kNegInf;
-        for (int s = 0; s < S; ++s)
-            M = fmaxf(M, r[2 * s]);
-        float Ls = 0.0f;
-        for (int s = 0; s < S; ++s)
-            Ls += r[2 * s] == kNegInf ? 0.0f : fast_exp2(r[2 * s] - M) * r[2 * s + 1];
-        const float inv = 1.0f / Ls;
-        for (int s = 0; s < S; ++s) {
-            const float m = r[2 * s];
-            r[2 * s] = m == kNegInf ? 0.0f : fast_exp2(m - M) * inv;  // weights overwrite maxima
+    constexpr int R = kThreads / D;  // rows per workgroup
+    __shared__ float xo[kThreads];
+    const int t = threadIdx.x, rl = t / D, d = t % D;
+    const size_t rows = (size_t)p.B * p.H_q;
+    const size_t row = (size_t)blockIdx.x * R + rl;
+    const int S = p.S_tot;
+    float Mx = kNegInf, acc = 0.0f, Ls = 0.0f;
+    if (row < rows) {
+        const float* ml = p.part_ml + row * S * 2;
+        const float* po = p.part_o + row * S * D + d;
+        for (int s0 = 0; s0 < S; s0 += kMergeChunk) {
+            float m[kMergeChunk], l[kMergeChunk], o[kMergeChunk];
+#pragma unroll
+            for (int k = 0; k < kMergeChunk; ++k) {
+                const bool in = s0 + k < S;
+                const int s = in ? s0 + k : s0;
+                m[k] = ml[2 * s];
+                l[k] = ml[2 * s + 1];
+                o[k] = po[(size_t)s * D];
+                if (!in)
+                    m[k] = kNegInf;
+            }
+            float cm = kNegInf;
+#pragma unroll
+            for (int k = 0; k < kMergeChunk; ++k)
+                cm = fmaxf(cm, m[k]);
+            const float nm = fmaxf(Mx, cm);
+            if (nm != kNegInf) {
+                const float sc = Mx == kNegInf ? 0.0f : fast_exp2(Mx - nm);
+                acc *= sc;
+                Ls *= sc;
+#pragma unroll
+                for (int k = 0; k < kMergeChunk; ++k) {
+                    const float w = m[k] == kNegInf ? 0.0f : fast_exp2(m[k] - nm);
+                    acc += w * o[k];
+                    Ls += w * l[k];
+                }
+                Mx = nm;
+            }
         }
     }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
-        const int h = idx / D, d = idx % D;
-        const float* o = p.part_o + ((row0 + h) * S) * D + d;
-        const float* wr = w + 2 * S * h;
-        float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
-        int s = 0;
-        for (; s + 4 <= S; s += 4) {
-            acc0 += wr[2 * s] * o[(size_t)s * D];
-            acc1 += wr[2 * s + 2] * o[(size_t)(s + 1) * D];
-            acc2 += wr[2 * s + 4] * o[(size_t)(s + 2) * D];
-            acc3 += wr[2 * s + 6] * o[(size_t)(s + 3) * D];
-        }
-        for (; s < S; ++s)
-            acc0 += wr[2 * s] * o[(size_t)s * D];
-        xo[idx] = (acc0 + acc1) + (acc2 + acc3);
+    const float v = row < rows ? acc / Ls : 0.0f;
+    if (!p.rotate) {
+        if (row < rows)
+            p.out[row * D + d] = v;
+        return;
     }
+    // inverse rotation of the R rows in LDS (the normalized transform is its own inverse)
+    xo[t] = v;
     __syncthreads();
-    finish_rows<D>(p, xo, row0, G);
+    for (int h = 1; h < D; h <<= 1) {
+        float nv = 0.0f;
+        if (t < R * D) {
+            const int partner = (d & h) ? t - h : t + h;
+            const float a = xo[t], c = xo[partner];
+            nv = (d & h) ? c - a : a + c;
+        }
+        __syncthreads();
+        xo[t] = nv;
+        __syncthreads();
+    }
+    if (row < rows)
+        p.out[row * D + d] = xo[t] * p.rot_c;
 }
 
 // Workgroups of the split kernel instance for `p` that fit on one compute
@@ -875,8 +898,8 @@ hipError_t launch_decode_d(const AttnParams& p, hipStream_t stream)
     const hipError_t e = by_format<LaunchSplit, D>(p, stream);
     if (e != hipSuccess || p.S_tot == 1)
         return e;
-    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3(p.B * p.H), dim3(kThreads),
-                       (size_t)(2 * p.S_tot + D) * p.G * sizeof(float), stream, p);
+    const int rows = p.B * p.H_q, per = kThreads / D;
+    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3((rows + per - 1) / per), dim3(kThreads), 0, stream, p);
     return hipGetLastError();
 }
 
