@@ -254,6 +254,25 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
     }
     hipStream_t s = (hipStream_t)stream;
     const int N = d_q + 2 * d_kv;
+    if (M <= 32) {
+        // decode: one fused kernel computes the adapter activations itself
+        kvq::ProjParams p = {};
+        p.x = (const uint16_t*)H;
+        p.w = (const uint16_t*)W;
+        p.a = (const uint16_t*)A;
+        p.bm = (const uint16_t*)Bm;
+        p.y0 = (uint16_t*)Q;
+        p.y1 = (uint16_t*)K;
+        p.y2 = (uint16_t*)V;
+        p.M = M;
+        p.K = d_in;
+        p.N = N;
+        p.n1 = d_q;
+        p.n2 = d_q + d_kv;
+        p.rank = rank;
+        p.scale = lora_scale;
+        return kvq::launch_project(p, s) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+    }
     if (rank > 0) {
         kvq::ProjParams a = {};
         a.x = (const uint16_t*)H;

@@ -51,7 +51,8 @@ struct ProjParams {
     const uint16_t* x;    // bf16 [M][K]  (hidden states)
     const uint16_t* w;    // bf16 [N][K]  (weight rows)
     const uint16_t* bm;   // bf16 [N][rank] adapter up-projection rows (rank > 0)
-    const float* t;       // fp32 [M][3 rank] scaled adapter activations (rank > 0)
+    const float* t;       // fp32 [M][3 rank] scaled adapter activations (rank > 0, two-pass path)
+    const uint16_t* a;    // bf16 [3 rank][K] adapter down-projections (rank > 0, fused decode path)
     uint16_t* y0;         // bf16 outputs: columns [0, n1) -> y0, [n1, n2) -> y1, [n2, N) -> y2
     uint16_t* y1;
     uint16_t* y2;
@@ -59,7 +60,7 @@ struct ProjParams {
     int M, K, N;
     int n1, n2;           // column split points (d_q, d_q + d_kv)
     int rank;
-    float scale;          // multiplies the fp32 output (activation pass)
+    float scale;          // multiplies the fp32 output (activation pass); the adapter scale (fused path)
 };
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
 

@@ -7,10 +7,14 @@
 //      of the same accumulators: t_p (split into bf16 hi + lo parts) times
 //      B_p^T, then one rounding to bf16 and routing of the columns to Q/K/V.
 //
-// M <= 32 (decode: one token per sequence) streams the weights from HBM with
-// a skinny kernel: a workgroup owns 16 weight rows and its four waves split
-// the reduction dimension, keeping many 16-byte loads in flight.  Larger M
-// (prefill) uses a 128x128 tiled GEMM staged through LDS.
+// M <= 32 (decode: one token per sequence) runs as one fused kernel that
+// streams the weights from HBM: a workgroup owns 16 weight rows and its
+// eight waves split the reduction dimension, each issuing its 16-byte loads
+// of W, H and the adapter rows A_p in one batch.  The same H fragments feed
+// both Y = H W^T and the adapter activations t = H A_p^T (its own copy per
+// workgroup: the adapter rows are small and stay in L2), which are reduced
+// across waves in LDS and applied as the K-extension.  Larger M (prefill)
+// uses the two passes with a 128x128 tiled GEMM staged through LDS.
 
 #include "kvq_device.h"
 #include "kvq_internal.h"
@@ -106,78 +110,165 @@ __device__ __forceinline__ bf16x8 lora_weight_operand(const ProjParams& p, int n
     return __builtin_bit_cast(bf16x8, a);
 }
 
-// ------------------------------------------------------------------ skinny
-// Workgroup: weight rows [n0, n0 + 16) x all M (<= 32) tokens.
-// MFMA roles: A = W rows (M-dim = 16 weight rows), B = H^T (N-dim = 16 tokens).
-// Output lane layout: token = 16 nt + (lane % 16), row n0 + 4 qg + i.
-constexpr int kSkinnyUnroll = 8;
+// ----------------------------------------------------------- fused decode
+// Workgroup: weight rows [n0, n0 + 16) x all M (<= 16 MT) tokens, 8 waves.
+// MFMA roles: Y: A = W rows (16 weight rows), B = H^T (16 tokens);
+//             t: A = H rows (16 tokens), B = A_p^T (16 adapter rows).
+// Output lane layout: token = 16 mt + (lane % 16), row n0 + 4 qg + i.
+constexpr int kDecWaves = 8;
 
-__global__ __launch_bounds__(kThreads) void proj_skinny_kernel(ProjParams p)
+template <int MT, int NKT>
+__global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams p)
 {
-    __shared__ floatx4 red[4][2][64];
+    constexpr int U = (MT + NKT <= 2) ? 8 : 4;   // K-steps per load batch
+    constexpr int NV = MT * (1 + NKT);           // floatx4 partials per lane
+    constexpr int NKK = (16 * NKT + 31) / 32;    // 32-wide rank chunks of the K-extension
+    extern __shared__ floatx4 red[];             // [kDecWaves][NV][64], then t [16 MT][16 NKT]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, qg = lane >> 4;
     const int n0 = blockIdx.x * 16;
-    const int nt_count = p.M > 16 ? 2 : 1;
+    const int proj = proj_of(p, n0);  // tiles never straddle projections (d_q, d_kv multiples of 16)
     const int steps = p.K / 32;
-    const int per = (steps + 3) / 4;
+    const int per = (steps + kDecWaves - 1) / kDecWaves;
     const int s_begin = wave * per, s_end = min(steps, s_begin + per);
 
-    const int wrow = n0 + r;
-    const uint16_t* wp = p.w + (size_t)min(wrow, p.N - 1) * p.K + 8 * qg;
-    const bool wok = wrow < p.N;
-    const uint16_t* xp0 = p.x + (size_t)min(r, p.M - 1) * p.K + 8 * qg;
-    const uint16_t* xp1 = p.x + (size_t)min(16 + r, p.M - 1) * p.K + 8 * qg;
-    const bool x0ok = r < p.M, x1ok = 16 + r < p.M;
-
-    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    for (int s = s_begin; s < s_end; s += kSkinnyUnroll) {
-        bf16x8 a[kSkinnyUnroll], b0[kSkinnyUnroll], b1[kSkinnyUnroll];
+    const uint16_t* wp = p.w + (size_t)min(n0 + r, p.N - 1) * p.K + 8 * qg;
+    const bool wok = n0 + r < p.N;
+    const uint16_t* xp[MT];
+    bool xok[MT];
 #pragma unroll
-        for (int u = 0; u < kSkinnyUnroll; ++u) {
-            int ss = s + u;
-            bool in = ss < s_end;
-            a[u] = (in && wok) ? load_bf16x8(wp + 32 * ss) : zero_bf16x8();
-            b0[u] = (in && x0ok) ? load_bf16x8(xp0 + 32 * ss) : zero_bf16x8();
-            b1[u] = (in && x1ok && nt_count > 1) ? load_bf16x8(xp1 + 32 * ss) : zero_bf16x8();
-        }
-#pragma unroll
-        for (int u = 0; u < kSkinnyUnroll; ++u) {
-            acc0 = mfma16_bf16(a[u], b0[u], acc0);
-            if (nt_count > 1)
-                acc1 = mfma16_bf16(a[u], b1[u], acc1);
-        }
+    for (int mt = 0; mt < MT; ++mt) {
+        xp[mt] = p.x + (size_t)min(16 * mt + r, p.M - 1) * p.K + 8 * qg;
+        xok[mt] = 16 * mt + r < p.M;
     }
-    red[wave][0][lane] = acc0;
-    red[wave][1][lane] = acc1;
+    const uint16_t* ap[NKT > 0 ? NKT : 1];
+    bool aok[NKT > 0 ? NKT : 1];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) {
+        ap[kt] = p.a + (size_t)(proj * p.rank + min(16 * kt + r, p.rank - 1)) * p.K + 8 * qg;
+        aok[kt] = 16 * kt + r < p.rank;
+    }
+    // adapter up-projection operands, read early so their latency hides
+    bf16x8 bop[NKK > 0 ? NKK : 1];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+        bop[kk] = lora_weight_operand(p, n0 + r, proj, kk, qg);
+
+    floatx4 acc[MT], tacc[MT][NKT > 0 ? NKT : 1];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+            tacc[mt][kt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int s = s_begin; s < s_end; s += U) {
+        bf16x8 wv[U], xv[MT][U], av[NKT > 0 ? NKT : 1][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const bool in = s + u < s_end;
+            wv[u] = (in && wok) ? load_bf16x8(wp + 32 * (s + u)) : zero_bf16x8();
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                xv[mt][u] = (in && xok[mt]) ? load_bf16x8(xp[mt] + 32 * (s + u)) : zero_bf16x8();
+#pragma unroll
+            for (int kt = 0; kt < NKT; ++kt)
+                av[kt][u] = (in && aok[kt]) ? load_bf16x8(ap[kt] + 32 * (s + u)) : zero_bf16x8();
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                acc[mt] = mfma16_bf16(wv[u], xv[mt][u], acc[mt]);
+#pragma unroll
+                for (int kt = 0; kt < NKT; ++kt)
+                    tacc[mt][kt] = mfma16_bf16(xv[mt][u], av[kt][u], tacc[mt][kt]);
+            }
+    }
+    // reduce the eight waves' partials
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        red[(wave * NV + mt) * 64 + lane] = acc[mt];
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+            red[(wave * NV + MT + mt * NKT + kt) * 64 + lane] = tacc[mt][kt];
+    }
     __syncthreads();
     if (wave != 0)
         return;
-    acc0 = red[0][0][lane] + red[1][0][lane] + red[2][0][lane] + red[3][0][lane];
-    acc1 = red[0][1][lane] + red[1][1][lane] + red[2][1][lane] + red[3][1][lane];
-
-    if (p.rank > 0) {
-        // Tiles never straddle projections (d_q, d_kv are multiples of 16).
-        const int proj = proj_of(p, n0);
-        const int nk = (p.rank + 31) / 32;
-        for (int kk = 0; kk < nk; ++kk) {
-            bf16x8 wa = lora_weight_operand(p, wrow, proj, kk, qg);
-            bf16x8 hi, lo;
-            lora_token_operand(p, r, proj, kk, qg, &hi, &lo);
-            acc0 = mfma16_bf16(wa, hi, acc0);
-            acc0 = mfma16_bf16(wa, lo, acc0);
-            if (nt_count > 1) {
-                lora_token_operand(p, 16 + r, proj, kk, qg, &hi, &lo);
-                acc1 = mfma16_bf16(wa, hi, acc1);
-                acc1 = mfma16_bf16(wa, lo, acc1);
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        floatx4 sum = red[v * 64 + lane];
+#pragma unroll
+        for (int w = 1; w < kDecWaves; ++w)
+            sum += red[(w * NV + v) * 64 + lane];
+        if (v < MT)
+            acc[v] = sum;
+        else
+            red[v * 64 + lane] = sum;  // wave 0's own slot: read back below
+    }
+    if constexpr (NKT > 0) {
+        // t[m][k] = scale * sum, from the accumulator layout (lane: k = 16 kt + r,
+        // m = 16 mt + 4 qg + i) to rows of m in LDS (after the partial slots)
+        float* tl = (float*)(red + kDecWaves * NV * 64);
+        constexpr int TK = 16 * NKT;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int kt = 0; kt < NKT; ++kt) {
+                const floatx4 tv = red[(MT + mt * NKT + kt) * 64 + lane];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    tl[(16 * mt + 4 * qg + i) * TK + 16 * kt + r] = tv[i] * p.scale;
             }
-        }
+        // one wave: LDS writes above are visible to its reads below in order
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                float v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int k = 32 * kk + 8 * qg + e;
+                    v[e] = k < TK ? tl[(16 * mt + r) * TK + k] : 0.0f;
+                }
+                bf16x8 hi, lo;
+                split_bf16x8(v, &hi, &lo);
+                acc[mt] = mfma16_bf16(bop[kk], hi, acc[mt]);
+                acc[mt] = mfma16_bf16(bop[kk], lo, acc[mt]);
+            }
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        store_out(p, r, n0 + 4 * qg + i, acc0[i]);
-        if (nt_count > 1)
-            store_out(p, 16 + r, n0 + 4 * qg + i, acc1[i]);
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            store_out(p, 16 * mt + r, n0 + 4 * qg + i, acc[mt][i]);
+}
+
+template <int MT, int NKT>
+hipError_t launch_decode_proj(const ProjParams& p, hipStream_t stream)
+{
+    constexpr int NV = MT * (1 + NKT);
+    const size_t lds = sizeof(floatx4) * kDecWaves * NV * 64 + sizeof(float) * 16 * MT * 16 * NKT;
+    hipLaunchKernelGGL((proj_decode_kernel<MT, NKT>), dim3((p.N + 15) / 16), dim3(kDecWaves * 64), lds, stream, p);
+    return hipGetLastError();
+}
+
+template <int MT>
+hipError_t launch_decode_proj_r(const ProjParams& p, hipStream_t stream)
+{
+    const int nkt = (p.rank + 15) / 16;
+    switch (nkt) {
+    case 0:
+        return launch_decode_proj<MT, 0>(p, stream);
+    case 1:
+        return launch_decode_proj<MT, 1>(p, stream);
+    case 2:
+        return launch_decode_proj<MT, 2>(p, stream);
+    case 3:
+        return launch_decode_proj<MT, 3>(p, stream);
+    default:
+        return launch_decode_proj<MT, 4>(p, stream);
     }
 }
 
@@ -295,7 +386,8 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
     if (p.M <= 0)
         return hipSuccess;
     if (p.M <= 32) {
-        hipLaunchKernelGGL(proj_skinny_kernel, dim3((p.N + 15) / 16), dim3(kThreads), 0, stream, p);
+        // fused path: W, H and (rank > 0) the adapter rows p.a in one kernel
+        return p.M <= 16 ? launch_decode_proj_r<1>(p, stream) : launch_decode_proj_r<2>(p, stream);
     } else {
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + kBM - 1) / kBM);
         hipLaunchKernelGGL(proj_big_kernel, grid, dim3(kThreads), 0, stream, p);
