@@ -139,12 +139,15 @@ def main():
             cache.storage.copy_(snapshot)
             cache.restore(wl.context)
 
+    Kv, Vv, Qv = Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D), Qd.view(B, Hq, D)
+    Hsteps = [Hdec[i] for i in range(wl.decode_steps)]
+
     def step(i, ev=None):
-        kvq.project_qkv(Hdec[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
-        cache.append(Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D))
+        kvq.project_qkv(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
+        cache.append(Kv, Vv)
         if ev is not None:
             ev[0].record()
-        cache.decode_attn(Qd.view(B, Hq, D), Hq, sm, O, wsa)
+        cache.decode_attn(Qv, Hq, sm, O, wsa)
         if ev is not None:
             ev[1].record()
 

@@ -280,6 +280,108 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
     }
 }
 
+// One decoded token per (sequence, KV head) without a window: a workgroup of
+// D threads, thread d owning channel d of the token's K and V.  Every load
+// (the token's K and V, and the value piece it shares with earlier tokens)
+// is issued first; the rotation runs as the same butterflies as fwht_rows;
+// group statistics are all-reduced across the group's threads (min, max and
+// max-magnitude are exact in any order, so they equal the block kernel's),
+// then each thread codes its channel, key pieces are OR-reduced over eight
+// lanes and each value piece is merged with the bits of earlier tokens.
+template <int D>
+__device__ __forceinline__ float group_reduce(float v, int g, bool is_max, float* red, int slot)
+{
+    const int lanes = g < 64 ? g : 64;
+    for (int off = 1; off < lanes; off <<= 1) {
+        const float o = __shfl_xor(v, off);
+        v = is_max ? fmaxf(v, o) : fminf(v, o);
+    }
+    if (g > 64) {
+        // one value per wave, combined over the g / 64 waves of the group
+        const int wave = threadIdx.x >> 6;
+        if ((threadIdx.x & 63) == 0)
+            red[slot * 4 + wave] = v;
+        __syncthreads();
+        const int w0 = (wave / (g / 64)) * (g / 64);
+        v = red[slot * 4 + w0];
+        for (int w = 1; w < g / 64; ++w)
+            v = is_max ? fmaxf(v, red[slot * 4 + w0 + w]) : fminf(v, red[slot * 4 + w0 + w]);
+    }
+    return v;
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void append_token_kernel(AppendParams p)
+{
+    __shared__ float xs[2][D];
+    __shared__ float red[8 * 4];
+    const int unit = blockIdx.x, b = unit / p.H, h = unit % p.H, d = threadIdx.x;
+    const int t = p.n0, tau = t & 31, j = t & 7;
+    const size_t blk = (size_t)unit * (p.T / kBlockTok) + (size_t)(t / kBlockTok);
+    const size_t vpi = value_piece<D>(blk, tau >> 3, d);
+    const size_t in = ((size_t)b * p.H + h) * D + d;  // n_new == 1
+    float x[2] = {bf16_to_f32(p.kin[in]), bf16_to_f32(p.vin[in])};
+    const uint32_t old = load_piece(p.vc, vpi, p.v_bits);
+    if (p.rotate) {
+        xs[0][d] = x[0];
+        xs[1][d] = x[1];
+        __syncthreads();
+        for (int hw = 1; hw < D; hw <<= 1) {
+            float nv[2];
+#pragma unroll
+            for (int w = 0; w < 2; ++w)
+                nv[w] = (d & hw) ? xs[w][d - hw] - xs[w][d] : xs[w][d] + xs[w][d + hw];
+            __syncthreads();
+            xs[0][d] = nv[0];
+            xs[1][d] = nv[1];
+            __syncthreads();
+        }
+        x[0] = xs[0][d] * p.rot_c;
+        x[1] = xs[1][d] * p.rot_c;
+    }
+#pragma unroll
+    for (int w = 0; w < 2; ++w) {
+        const int mode = w ? p.v_mode : p.k_mode, bits = w ? p.v_bits : p.k_bits;
+        const int g = w ? p.v_group : p.k_group, gi = d / g, ng = D / g;
+        float s, z;
+        if (mode == KVQ_AFFINE) {
+            const float mn = group_reduce<D>(x[w], g, false, red, 2 * w);
+            const float mx = group_reduce<D>(x[w], g, true, red, 2 * w + 1);
+            const float top = (float)((1 << bits) - 1);
+            s = (mx - mn) / top;
+            if (!(s >= 1e-8f))
+                s = 1e-8f;
+            z = mn + 0.0f;  // canonical +0 for a signed-zero minimum
+        } else {
+            const float ma = group_reduce<D>(fabsf(x[w]), g, true, red, 2 * w);
+            const float qmax = (float)((1 << (bits - 1)) - 1);
+            s = ma / qmax;
+            if (!(s >= 1e-8f))
+                s = 1e-8f;
+            z = 0.0f;
+        }
+        const uint32_t c = code_one(x[w], s, z, mode, bits);
+        if (d % g == 0) {
+            const size_t mi = (blk * ng + gi) * kBlockTok + tau;
+            (w ? p.vs : p.ks)[mi] = s;
+            if (mode == KVQ_AFFINE)
+                (w ? p.vz : p.kz)[mi] = z;
+        }
+        if (w == 0) {
+            // key piece d / 8: codes of channels 8P .. 8P + 7 at bits k_bits e
+            uint32_t piece = c << (bits * (d & 7));
+            piece |= __shfl_xor(piece, 1);
+            piece |= __shfl_xor(piece, 2);
+            piece |= __shfl_xor(piece, 4);
+            if ((d & 7) == 0)
+                store_piece(p.kc, key_piece<D>(blk, tau, d >> 3), bits, piece);
+        } else {
+            const uint32_t keep = j == 0 ? 0u : ((1u << (bits * j)) - 1u);
+            store_piece(p.vc, vpi, bits, (old & keep) | (c << (bits * j)));
+        }
+    }
+}
+
 // fp16 window: slot t mod (R + F) <- fp16 of token t (rotated first when
 // the format rotates), for t in [ring_lo, n0 + n_new).  Runs after the coder
 // of the same call, which may still read the slots being replaced.
@@ -312,6 +414,10 @@ template <int D>
 hipError_t launch_append_d(const AppendParams& p, hipStream_t stream)
 {
     const int units = p.B * p.H;
+    if (p.n_new == 1 && p.ring == 0 && p.k_axis == KVQ_PER_TOKEN) {
+        hipLaunchKernelGGL(append_token_kernel<D>, dim3(units), dim3(D), 0, stream, p);
+        return hipGetLastError();
+    }
     if (p.q1 > p.q0) {
         int nblk = (p.q1 + kBlockTok - 1) / kBlockTok - p.q0 / kBlockTok;
         hipLaunchKernelGGL(append_code_kernel<D>, dim3(nblk, units), dim3(kThreads), 0, stream, p);

@@ -254,8 +254,8 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
     }
     hipStream_t s = (hipStream_t)stream;
     const int N = d_q + 2 * d_kv;
-    if (M <= 32) {
-        // decode: one fused kernel computes the adapter activations itself
+    if (M <= 32 && rank <= 16) {
+        // decode, small rank: one fused kernel computes the adapter activations itself
         kvq::ProjParams p = {};
         p.x = (const uint16_t*)H;
         p.w = (const uint16_t*)W;

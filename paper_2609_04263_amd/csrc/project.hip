@@ -111,29 +111,48 @@ __device__ __forceinline__ bf16x8 lora_weight_operand(const ProjParams& p, int n
 }
 
 // ----------------------------------------------------------- fused decode
-// Workgroup: weight rows [n0, n0 + 16) x all M (<= 16 MT) tokens, 8 waves.
+// Workgroup: weight rows [n0, n0 + 16 R) x all M (<= 16 MT) tokens, 8 waves.
+// Each wave owns one eighth of the reduction dimension for all R row tiles,
+// so one H fragment (and one adapter fragment) serves R weight tiles: the
+// rows of H and A_p, which every workgroup reads, cost 1/R of the weight
+// traffic instead of as much as it.  Workgroups start their waves at
+// different eighths so that concurrent workgroups read different lines.
 // MFMA roles: Y: A = W rows (16 weight rows), B = H^T (16 tokens);
 //             t: A = H rows (16 tokens), B = A_p^T (16 adapter rows).
-// Output lane layout: token = 16 mt + (lane % 16), row n0 + 4 qg + i.
+// Output lane layout: token = 16 mt + (lane % 16), row n0 + 16 rt + 4 qg + i.
 constexpr int kDecWaves = 8;
 
-template <int MT, int NKT>
+template <int R, int MT, int NKT, bool TLOAD>
+struct DecShape {
+    static constexpr int NV = R * MT + MT * NKT;       // floatx4 partials per lane
+    static constexpr int NKK = (16 * NKT + 31) / 32;   // 32-wide rank chunks of the fused K-extension
+    static constexpr int PER_STEP = R + MT + NKT;      // 16-byte loads per K-step
+    static constexpr int U = PER_STEP <= 3 ? 8 : PER_STEP <= 6 ? 4 : 2;  // K-steps per load batch
+    static constexpr size_t LDS = sizeof(floatx4) * kDecWaves * NV * 64 + sizeof(float) * 16 * MT * 16 * NKT;
+};
+
+template <int R, int MT, int NKT, bool TLOAD>
 __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams p)
 {
-    constexpr int U = (MT + NKT <= 2) ? 8 : 4;   // K-steps per load batch
-    constexpr int NV = MT * (1 + NKT);           // floatx4 partials per lane
-    constexpr int NKK = (16 * NKT + 31) / 32;    // 32-wide rank chunks of the K-extension
-    extern __shared__ floatx4 red[];             // [kDecWaves][NV][64], then t [16 MT][16 NKT]
+    using S = DecShape<R, MT, NKT, TLOAD>;
+    constexpr int NV = S::NV, NKK = S::NKK, U = S::U;
+    extern __shared__ floatx4 red[];  // [kDecWaves][NV][64], then t [16 MT][16 NKT]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, qg = lane >> 4;
-    const int n0 = blockIdx.x * 16;
-    const int proj = proj_of(p, n0);  // tiles never straddle projections (d_q, d_kv multiples of 16)
+    const int n0 = blockIdx.x * 16 * R;
+    const int proj = proj_of(p, n0);  // tiles never straddle projections (see launch_project)
     const int steps = p.K / 32;
     const int per = (steps + kDecWaves - 1) / kDecWaves;
-    const int s_begin = wave * per, s_end = min(steps, s_begin + per);
+    const int chunk = (wave + (int)blockIdx.x) % kDecWaves;
+    const int s_begin = chunk * per, s_end = min(steps, s_begin + per);
 
-    const uint16_t* wp = p.w + (size_t)min(n0 + r, p.N - 1) * p.K + 8 * qg;
-    const bool wok = n0 + r < p.N;
+    const uint16_t* wp[R];
+    bool wok[R];
+#pragma unroll
+    for (int rt = 0; rt < R; ++rt) {
+        wp[rt] = p.w + (size_t)min(n0 + 16 * rt + r, p.N - 1) * p.K + 8 * qg;
+        wok[rt] = n0 + 16 * rt + r < p.N;
+    }
     const uint16_t* xp[MT];
     bool xok[MT];
 #pragma unroll
@@ -148,26 +167,25 @@ __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams 
         ap[kt] = p.a + (size_t)(proj * p.rank + min(16 * kt + r, p.rank - 1)) * p.K + 8 * qg;
         aok[kt] = 16 * kt + r < p.rank;
     }
-    // adapter up-projection operands, read early so their latency hides
-    bf16x8 bop[NKK > 0 ? NKK : 1];
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk)
-        bop[kk] = lora_weight_operand(p, n0 + r, proj, kk, qg);
 
-    floatx4 acc[MT], tacc[MT][NKT > 0 ? NKT : 1];
+    floatx4 acc[R][MT], tacc[MT][NKT > 0 ? NKT : 1];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int rt = 0; rt < R; ++rt)
+            acc[rt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt)
             tacc[mt][kt] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
     for (int s = s_begin; s < s_end; s += U) {
-        bf16x8 wv[U], xv[MT][U], av[NKT > 0 ? NKT : 1][U];
+        bf16x8 wv[R][U], xv[MT][U], av[NKT > 0 ? NKT : 1][U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const bool in = s + u < s_end;
-            wv[u] = (in && wok) ? load_bf16x8(wp + 32 * (s + u)) : zero_bf16x8();
+#pragma unroll
+            for (int rt = 0; rt < R; ++rt)
+                wv[rt][u] = (in && wok[rt]) ? load_bf16x8(wp[rt] + 32 * (s + u)) : zero_bf16x8();
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
                 xv[mt][u] = (in && xok[mt]) ? load_bf16x8(xp[mt] + 32 * (s + u)) : zero_bf16x8();
@@ -179,51 +197,62 @@ __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams 
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                acc[mt] = mfma16_bf16(wv[u], xv[mt][u], acc[mt]);
+#pragma unroll
+                for (int rt = 0; rt < R; ++rt)
+                    acc[rt][mt] = mfma16_bf16(wv[rt][u], xv[mt][u], acc[rt][mt]);
 #pragma unroll
                 for (int kt = 0; kt < NKT; ++kt)
                     tacc[mt][kt] = mfma16_bf16(xv[mt][u], av[kt][u], tacc[mt][kt]);
             }
     }
-    // reduce the eight waves' partials
+    // reduce the eight waves' partials: slot v of every wave -> wave v % 8 sums it
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        red[(wave * NV + mt) * 64 + lane] = acc[mt];
+    for (int rt = 0; rt < R; ++rt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            red[(wave * NV + rt * MT + mt) * 64 + lane] = acc[rt][mt];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt)
-            red[(wave * NV + MT + mt * NKT + kt) * 64 + lane] = tacc[mt][kt];
-    }
+            red[(wave * NV + R * MT + mt * NKT + kt) * 64 + lane] = tacc[mt][kt];
     __syncthreads();
-    if (wave != 0)
-        return;
-#pragma unroll
-    for (int v = 0; v < NV; ++v) {
+    for (int v = wave; v < NV; v += kDecWaves) {
         floatx4 sum = red[v * 64 + lane];
 #pragma unroll
         for (int w = 1; w < kDecWaves; ++w)
             sum += red[(w * NV + v) * 64 + lane];
-        if (v < MT)
-            acc[v] = sum;
-        else
-            red[v * 64 + lane] = sum;  // wave 0's own slot: read back below
+        red[v * 64 + lane] = sum;  // wave 0's slots hold the totals
     }
     if constexpr (NKT > 0) {
-        // t[m][k] = scale * sum, from the accumulator layout (lane: k = 16 kt + r,
-        // m = 16 mt + 4 qg + i) to rows of m in LDS (after the partial slots)
+        __syncthreads();
+        // t[m][k] = scale * total, from the accumulator layout (lane: k = 16 kt + r,
+        // m = 16 mt + 4 qg + i) to rows of m after the partial slots
         float* tl = (float*)(red + kDecWaves * NV * 64);
         constexpr int TK = 16 * NKT;
+        if (wave == 0) {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int kt = 0; kt < NKT; ++kt) {
+                    const floatx4 tv = red[(R * MT + mt * NKT + kt) * 64 + lane];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        tl[(16 * mt + 4 * qg + i) * TK + 16 * kt + r] = tv[i] * p.scale;
+                }
+        }
+        __syncthreads();
+        if (wave >= R)
+            return;
+        // wave rt applies the K-extension to row tile rt
+        const int rt = wave;
+        floatx4 out[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
+            out[mt] = red[(rt * MT + mt) * 64 + lane];
 #pragma unroll
-            for (int kt = 0; kt < NKT; ++kt) {
-                const floatx4 tv = red[(MT + mt * NKT + kt) * 64 + lane];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    tl[(16 * mt + 4 * qg + i) * TK + 16 * kt + r] = tv[i] * p.scale;
-            }
-        // one wave: LDS writes above are visible to its reads below in order
-#pragma unroll
-        for (int kk = 0; kk < NKK; ++kk)
+        for (int kk = 0; kk < NKK; ++kk) {
+            const bf16x8 bop = lora_weight_operand(p, n0 + 16 * rt + r, proj, kk, qg);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 float v[8];
@@ -234,42 +263,72 @@ __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams 
                 }
                 bf16x8 hi, lo;
                 split_bf16x8(v, &hi, &lo);
-                acc[mt] = mfma16_bf16(bop[kk], hi, acc[mt]);
-                acc[mt] = mfma16_bf16(bop[kk], lo, acc[mt]);
+                out[mt] = mfma16_bf16(bop, hi, out[mt]);
+                out[mt] = mfma16_bf16(bop, lo, out[mt]);
             }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                store_out(p, 16 * mt + r, n0 + 16 * rt + 4 * qg + i, out[mt][i]);
+    } else {
+        __syncthreads();
+        if (wave >= R)
+            return;
+        const int rt = wave;
+        floatx4 out[MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+            out[mt] = red[(rt * MT + mt) * 64 + lane];
+        if (TLOAD && p.rank > 0) {
+            // K-extension with the activations of a separate pass (fp32 in p.t)
+            const int nk = (p.rank + 31) / 32;
+            for (int kk = 0; kk < nk; ++kk) {
+                const bf16x8 bop = lora_weight_operand(p, n0 + 16 * rt + r, proj, kk, qg);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    bf16x8 hi, lo;
+                    lora_token_operand(p, 16 * mt + r, proj, kk, qg, &hi, &lo);
+                    out[mt] = mfma16_bf16(bop, hi, out[mt]);
+                    out[mt] = mfma16_bf16(bop, lo, out[mt]);
+                }
+            }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                store_out(p, 16 * mt + r, n0 + 16 * rt + 4 * qg + i, out[mt][i]);
+        }
     }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            store_out(p, 16 * mt + r, n0 + 4 * qg + i, acc[mt][i]);
 }
 
-template <int MT, int NKT>
+template <int R, int MT, int NKT, bool TLOAD>
 hipError_t launch_decode_proj(const ProjParams& p, hipStream_t stream)
 {
-    constexpr int NV = MT * (1 + NKT);
-    const size_t lds = sizeof(floatx4) * kDecWaves * NV * 64 + sizeof(float) * 16 * MT * 16 * NKT;
-    hipLaunchKernelGGL((proj_decode_kernel<MT, NKT>), dim3((p.N + 15) / 16), dim3(kDecWaves * 64), lds, stream, p);
+    constexpr size_t lds = DecShape<R, MT, NKT, TLOAD>::LDS;
+    hipLaunchKernelGGL((proj_decode_kernel<R, MT, NKT, TLOAD>), dim3((p.N + 16 * R - 1) / (16 * R)),
+                       dim3(kDecWaves * 64), lds, stream, p);
     return hipGetLastError();
 }
 
+// Decode-path dispatch.  Adapters of rank <= 16 are fused (each workgroup
+// computes its projection's activations: one adapter row tile per row tile
+// of weights); larger ranks read activations from a separate pass, since
+// recomputing them per workgroup would read the adapter rows more often
+// than the weights.  Workgroups take two row tiles when the output is wide
+// enough to keep all compute units busy with half as many workgroups.
 template <int MT>
-hipError_t launch_decode_proj_r(const ProjParams& p, hipStream_t stream)
+hipError_t launch_decode_proj_m(const ProjParams& p, hipStream_t stream)
 {
-    const int nkt = (p.rank + 15) / 16;
-    switch (nkt) {
-    case 0:
-        return launch_decode_proj<MT, 0>(p, stream);
-    case 1:
-        return launch_decode_proj<MT, 1>(p, stream);
-    case 2:
-        return launch_decode_proj<MT, 2>(p, stream);
-    case 3:
-        return launch_decode_proj<MT, 3>(p, stream);
-    default:
-        return launch_decode_proj<MT, 4>(p, stream);
-    }
+    const int dq = p.n1, dkv = p.n2 - p.n1;
+    const bool two = p.N >= 4096 && dq % 32 == 0 && dkv % 32 == 0;
+    if (p.yf || p.rank == 0)
+        return two ? launch_decode_proj<2, MT, 0, false>(p, stream) : launch_decode_proj<1, MT, 0, false>(p, stream);
+    if (p.a && p.rank <= 16)
+        return two ? launch_decode_proj<2, MT, 1, false>(p, stream) : launch_decode_proj<1, MT, 1, false>(p, stream);
+    return two ? launch_decode_proj<2, MT, 0, true>(p, stream) : launch_decode_proj<1, MT, 0, true>(p, stream);
 }
 
 // --------------------------------------------------------------------- big
@@ -387,7 +446,7 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
         return hipSuccess;
     if (p.M <= 32) {
         // fused path: W, H and (rank > 0) the adapter rows p.a in one kernel
-        return p.M <= 16 ? launch_decode_proj_r<1>(p, stream) : launch_decode_proj_r<2>(p, stream);
+        return p.M <= 16 ? launch_decode_proj_m<1>(p, stream) : launch_decode_proj_m<2>(p, stream);
     } else {
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + kBM - 1) / kBM);
         hipLaunchKernelGGL(proj_big_kernel, grid, dim3(kThreads), 0, stream, p);

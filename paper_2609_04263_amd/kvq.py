@@ -92,8 +92,16 @@ def _ptr(t):
     return t.data_ptr()
 
 
+try:  # raw handle of torch's current stream without building a Stream object
+    _raw_stream = torch._C._cuda_getCurrentRawStream
+except AttributeError:  # pragma: no cover - older torch
+    _raw_stream = None
+
+
 def _stream(stream) -> int:
     if stream is None:
+        if _raw_stream is not None:
+            return _raw_stream(torch.cuda.current_device())
         return torch.cuda.current_stream().cuda_stream
     if isinstance(stream, int):
         return stream
@@ -123,6 +131,7 @@ class Cache:
         _check(_lib.kvq_cache_init(C.byref(self.fmt), B, H_kv, D, T_max, C.c_void_p(_ptr(storage)),
                                    storage.numel() * storage.element_size(), C.byref(h)), "cache_init")
         self.handle = h
+        self._fmt_ref = C.byref(self.fmt)
 
     def __del__(self):
         h = getattr(self, "handle", None)
@@ -158,9 +167,10 @@ class Cache:
         """Append bf16 K, V [B, n_new, H_kv, D] (device tensors)."""
         if n_new is None:
             n_new = K.shape[1] if K.dim() == 4 else 1
-        f = self.fmt if fmt is None else Format.of(fmt)
-        _check(_lib.kvq_append(self.handle, C.c_void_p(_ptr(K)), C.c_void_p(_ptr(V)), n_new, C.byref(f),
-                               C.c_void_p(_stream(stream))), "append")
+        f = self._fmt_ref if fmt is None else C.byref(Format.of(fmt))
+        st = _lib.kvq_append(self.handle, K.data_ptr(), V.data_ptr(), n_new, f, _stream(stream))
+        if st:
+            _check(st, "append")
 
     def decode_workspace_bytes(self, H_q: int) -> int:
         out = C.c_size_t()
@@ -174,9 +184,10 @@ class Cache:
     def decode_attn(self, Q, H_q: int, sm_scale: float, O, workspace, stream=None) -> None:
         """O[B, H_q, D] (fp32) <- attention of bf16 Q[B, H_q, D] over the cache."""
         nbytes = workspace.numel() * workspace.element_size()
-        _check(_lib.kvq_decode_attn(self.handle, C.c_void_p(_ptr(Q)), H_q, C.c_float(sm_scale),
-                                    C.c_void_p(_ptr(O)), C.c_void_p(_ptr(workspace)), nbytes,
-                                    C.c_void_p(_stream(stream))), "decode_attn")
+        st = _lib.kvq_decode_attn(self.handle, Q.data_ptr(), H_q, sm_scale, O.data_ptr(), workspace.data_ptr(),
+                                  nbytes, _stream(stream))
+        if st:
+            _check(st, "decode_attn")
 
 
 # ------------------------------------------------------------- projection
@@ -192,8 +203,7 @@ def project_qkv(H, W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, 
     """Q/K/V (bf16) <- H W^T + lora_scale * (H A_p^T) B_p^T per projection."""
     M, d_in = H.shape[0], H.shape[-1]
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(_lib.kvq_project_qkv(C.c_void_p(_ptr(H)), M, d_in, C.c_void_p(_ptr(W)), d_q, d_kv,
-                                C.c_void_p(_ptr(A)), C.c_void_p(_ptr(Bm)), rank, C.c_float(lora_scale),
-                                C.c_void_p(_ptr(Q)), C.c_void_p(_ptr(K)), C.c_void_p(_ptr(V)),
-                                C.c_void_p(_ptr(workspace)), nbytes, C.c_void_p(_stream(stream))),
-           "project_qkv")
+    st = _lib.kvq_project_qkv(_ptr(H), M, d_in, _ptr(W), d_q, d_kv, _ptr(A), _ptr(Bm), rank, lora_scale,
+                              _ptr(Q), _ptr(K), _ptr(V), _ptr(workspace), nbytes, _stream(stream))
+    if st:
+        _check(st, "project_qkv")
