@@ -47,12 +47,16 @@ def parse():
     ap.add_argument("--phase", choices=["decode", "prefill"], default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=None)
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="before the timed region, copy a buffer of this many MiB once (a kernel of known "
+                         "bytes for calibrating rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
     return ap.parse_args()
 
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("attn.hip", "kvq_device.h", "kvq_internal.h"):
+    for f in ("attn.hip", "attn_impl.h", "attn_d64.hip", "attn_d128.hip", "attn_d256.hip", "kvq_device.h",
+              "kvq_internal.h"):
         with open(os.path.join(ROOT, "paper_2609_04263_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -139,6 +143,13 @@ def main():
             cache.storage.copy_(snapshot)
             cache.restore(wl.context)
 
+    if args.copy_probe_mb:
+        # one elementwise kernel that reads and writes exactly this many bytes
+        src = torch.empty(args.copy_probe_mb << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.add(src, 1, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     Kv, Vv, Qv = Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D), Qd.view(B, Hq, D)
     Hsteps = [Hdec[i] for i in range(wl.decode_steps)]
 

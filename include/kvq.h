@@ -78,16 +78,31 @@ typedef struct kvq_cache kvq_cache;
 /* Bytes of cache storage for B sequences, H_kv heads of size D (64, 128 or
  * 256) and up to T_max tokens.  The storage image has eight sections, each
  * starting at a multiple of 256 bytes (T_alloc = T_max rounded up to 32):
- *   0 Kc u32 [B][H_kv][T_alloc][D*k_bits/32]  K codes, packed along head_dim
- *   1 Ks f32 [B][H_kv][T_alloc][D/k_group]    (per channel: [T_alloc/32][D])
- *   2 Kz f32, like Ks; affine keys only (else 0 bytes)
- *   3 Vc u32 [B][H_kv][T_alloc*v_bits/32][D]  V codes, packed along tokens
- *   4 Vs f32 [B][H_kv][T_alloc][D/v_group]
- *   5 Vz f32, like Vs; affine values only
- *   6 Kr f16 [B][H_kv][residual+flush][D]     fp16 window, slot t mod (R+F)
+ *   0 Kc key codes           D*k_bits/8 bytes per token
+ *   1 Ks f32 key scales      per token: D/k_group per token; per channel: D per 32 tokens
+ *   2 Kz f32 key offsets, like Ks; affine keys only (else 0 bytes)
+ *   3 Vc value codes         D*v_bits/8 bytes per token
+ *   4 Vs f32 value scales    D/v_group per token
+ *   5 Vz f32 value offsets, like Vs; affine values only
+ *   6 Kr f16 [B][H_kv][residual+flush][D]  fp16 window, slot t mod (R+F)
  *   7 Vr f16, like Kr
- * In a packed word, element j of its run of 32/bits codes occupies bits
- * [bits*j, bits*j + bits). */
+ * Sections 0-5 are blocked by 32-token blocks: with u = b*H_kv + h,
+ * NB = T_alloc/32, token t at position tau = t%32 of block beta = t/32, and
+ * i = u*NB + beta:
+ *   Codes come in pieces of eight codes (code j at bits [bits*j, +bits); a
+ *   piece is 32 bits for 4-bit codes, 16 bits for 2-bit codes; piece index
+ *   x starts at byte x*bits of its section).  Token tau has row
+ *   r = 4*(tau/8) + tau%4 and half e = (tau/4)%2 of its block.
+ *   Kc piece (t, P), channels 8P..8P+7 of token t, is at index
+ *       ((i*2 + e)*64 + r + 16*(P%4)) * (D/32) + P/4
+ *   Vc piece (octet o = tau/8, channel d), tokens 8o..8o+7 of channel d,
+ *       is at index (i*64 + d%16 + 16*o) * (D/16) + d/16
+ *   Ks/Kz per token, group g: float index (i*(D/k_group) + g)*32 + tau;
+ *       per channel (32-token group beta, channel d): i*D + d
+ *   Vs/Vz group g: float index (i*(D/v_group) + g)*32 + tau
+ * This is the order in which the decode kernel consumes the codes (a
+ * 64-lane MFMA operand layout), so attention reads them without any
+ * rearrangement; the paper fixes the codes and metadata, not this order. */
 kvq_status kvq_cache_bytes(const kvq_format* fmt, int B, int H_kv, int D, int T_max, size_t* bytes);
 
 /* Create a handle over caller storage (at least kvq_cache_bytes bytes,
@@ -164,6 +179,10 @@ kvq_status kvq_decode_workspace_bytes(const kvq_cache* cache, int H_q, size_t* b
  *      cached tokens (coded tokens reconstructed in-kernel, window tokens
  *      from fp16).  With a rotating format q is rotated first and the
  *      output rotated back.
+ * Products are formed from binary16 MFMA operands and accumulated in fp32:
+ * query elements (after rotation), query x key channel scale x sm_scale x
+ * log2(e) for per-channel keys, and each value group's scale must have
+ * magnitude below 65504 (binary16's largest finite value).
  * An empty cache (n == 0) returns KVQ_ERR_ARG. */
 kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
                            void* workspace, size_t ws_bytes, void* stream);
