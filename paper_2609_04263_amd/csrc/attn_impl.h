@@ -293,6 +293,50 @@ struct Split {
         lsum += ps;
     }
 
+    // Per-token key scores of the 32 tokens of a block (l[4 h2 + i]: token
+    // 8 qg + 4 h2 + i): per group of 2^GKS K-blocks one chained MFMA sum
+    // acc_g = sum_d A_d q_d, then S = sum_g s_g acc_g + z'_g sum_{d in g} q_d.
+    template <int GKS>
+    __device__ __forceinline__ void token_key_scores(const BlockRegs<C>& r, const float4* ks, const float4* kz,
+                                                     int qg, bool qlo_on, const CodeBits& kcb, float* l)
+    {
+        constexpr int GK = (1 << GKS) < NKB ? (1 << GKS) : NKB;  // K-blocks per group
+        constexpr int NG = NKB / GK;
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2) {
+            floatx4 acc[NG];
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                acc[g] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int u = 0; u < GK; ++u) {
+                    const int kb = g * GK + u;
+                    const half8 a = biased_codes<C::KBITS>(r.k[h2], kb, kcb);
+                    acc[g] = mfma16(a, qhi[kb], acc[g]);
+                    if (qlo_on)
+                        acc[g] = mfma16(a, qlo[kb], acc[g]);
+                }
+            }
+            floatx4 S;
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                float qs = qsum[g * GK];
+#pragma unroll
+                for (int u = 1; u < GK; ++u)
+                    qs += qsum[g * GK + u];
+                // scale and offset of group g for tokens 8 qg + 4 h2 + i
+                const int fi = g * 8 + 2 * qg + h2;
+                const float4 s4 = ks[fi], z4 = kz[fi];
+                const floatx4 t = {s4.x * acc[g][0] + z4.x * qs, s4.y * acc[g][1] + z4.y * qs,
+                                   s4.z * acc[g][2] + z4.z * qs, s4.w * acc[g][3] + z4.w * qs};
+                S = g == 0 ? t : S + t;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                l[4 * h2 + i] = S[i];
+        }
+    }
+
     // One coded 32-token block whose loads are in `r`; tokens at or beyond
     // `valid` are masked.  `wl` is the wave's metadata buffer; `vg` the value
     // group of this lane's column when every group has its own columns.
@@ -333,33 +377,20 @@ struct Split {
         // ---------------------------------------------------- scores
         float l[8];
         if constexpr (!C::PERCH) {
-#pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-                half8 a[NKB];
-                floatx4 acc[NKB];
-#pragma unroll
-                for (int kb = 0; kb < NKB; ++kb) {
-                    a[kb] = biased_codes<C::KBITS>(r.k[h2], kb, kcb);
-                    acc[kb] = mfma16(a[kb], qhi[kb], floatx4{0.0f, 0.0f, 0.0f, 0.0f});
-                }
-                if (qlo_on) {
-#pragma unroll
-                    for (int kb = 0; kb < NKB; ++kb)
-                        acc[kb] = mfma16(a[kb], qlo[kb], acc[kb]);
-                }
-                floatx4 S;
-#pragma unroll
-                for (int kb = 0; kb < NKB; ++kb) {
-                    // scale and offset of group kb >> lgk for tokens 8 qg + 4 h2 + i
-                    const int fi = (kb >> lgk) * 8 + 2 * qg + h2;
-                    const float4 s4 = ks[fi], z4 = kz[fi];
-                    const floatx4 t = {s4.x * acc[kb][0] + z4.x * qsum[kb], s4.y * acc[kb][1] + z4.y * qsum[kb],
-                                       s4.z * acc[kb][2] + z4.z * qsum[kb], s4.w * acc[kb][3] + z4.w * qsum[kb]};
-                    S = kb == 0 ? t : S + t;
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    l[4 * h2 + i] = S[i];
+            // key groups of 32 << lgk channels: one MFMA chain and one scale per group
+            switch (lgk) {
+            case 0:
+                token_key_scores<0>(r, ks, kz, qg, qlo_on, kcb, l);
+                break;
+            case 1:
+                token_key_scores<1>(r, ks, kz, qg, qlo_on, kcb, l);
+                break;
+            case 2:
+                token_key_scores<2>(r, ks, kz, qg, qlo_on, kcb, l);
+                break;
+            default:
+                token_key_scores<3>(r, ks, kz, qg, qlo_on, kcb, l);
+                break;
             }
         } else {
             // Per-channel keys: B = q * s_d (hi + lo), and sum_d q_d z'_d per head.
@@ -582,27 +613,29 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     const int blk_end = ring_split ? 0 : min(nblk, blk_begin + p.bps);
     const size_t ub0 = (size_t)unit * NB;
 
-    // ---- queries (bf16 -> fp32 rows in LDS; rows >= G zero), first block's loads
-    constexpr int QPIECES = 16 * D / 8;
-    constexpr int QLOADS = (QPIECES + kThreads - 1) / kThreads;
-    u32x4 qraw[QLOADS];
+    // ---- queries.  Without rotation each lane reads its own operand
+    // pieces (head `head`, channels 32 kb + 8 qg .. + 7) straight from
+    // global memory; a rotated query is first transformed as fp32 rows in LDS.
+    const size_t qrow = (size_t)b * p.H_q + (size_t)j * G;
+    u32x4 qpc[NKB];
+    if (!p.rotate) {
 #pragma unroll
-    for (int u = 0; u < QLOADS; ++u) {
-        const int pc = u * kThreads + (int)threadIdx.x, row = pc / (D / 8);
-        qraw[u] = u32x4{0u, 0u, 0u, 0u};
-        if (pc < QPIECES && row < G)
-            qraw[u] = *(const u32x4*)(p.q + ((size_t)b * p.H_q + (size_t)j * G + row) * D + (pc % (D / 8)) * 8);
+        for (int kb = 0; kb < NKB; ++kb)
+            qpc[kb] = active ? *(const u32x4*)(p.q + (qrow + head) * D + 32 * kb + 8 * qg) : u32x4{0u, 0u, 0u, 0u};
     }
     BlockRegs<C> ra, rb;
     int blk = blk_begin + wave;
     if (blk_end > blk_begin)
         load_block<C>(ra, p, mm, ub0 + min(blk, blk_end - 1), lane);
     float* lq = (float*)lds;
-#pragma unroll
-    for (int u = 0; u < QLOADS; ++u) {
-        const int pc = u * kThreads + (int)threadIdx.x;
-        if (pc < QPIECES) {
-            const uint32_t w[4] = {qraw[u].x, qraw[u].y, qraw[u].z, qraw[u].w};
+    if (p.rotate) {
+        constexpr int QPIECES = 16 * D / 8;
+        for (int pc = threadIdx.x; pc < QPIECES; pc += kThreads) {
+            const int row = pc / (D / 8);
+            u32x4 raw = {0u, 0u, 0u, 0u};
+            if (row < G)
+                raw = *(const u32x4*)(p.q + (qrow + row) * D + (pc % (D / 8)) * 8);
+            const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
             float* dst = lq + pc * 8;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -610,9 +643,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
                 dst[2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
             }
         }
-    }
-    __syncthreads();
-    if (p.rotate) {
+        __syncthreads();
         for (int h = 1; h < D; h <<= 1) {
             for (int idx = threadIdx.x; idx < 16 * (D / 2); idx += kThreads) {
                 const int row = idx / (D / 2), k = idx % (D / 2);
@@ -635,7 +666,13 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
         float part = 0.0f;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-            v[k] = active ? lq[head * D + 32 * kb + 8 * qg + perm4(k)] : 0.0f;
+            if (p.rotate) {
+                v[k] = active ? lq[head * D + 32 * kb + 8 * qg + perm4(k)] : 0.0f;
+            } else {
+                // element perm4(k) of the eight bf16 channels: word perm4(k) / 2, half perm4(k) % 2
+                const uint32_t w = qpc[kb][perm4(k) >> 1];
+                v[k] = __uint_as_float((perm4(k) & 1) ? (w & 0xFFFF0000u) : (w << 16));
+            }
             part += v[k];
         }
         if constexpr (C::PERCH) {
@@ -647,7 +684,8 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
             S.qsum[kb] = sum_rows(part);
         }
     }
-    __syncthreads();  // the metadata buffers overwrite the query rows
+    if (p.rotate)
+        __syncthreads();  // the metadata buffers overwrite the query rows
 
     const CodeBits kcb = code_bits<C::KBITS>(), vcb = code_bits<C::VBITS>();
     if (!ring_split) {
