@@ -54,10 +54,15 @@ def parse():
 
 
 def kernel_source_hash() -> str:
+    """Hash of the decode-attention sources (the kernel the traffic counters describe)."""
+    import glob
+    csrc = os.path.join(ROOT, "paper_2609_04263_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(csrc, "attn*.hip")) + glob.glob(os.path.join(csrc, "attn*.h")))
+    files += [os.path.join(csrc, f) for f in ("kvq_device.h", "kvq_internal.h")]
     h = hashlib.sha256()
-    for f in ("attn.hip", "attn_impl.h", "attn_d64.hip", "attn_d128.hip", "attn_d256.hip", "kvq_device.h",
-              "kvq_internal.h"):
-        with open(os.path.join(ROOT, "paper_2609_04263_amd", "csrc", f), "rb") as fh:
+    for f in files:
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
             h.update(fh.read())
     return h.hexdigest()[:16]
 

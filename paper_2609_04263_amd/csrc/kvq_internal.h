@@ -61,6 +61,7 @@ struct ProjParams {
     int n1, n2;           // column split points (d_q, d_q + d_kv)
     int rank;
     float scale;          // multiplies the fp32 output (activation pass); the adapter scale (fused path)
+    int nxcd;             // XCDs the large-M tile order spreads over (set at launch)
 };
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
 

@@ -16,6 +16,8 @@
 // across waves in LDS and applied as the K-extension.  Larger M (prefill)
 // uses the two passes with a 128x128 tiled GEMM staged through LDS.
 
+#include <atomic>
+
 #include "kvq_device.h"
 #include "kvq_internal.h"
 
@@ -438,6 +440,274 @@ __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
                 store_out(p, m0 + wm * 64 + 16 * mi + 4 * qg + i, n0 + wn * 64 + 16 * ni + r, acc[mi][ni][i]);
 }
 
+
+// -------------------------------------------------------------------- gemm
+// Large-M main pass: 256x256 output tile per workgroup, four waves in a 2x2
+// grid of 128x128 sub-tiles, v_mfma_f32_32x32x16_bf16 (16 accumulators of
+// 32x32 per wave).  A 128x128 sub-tile reads 64 bytes of LDS per 4096 MACs,
+// half of what 64x64 sub-tiles need, which keeps the compute units' LDS
+// bandwidth below what the matrix cores consume.  Operands reach LDS by
+// global_load_lds_dwordx4 (16 bytes per lane, no registers) in a ring of
+// kGStages stages of K = 32; a stage's rows are 64 bytes (four 16-byte
+// chunks) and chunk c of row r is stored at chunk position c ^ sw(r) with
+// sw(r) = (bit1(r) ^ bit3(r)) | bit2(r) << 1, so the rows that one phase of a
+// 16-byte-per-lane fragment read serves (8 rows with 32 banks, 16 with 64)
+// fall on distinct banks.  Workgroups take tiles so that the ones running
+// together on an XCD form a patch of 4 row blocks x 8 column blocks, whose
+// operands its L2 shares.
+// The adapter branch is applied as a K-extension of the same accumulators
+// (activation hi + lo times B_p), then outputs are rounded once to bf16.
+constexpr int kGM = 256, kGN = 256, kGK = 32, kGStages = 4;
+constexpr int kGStageBytes = (kGM + kGN) * kGK * 2;  // A then B rows of one stage
+constexpr size_t kGLds = (size_t)kGStages * kGStageBytes;
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ floatx16 mfma32_bf16(bf16x8 a, bf16x8 b, floatx16 c)
+{
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// 16 bytes per lane from global memory to LDS address lds_addr + 16 lane
+// (lds_addr wave-uniform; M0 holds it while the copy issues and is restored).
+// Inline assembly, so that the compiler does not make later LDS reads wait
+// for every outstanding vector memory operation; the explicit waits of the
+// stage ring order them.
+__device__ __forceinline__ void gemm_dma16(const void* src, uint32_t lds_addr)
+{
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "global_load_lds_dwordx4 %2, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(m0v), "v"(src)
+        : "memory");
+}
+
+template <int V>
+__device__ __forceinline__ void gemm_wait_vm()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(V) : "memory");
+}
+
+__device__ __forceinline__ int gemm_swz(int row)
+{
+    return (((row >> 1) ^ (row >> 3)) & 1) | (row & 4) >> 1;
+}
+
+__global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t glds[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1, wn = wave & 1;
+    // tile order: XCD x (= workgroup id mod p.nxcd) takes the contiguous
+    // range [x per, (x + 1) per) of tiles t, which run in groups of up to
+    // kGroupM row blocks: t -> (row block g kGroupM + r % gm, column block r / gm)
+    const int nbn = (p.N + kGN - 1) / kGN, nbm = (p.M + kGM - 1) / kGM;
+    const int ntiles = nbn * nbm, nx = p.nxcd;
+    const int per = (ntiles + nx - 1) / nx;
+    const int t = (blockIdx.x % nx) * per + blockIdx.x / nx;
+    if (t >= ntiles)
+        return;
+    constexpr int kGroupM = 4;
+    const int grp = t / (kGroupM * nbn), rem = t % (kGroupM * nbn);
+    const int gm = min(kGroupM, nbm - grp * kGroupM);
+    const int m0 = (grp * kGroupM + rem % gm) * kGM, n0 = (rem / gm) * kGN;
+    const uint32_t lbase = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_void_t*)glds);
+
+    // DMA: each stage is 32 copies of 1 KiB (16 rows x 64 bytes): copies
+    // 0..15 A rows, 16..31 B rows; wave w issues copies 8 w .. 8 w + 7.
+    // Lane i of a copy writes LDS row 16 j + i / 4, chunk position i % 4,
+    // which holds source chunk (i % 4) ^ ((row >> 1) & 3).  Rows past M (N)
+    // re-read the last row; their results are never stored.
+    uint64_t src[8];  // byte addresses of this lane's chunks for k = 0
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        const int copy = 8 * wave + c;
+        const bool isb = copy >= 16;
+        const int row = 16 * (copy & 15) + (lane >> 2);
+        const int chunk = (lane & 3) ^ gemm_swz(row);
+        const int g = isb ? min(n0 + row, p.N - 1) : min(m0 + row, p.M - 1);
+        const uint16_t* base = isb ? p.w : p.x;
+        src[c] = (uint64_t)(base + (size_t)g * p.K + 8 * chunk);
+    }
+    const int nks = p.K / kGK;
+
+    floatx16 acc[4][4];
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+            acc[mi][ni] = floatx16{};
+
+    // fragment rows of this lane (A: tokens, B: weight rows); chunk c of a
+    // row sits at LDS byte row * 64 + 16 (c ^ sw(row)), and the swizzle
+    // depends only on the lane (the rows differ by multiples of 32)
+    const int fr = lane & 31, fk = lane >> 5, sw = gemm_swz(fr);
+    int aoff[2], boff[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+        aoff[kk] = (wm * 128 + fr) * 64 + 16 * ((2 * kk + fk) ^ sw);
+        boff[kk] = kGM * kGK * 2 + (wn * 128 + fr) * 64 + 16 * ((2 * kk + fk) ^ sw);
+    }
+
+    auto issue = [&](int ks) {
+        const uint32_t st = lbase + (uint32_t)((ks % kGStages) * kGStageBytes);
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            gemm_dma16((const void*)(src[c] + (uint64_t)ks * kGK * 2), st + (uint32_t)((8 * wave + c) * 1024));
+    };
+    auto fetch = [&](int ks, int kk, bf16x8* fa, bf16x8* fb) {
+        const uint8_t* stg = glds + (ks % kGStages) * kGStageBytes;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(stg + aoff[kk] + 2048 * i));
+            fb[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(stg + boff[kk] + 2048 * i));
+        }
+    };
+    auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 4; ++ni)
+                acc[mi][ni] = mfma32_bf16(fa[mi], fb[ni], acc[mi][ni]);
+    };
+
+    // Pipeline: while the 16 MFMAs of one half-stage run, the fragments of
+    // the next half-stage are read from LDS.  Stage ks + 1 becomes readable
+    // at a barrier in the middle of stage ks (all waves' copies of it have
+    // landed, and every wave is done with stage ks - 1, whose buffer then
+    // receives stage ks + 3).
+    for (int ks = 0; ks < kGStages - 1 && ks < nks; ++ks)
+        issue(ks);
+    if (nks >= 3)
+        gemm_wait_vm<16>();
+    else if (nks == 2)
+        gemm_wait_vm<8>();
+    else
+        gemm_wait_vm<0>();
+    __syncthreads();
+    bf16x8 a0[4], b0[4], a1[4], b1[4];
+    fetch(0, 0, a0, b0);
+    for (int ks = 0; ks < nks; ++ks) {
+        fetch(ks, 1, a1, b1);
+        mma(a0, b0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads of the second half
+        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // MFMAs of the first half
+        if (ks + 1 < nks) {
+            if (ks + 2 < nks)
+                gemm_wait_vm<8>();  // stage ks + 2 may still be in flight
+            else
+                gemm_wait_vm<0>();
+            __syncthreads();
+            if (ks + kGStages - 1 < nks)
+                issue(ks + kGStages - 1);
+            fetch(ks + 1, 0, a0, b0);
+        }
+        mma(a1, b1);
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads of the next stage's first half
+        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // MFMAs of the second half
+    }
+
+    // adapter branch: K-extension over the rank, 16 at a time
+    if (p.rank > 0) {
+        const int p_lo = proj_of(p, n0), p_hi = proj_of(p, min(n0 + kGN, p.N) - 1);
+        for (int proj = p_lo; proj <= p_hi; ++proj) {
+            for (int k0 = 0; k0 < p.rank; k0 += 16) {
+                bf16x8 wop[4];
+#pragma unroll
+                for (int ni = 0; ni < 4; ++ni) {
+                    const int n = n0 + wn * 128 + 32 * ni + fr;
+                    const bool ok = n < p.N && proj_of(p, n) == proj;
+                    uint16_t v[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int k = k0 + 8 * fk + e;
+                        v[e] = (ok && k < p.rank) ? p.bm[(size_t)n * p.rank + k] : (uint16_t)0;
+                    }
+                    u32x4 w4;
+                    w4.x = v[0] | ((uint32_t)v[1] << 16);
+                    w4.y = v[2] | ((uint32_t)v[3] << 16);
+                    w4.z = v[4] | ((uint32_t)v[5] << 16);
+                    w4.w = v[6] | ((uint32_t)v[7] << 16);
+                    wop[ni] = __builtin_bit_cast(bf16x8, w4);
+                }
+#pragma unroll
+                for (int mi = 0; mi < 4; ++mi) {
+                    const int m = m0 + wm * 128 + 32 * mi + fr;
+                    float v[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int k = k0 + 8 * fk + e;
+                        v[e] = (m < p.M && k < p.rank) ? p.t[(size_t)m * 3 * p.rank + proj * p.rank + k] : 0.0f;
+                    }
+                    bf16x8 hi, lo;
+                    split_bf16x8(v, &hi, &lo);
+#pragma unroll
+                    for (int ni = 0; ni < 4; ++ni) {
+                        acc[mi][ni] = mfma32_bf16(hi, wop[ni], acc[mi][ni]);
+                        acc[mi][ni] = mfma32_bf16(lo, wop[ni], acc[mi][ni]);
+                    }
+                }
+            }
+        }
+    }
+
+    // Output, one 32-row slice of each wave's sub-tile at a time through LDS
+    // (the stage ring is free once every wave is past its last stage): the
+    // 32x32 accumulator element e of lane l is row 8 (e / 4) + 4 (l / 32) +
+    // e % 4, column l % 32 of its block; each lane then writes a pair of
+    // adjacent columns of every row, rounded to bf16, so a row's 128 columns
+    // are one 256-byte store per wave.
+    float* xo = (float*)glds + wave * (32 * 128);
+    const int rn0 = n0 + wn * 128;
+    const int cpair = n0 + wn * 128 + 2 * lane;
+    const int proj = proj_of(p, min(cpair, p.N - 1));
+    uint16_t* ybase = proj == 0 ? p.y0 : proj == 1 ? p.y1 : p.y2;
+    const int ywidth = proj == 0 ? p.n1 : proj == 1 ? p.n2 - p.n1 : p.N - p.n2;
+    const int ycol = cpair - (proj == 0 ? 0 : proj == 1 ? p.n1 : p.n2);
+    (void)rn0;
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi) {
+        __syncthreads();  // the previous slice's reads (or the last stage's) are done
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                xo[(8 * (e >> 2) + 4 * fk + (e & 3)) * 128 + 32 * ni + fr] = acc[mi][ni][e];
+        __syncthreads();
+        const int mrow0 = m0 + wm * 128 + 32 * mi;
+        for (int r = 0; r < 32; ++r) {
+            const int m = mrow0 + r;
+            const float2 v = *(const float2*)(xo + r * 128 + 2 * lane);
+            if (m < p.M && cpair < p.N) {
+                const uint32_t w = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+                *(uint32_t*)(ybase + (size_t)m * ywidth + ycol) = w;
+            }
+        }
+    }
+}
+
+// XCDs of the current device (1 when unknown), cached per device.
+int gemm_xcds()
+{
+    static std::atomic<int> cached[64];
+    int dev = 0, nx = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 1;
+    if ((nx = cached[dev].load(std::memory_order_relaxed)) > 0)
+        return nx;
+    if (hipDeviceGetAttribute(&nx, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || nx < 1)
+        nx = 1;
+    cached[dev].store(nx, std::memory_order_relaxed);
+    return nx;
+}
+
 }  // namespace
 
 hipError_t launch_project(const ProjParams& p, hipStream_t stream)
@@ -447,6 +717,12 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
     if (p.M <= 32) {
         // fused path: W, H and (rank > 0) the adapter rows p.a in one kernel
         return p.M <= 16 ? launch_decode_proj_m<1>(p, stream) : launch_decode_proj_m<2>(p, stream);
+    } else if (p.M >= kGM && p.N >= kGN && !p.yf && p.K % kGK == 0) {
+        const int tiles = ((p.M + kGM - 1) / kGM) * ((p.N + kGN - 1) / kGN);
+        ProjParams q = p;
+        q.nxcd = gemm_xcds();
+        const int per = (tiles + q.nxcd - 1) / q.nxcd;
+        hipLaunchKernelGGL(proj_gemm_kernel, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
     } else {
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + kBM - 1) / kBM);
         hipLaunchKernelGGL(proj_big_kernel, grid, dim3(kThreads), 0, stream, p);
