@@ -446,57 +446,34 @@ __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
 // grid of 128x128 sub-tiles, v_mfma_f32_32x32x16_bf16 (16 accumulators of
 // 32x32 per wave).  A 128x128 sub-tile reads 64 bytes of LDS per 4096 MACs,
 // half of what 64x64 sub-tiles need, which keeps the compute units' LDS
-// bandwidth below what the matrix cores consume.  Operands reach LDS by
-// global_load_lds_dwordx4 (16 bytes per lane, no registers) in a ring of
-// kGStages stages of K = 32; a stage's rows are 64 bytes (four 16-byte
-// chunks) and chunk c of row r is stored at chunk position c ^ sw(r) with
-// sw(r) = (bit1(r) ^ bit3(r)) | bit2(r) << 1, so the rows that one phase of a
-// 16-byte-per-lane fragment read serves (8 rows with 32 banks, 16 with 64)
-// fall on distinct banks.  Workgroups take tiles so that the ones running
-// together on an XCD form a patch of 4 row blocks x 8 column blocks, whose
-// operands its L2 shares.
+// bandwidth below what the matrix cores consume.
+// Operands reach LDS through registers in two stages of K = 64: a copy moves
+// 8 rows x 128 bytes (16 bytes per lane), so every cache line is fetched
+// whole by one instruction (a 64-byte half-line per load doubles the requests
+// the L2 serves).  Each stage's copies are loaded two stages before they are
+// written to LDS (two register sets of 16 x 16 bytes per lane), which hides
+// the latency of the L2 misses that the first touch of every row incurs.
+// Chunk c (16 bytes) of row r sits at chunk position c ^ sw(r),
+// sw(r) = (r & 7) ^ bit3(r): the 8 rows (32 banks) or 16 rows (64 banks)
+// that one phase of a 16-byte fragment read serves fall on distinct banks.
+// Workgroups take tiles so that the ones running together on an XCD form a
+// patch of 4 row blocks x 8 column blocks, whose operands its L2 shares.
 // The adapter branch is applied as a K-extension of the same accumulators
 // (activation hi + lo times B_p), then outputs are rounded once to bf16.
-constexpr int kGM = 256, kGN = 256, kGK = 32, kGStages = 4;
+constexpr int kGM = 256, kGN = 256, kGK = 64;
 constexpr int kGStageBytes = (kGM + kGN) * kGK * 2;  // A then B rows of one stage
-constexpr size_t kGLds = (size_t)kGStages * kGStageBytes;
+constexpr size_t kGLds = 2 * (size_t)kGStageBytes;
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ floatx16 mfma32_bf16(bf16x8 a, bf16x8 b, floatx16 c)
 {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// 16 bytes per lane from global memory to LDS address lds_addr + 16 lane
-// (lds_addr wave-uniform; M0 holds it while the copy issues and is restored).
-// Inline assembly, so that the compiler does not make later LDS reads wait
-// for every outstanding vector memory operation; the explicit waits of the
-// stage ring order them.
-__device__ __forceinline__ void gemm_dma16(const void* src, uint32_t lds_addr)
-{
-    const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "global_load_lds_dwordx4 %2, off\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(m0v), "v"(src)
-        : "memory");
-}
-
-template <int V>
-__device__ __forceinline__ void gemm_wait_vm()
-{
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(V) : "memory");
-}
-
 __device__ __forceinline__ int gemm_swz(int row)
 {
-    return (((row >> 1) ^ (row >> 3)) & 1) | (row & 4) >> 1;
+    return (row & 7) ^ ((row >> 3) & 1);
 }
 
 __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
@@ -518,23 +495,26 @@ __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
     const int grp = t / (kGroupM * nbn), rem = t % (kGroupM * nbn);
     const int gm = min(kGroupM, nbm - grp * kGroupM);
     const int m0 = (grp * kGroupM + rem % gm) * kGM, n0 = (rem / gm) * kGN;
-    const uint32_t lbase = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_void_t*)glds);
 
-    // DMA: each stage is 32 copies of 1 KiB (16 rows x 64 bytes): copies
-    // 0..15 A rows, 16..31 B rows; wave w issues copies 8 w .. 8 w + 7.
-    // Lane i of a copy writes LDS row 16 j + i / 4, chunk position i % 4,
-    // which holds source chunk (i % 4) ^ ((row >> 1) & 3).  Rows past M (N)
-    // re-read the last row; their results are never stored.
-    uint64_t src[8];  // byte addresses of this lane's chunks for k = 0
+    // Copies: a stage is 64 copies of 1 KiB (8 rows x 128 bytes), 0..31 the
+    // A rows and 32..63 the B rows; wave w moves copies 16 w .. 16 w + 15, so
+    // waves 0, 1 read A and waves 2, 3 read B, from a wave-uniform base (the
+    // tile's first row) plus a 32-bit per-lane offset.  Lane i of a copy
+    // writes LDS row 8 j + i / 8, chunk position i % 8, which holds source
+    // chunk (i % 8) ^ sw(row).  Rows past M (N) re-read the last row; their
+    // results are never stored.
+    const bool wisb = wave >= 2;
+    const uint64_t wbase0 = wisb ? (uint64_t)(p.w + (size_t)n0 * p.K) : (uint64_t)(p.x + (size_t)m0 * p.K);
+    const uint32_t blo = __builtin_amdgcn_readfirstlane((uint32_t)wbase0);
+    const uint32_t bhi = __builtin_amdgcn_readfirstlane((uint32_t)(wbase0 >> 32));
+    const uint64_t wbase = ((uint64_t)bhi << 32) | blo;
+    const int rlast = wisb ? p.N - 1 - n0 : p.M - 1 - m0;
+    uint32_t voff[16];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        const int copy = 8 * wave + c;
-        const bool isb = copy >= 16;
-        const int row = 16 * (copy & 15) + (lane >> 2);
-        const int chunk = (lane & 3) ^ gemm_swz(row);
-        const int g = isb ? min(n0 + row, p.N - 1) : min(m0 + row, p.M - 1);
-        const uint16_t* base = isb ? p.w : p.x;
-        src[c] = (uint64_t)(base + (size_t)g * p.K + 8 * chunk);
+    for (int c = 0; c < 16; ++c) {
+        const int row = 8 * ((16 * wave + c) & 31) + (lane >> 3);
+        const int chunk = (lane & 7) ^ gemm_swz(row);
+        voff[c] = (uint32_t)min(row, rlast) * (uint32_t)p.K * 2u + 16u * (uint32_t)chunk;
     }
     const int nks = p.K / kGK;
 
@@ -546,73 +526,104 @@ __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
             acc[mi][ni] = floatx16{};
 
     // fragment rows of this lane (A: tokens, B: weight rows); chunk c of a
-    // row sits at LDS byte row * 64 + 16 (c ^ sw(row)), and the swizzle
+    // row sits at LDS byte row * 128 + 16 (c ^ sw(row)), and the swizzle
     // depends only on the lane (the rows differ by multiples of 32)
     const int fr = lane & 31, fk = lane >> 5, sw = gemm_swz(fr);
-    int aoff[2], boff[2];
+    int aoff[4], boff[4];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-        aoff[kk] = (wm * 128 + fr) * 64 + 16 * ((2 * kk + fk) ^ sw);
-        boff[kk] = kGM * kGK * 2 + (wn * 128 + fr) * 64 + 16 * ((2 * kk + fk) ^ sw);
+    for (int kk = 0; kk < 4; ++kk) {
+        aoff[kk] = (wm * 128 + fr) * 128 + 16 * ((2 * kk + fk) ^ sw);
+        boff[kk] = kGM * kGK * 2 + (wn * 128 + fr) * 128 + 16 * ((2 * kk + fk) ^ sw);
     }
 
-    auto issue = [&](int ks) {
-        const uint32_t st = lbase + (uint32_t)((ks % kGStages) * kGStageBytes);
-#pragma unroll
-        for (int c = 0; c < 8; ++c)
-            gemm_dma16((const void*)(src[c] + (uint64_t)ks * kGK * 2), st + (uint32_t)((8 * wave + c) * 1024));
+    // register staging: stage s's copies are loaded into R[s & 1] two stages
+    // before they are written to LDS buffer s & 1; stages past the end
+    // re-load the last one and land in a free buffer that is never read
+    const uint8_t* gbase = (const uint8_t*)wbase;
+    auto gload = [&](int kst, int j, u32x4* R) {
+        const int kr = min(kst, nks - 1);
+        R[j] = *(const __attribute__((address_space(1))) u32x4*)(gbase + (size_t)kr * kGK * 2 + voff[j]);
+    };
+    auto lstore = [&](int kst, int j, const u32x4* R) {
+        *(u32x4*)(glds + (kst & 1) * kGStageBytes + (16 * wave + j) * 1024 + 16 * lane) = R[j];
     };
     auto fetch = [&](int ks, int kk, bf16x8* fa, bf16x8* fb) {
-        const uint8_t* stg = glds + (ks % kGStages) * kGStageBytes;
+        const uint8_t* stg = glds + (ks & 1) * kGStageBytes;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(stg + aoff[kk] + 2048 * i));
-            fb[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(stg + boff[kk] + 2048 * i));
+            fa[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(stg + aoff[kk] + 4096 * i));
+            fb[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(stg + boff[kk] + 4096 * i));
         }
     };
-    auto mma = [&](const bf16x8* fa, const bf16x8* fb) {
+    // 16 MFMAs of one K = 16 step; after every 4th, one register copy moves:
+    // lstore(sst, j) then gload(sst + 2, j) into the same register
+    auto mma = [&](const bf16x8* fa, const bf16x8* fb, int sst, int j0, u32x4* R) {
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
+        for (int mi = 0; mi < 4; ++mi) {
 #pragma unroll
             for (int ni = 0; ni < 4; ++ni)
                 acc[mi][ni] = mfma32_bf16(fa[mi], fb[ni], acc[mi][ni]);
+            __builtin_amdgcn_sched_barrier(0);
+            lstore(sst, j0 + mi, R);
+            gload(sst + 2, j0 + mi, R);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     };
 
-    // Pipeline: while the 16 MFMAs of one half-stage run, the fragments of
-    // the next half-stage are read from LDS.  Stage ks + 1 becomes readable
-    // at a barrier in the middle of stage ks (all waves' copies of it have
-    // landed, and every wave is done with stage ks - 1, whose buffer then
-    // receives stage ks + 3).
-    for (int ks = 0; ks < kGStages - 1 && ks < nks; ++ks)
-        issue(ks);
-    if (nks >= 3)
-        gemm_wait_vm<16>();
-    else if (nks == 2)
-        gemm_wait_vm<8>();
-    else
-        gemm_wait_vm<0>();
-    __syncthreads();
-    bf16x8 a0[4], b0[4], a1[4], b1[4];
-    fetch(0, 0, a0, b0);
-    for (int ks = 0; ks < nks; ++ks) {
-        fetch(ks, 1, a1, b1);
-        mma(a0, b0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads of the second half
-        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // MFMAs of the first half
-        if (ks + 1 < nks) {
-            if (ks + 2 < nks)
-                gemm_wait_vm<8>();  // stage ks + 2 may still be in flight
-            else
-                gemm_wait_vm<0>();
-            __syncthreads();
-            if (ks + kGStages - 1 < nks)
-                issue(ks + kGStages - 1);
-            fetch(ks + 1, 0, a0, b0);
-        }
-        mma(a1, b1);
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads of the next stage's first half
-        __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // MFMAs of the second half
+    u32x4 R0[16], R1[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+        gload(0, j, R0);
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+        gload(1, j, R1);
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+        lstore(0, j, R0);
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+        gload(2, j, R0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        lstore(1, j, R1);
+        gload(3, j, R1);
     }
+    __syncthreads();
+    bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+    fetch(0, 0, fa0, fb0);
+    // Pipeline, per stage ks (buffer ks & 1), four K = 16 steps t: the MFMAs
+    // of step t run while the fragments of step t + 1 are read.  Steps 0..2
+    // write copies 4..15 of stage ks + 1 (buffer free since the previous
+    // barrier) from Rn = R[(ks + 1) & 1] and refill those registers with
+    // stage ks + 3.  Between steps 2 and 3 a barrier makes stage ks + 1
+    // readable and frees buffer ks & 1 (every wave has read its last
+    // fragments of stage ks); step 3 then writes copies 0..3 of stage ks + 2
+    // from Rc = R[ks & 1] and refills them with stage ks + 4.  A load thus
+    // has two stages to land; the compiler's counters order each LDS write
+    // after its load.
+    auto body = [&](int ks, u32x4* Rc, u32x4* Rn) {
+        fetch(ks, 1, fa1, fb1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa0, fb0, ks + 1, 4, Rn);
+        fetch(ks, 2, fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa1, fb1, ks + 1, 8, Rn);
+        fetch(ks, 3, fa1, fb1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa0, fb0, ks + 1, 12, Rn);
+        __syncthreads();
+        if (ks + 1 < nks)
+            fetch(ks + 1, 0, fa0, fb0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(fa1, fb1, ks + 2, 0, Rc);
+    };
+    int ks = 0;
+    for (; ks + 1 < nks; ks += 2) {
+        body(ks, R0, R1);
+        body(ks + 1, R1, R0);
+    }
+    if (ks < nks)
+        body(ks, R0, R1);
 
     // adapter branch: K-extension over the rank, 16 at a time
     if (p.rank > 0) {
