@@ -18,6 +18,7 @@ the CPU oracle (single thread) on a bounded sample of decode steps.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
   python bench.py --phase prefill [--workload gqa12b_b8]   (projection GEMM, MFMA roofline)
+  python bench.py --phase merge [--workload llama8b_had]    (dense adapter merge, HBM roofline)
 """
 from __future__ import annotations
 
@@ -44,7 +45,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's decode steps)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--phase", choices=["decode", "prefill"], default="decode")
+    ap.add_argument("--phase", choices=["decode", "prefill", "merge"], default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=None)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -116,6 +117,8 @@ def main():
 
     if args.phase == "prefill":
         return bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch)
+    if args.phase == "merge":
+        return bench_merge(args, wl, W, A, Bm, kvq, torch)
 
     # ---------------------------------------------------------------- setup
     T_max = wl.context + wl.decode_steps
@@ -294,6 +297,34 @@ def bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torc
         "config": {"workload": wl.name, "M": M, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / BF16_PEAK_TFLOPS, "traffic": None},
+    }))
+
+
+def bench_merge(args, wl, W, A, Bm, kvq, torch):
+    """Dense adapter merge W' = W + s B_p A_p (Sec. 3.4 deployment): HBM roofline.
+    Algorithmic bytes: read W, A, B and write W' once, all bf16."""
+    out = torch.empty_like(W)
+    for _ in range(args.warmup):
+        kvq.merge_adapter(W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, out)
+    steps = args.steps or 50
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        kvq.merge_adapter(W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, out)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    nbytes = 2 * (2 * W.numel() + A.numel() + Bm.numel())
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "dense adapter merge GB/s", "value": gbs, "unit": "GB/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None},
     }))
 
 

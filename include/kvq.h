@@ -154,6 +154,22 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
                            const void* A, const void* Bm, int rank, float lora_scale, void* Q,
                            void* K, void* V, void* workspace, size_t ws_bytes, void* stream);
 
+/* Dense-merge deployment of the adapter (Sec. 3.4 "Deployment overhead": the
+ * dense-base update can be folded into the weights, leaving the projection
+ * shapes unchanged and removing the adapter branch at inference):
+ *     W'_p = W_p + lora_scale * B_p A_p   for p in {Q, K, V},
+ * accumulated in fp32 and rounded once to bf16 (round to nearest even).
+ * kvq_project_qkv with rank 0 on W' then computes the adapted projection.
+ *   W     bf16 [d_q + 2 d_kv][d_in]  base weights, rows as in kvq_project_qkv
+ *   A     bf16 [3 rank][d_in],  Bm bf16 [d_q + 2 d_kv][rank]
+ *   Wout  bf16 [d_q + 2 d_kv][d_in]  result; may be W itself (in place);
+ *         must not otherwise overlap W, A or Bm.
+ * d_in a multiple of 64; d_q, d_kv multiples of 32; 1 <= rank <= 64.
+ * All pointers 16-byte aligned device memory owned by the caller; nothing is
+ * allocated.  Invalid arguments return KVQ_ERR_ARG before any launch. */
+kvq_status kvq_merge_adapter(const void* W, int d_in, int d_q, int d_kv, const void* A, const void* Bm,
+                             int rank, float lora_scale, void* Wout, void* stream);
+
 /* Append n_new tokens per sequence (Sec. 3.1: new states are coded, packed
  * and appended; the cache keeps no unquantized copy beyond the fp16 window).
  *   K, V  bf16 [B][n_new][H_kv][D] (the natural view of the projection's

@@ -11,6 +11,7 @@ Paper: "Quality Recovery for Quantized KV Caches via Low-Rank Attention
 Adaptation".  Entry points and the passages they follow:
 
 * :func:`project`        -- Sec. 3 Eq. (1)-(2), Sec. 3.4 (explicit adapter).
+* :func:`merge_adapter`  -- Sec. 3.4 (dense-merge deployment W + (alpha/r) B A).
 * :func:`quant_affine`   -- Sec. 3.1 Eq. (3).
 * :func:`quant_sym`      -- Sec. 3.1, symmetric control (a reading).
 * :func:`fwht_f32`       -- Sec. 3.1, fixed normalized Hadamard transform.
@@ -92,6 +93,7 @@ def lib() -> C.CDLL:
                                       C.c_int, P, C.c_int, C.c_double, P]
         L.orc_project.argtypes = [P, C.c_int, C.c_int, P, C.c_int, C.c_int, P, P, C.c_int,
                                   C.c_double, P, P]
+        L.orc_merge_adapter.argtypes = [P, C.c_int, C.c_int, C.c_int, P, P, C.c_int, C.c_double, P, P]
         _lib = L
     return _lib
 
@@ -273,3 +275,24 @@ def project(Hm, W, A, Bm, rank: int, scale: float, d_q: int, d_kv: int):
     if st:
         raise OracleError(st, "project")
     return Y, Yb
+
+
+def merge_adapter(W, A, Bm, rank: int, scale: float, d_q: int, d_kv: int):
+    """Sec. 3.4 dense merge W' = W + scale * B_p A_p row by row.  Returns
+    (W' fp64, W' bf16 bits), each [d_q + 2 d_kv, d_in]."""
+    W = np.ascontiguousarray(W, dtype=np.uint16)
+    N, d_in = W.shape
+    assert N == d_q + 2 * d_kv
+    if rank > 0:
+        A = np.ascontiguousarray(A, dtype=np.uint16)
+        Bm = np.ascontiguousarray(Bm, dtype=np.uint16)
+        assert A.shape == (3 * rank, d_in) and Bm.shape == (N, rank)
+        pa, pb = _ptr(A), _ptr(Bm)
+    else:
+        pa = pb = None
+    Wd = np.zeros((N, d_in), dtype=np.float64)
+    Wb = np.zeros((N, d_in), dtype=np.uint16)
+    st = lib().orc_merge_adapter(_ptr(W), d_in, d_q, d_kv, pa, pb, rank, float(scale), _ptr(Wd), _ptr(Wb))
+    if st:
+        raise OracleError(st, "merge_adapter")
+    return Wd, Wb

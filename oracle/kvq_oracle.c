@@ -10,6 +10,8 @@
  * Adaptation" (Abdellatif).  What each entry point follows:
  *   orc_project       Sec. 3, Eq. (1)-(2) and Sec. 3.4 "Deployment overhead":
  *                     y_p = W_p h + (alpha/r) B_p (A_p h), in fp64.
+ *   orc_merge_adapter Sec. 3.4 "Deployment overhead": the dense-base update
+ *                     folded into the weights, W_p <- W_p + (alpha/r) B_p A_p.
  *   orc_quant_affine  Sec. 3.1 "Physical incremental cache", Eq. (3).
  *   orc_quant_sym     Sec. 3.1, the symmetric control (max-magnitude scale,
  *                     no offset); the exact formula is a reading (below).
@@ -837,5 +839,40 @@ int orc_project(const uint16_t* Hm, int M, int d_in, const uint16_t* W, int d_q,
     }
     free(h);
     free(t);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------ */
+
+/* Dense-merge deployment (Sec. 3.4 "Deployment overhead"): the adapter
+ * branch folded into the base weights, which leaves the projection shapes
+ * unchanged.  For every output row n of projection p (rows of W_Q, then
+ * W_K, then W_V) and input channel i:
+ *   W'[n][i] = W[n][i] + scale * sum_k B[n][k] A[p r + k][i],
+ * accumulated in fp64.  Wd (optional) receives W' in fp64, Wout (optional)
+ * W' rounded once to bf16 (nearest, ties to even).  Same argument shapes as
+ * orc_project; rank 0 copies W. */
+int orc_merge_adapter(const uint16_t* W, int d_in, int d_q, int d_kv, const uint16_t* A, const uint16_t* Bm,
+                      int rank, double scale, double* Wd, uint16_t* Wout)
+{
+    if (d_in < 1 || d_q < 1 || d_kv < 1 || rank < 0 || !W || (!Wd && !Wout))
+        return ORC_ERR_ARG;
+    if (rank > 0 && (!A || !Bm))
+        return ORC_ERR_ARG;
+    const int N = d_q + 2 * d_kv;
+    for (int n = 0; n < N; ++n) {
+        const int p = n < d_q ? 0 : (n < d_q + d_kv ? 1 : 2);
+        for (int i = 0; i < d_in; ++i) {
+            double upd = 0.0;
+            for (int k = 0; k < rank; ++k)
+                upd += (double)bf16_to_f32(Bm[(size_t)n * rank + k]) *
+                       (double)bf16_to_f32(A[((size_t)p * rank + k) * d_in + i]);
+            const double w = (double)bf16_to_f32(W[(size_t)n * d_in + i]) + scale * upd;
+            if (Wd)
+                Wd[(size_t)n * d_in + i] = w;
+            if (Wout)
+                Wout[(size_t)n * d_in + i] = orc_f64_to_bf16(w);
+        }
+    }
     return ORC_OK;
 }

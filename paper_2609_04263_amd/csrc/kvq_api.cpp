@@ -305,6 +305,28 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
     return kvq::launch_project(p, s) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 
+kvq_status kvq_merge_adapter(const void* W, int d_in, int d_q, int d_kv, const void* A, const void* Bm, int rank,
+                             float lora_scale, void* Wout, void* stream)
+{
+    if (d_in < 64 || d_in % 64 != 0 || d_q < 32 || d_kv < 32 || d_q % 32 != 0 || d_kv % 32 != 0)
+        return KVQ_ERR_ARG;
+    if (rank < 1 || rank > 64 || !isfinite(lora_scale))
+        return KVQ_ERR_ARG;
+    if (!W || !A || !Bm || !Wout || !aligned16(W) || !aligned16(A) || !aligned16(Bm) || !aligned16(Wout))
+        return KVQ_ERR_ARG;
+    kvq::MergeParams p = {};
+    p.w = (const uint16_t*)W;
+    p.a = (const uint16_t*)A;
+    p.bm = (const uint16_t*)Bm;
+    p.out = (uint16_t*)Wout;
+    p.d_in = d_in;
+    p.d_q = d_q;
+    p.d_kv = d_kv;
+    p.rank = rank;
+    p.scale = lora_scale;
+    return kvq::launch_merge(p, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+}
+
 kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int n_new, const kvq_format* fmt, void* stream)
 {
     if (!c || !fmt || n_new < 0)

@@ -65,6 +65,17 @@ struct ProjParams {
 };
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
 
+// ---------------------------------------------------------------- merge
+struct MergeParams {
+    const uint16_t* w;    // bf16 [d_q + 2 d_kv][d_in] base weights
+    const uint16_t* a;    // bf16 [3 rank][d_in] adapter down-projections
+    const uint16_t* bm;   // bf16 [d_q + 2 d_kv][rank] adapter up-projections
+    uint16_t* out;        // bf16 [d_q + 2 d_kv][d_in] merged weights (may equal w)
+    int d_in, d_q, d_kv, rank;
+    float scale;          // lora_scale
+};
+hipError_t launch_merge(const MergeParams& p, hipStream_t stream);
+
 // ---------------------------------------------------------------- decode
 struct AttnParams {
     const uint32_t* kc;

@@ -97,8 +97,11 @@ __device__ __forceinline__ void lora_token_operand(const ProjParams& p, int m, i
 
 __device__ __forceinline__ bf16x8 lora_weight_operand(const ProjParams& p, int n, int proj, int kk, int qg)
 {
-    uint16_t v[8];
     const bool ok = n < p.N && proj_of(p, n) == proj;
+    const int k0 = 32 * kk + 8 * qg;
+    if ((p.rank & 7) == 0 && ((uintptr_t)p.bm & 15) == 0)  // eight whole elements or none, 16-byte aligned
+        return (ok && k0 < p.rank) ? load_bf16x8(p.bm + (size_t)n * p.rank + k0) : zero_bf16x8();
+    uint16_t v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
         int k = 32 * kk + 8 * qg + e;
@@ -169,6 +172,13 @@ __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams 
         ap[kt] = p.a + (size_t)(proj * p.rank + min(16 * kt + r, p.rank - 1)) * p.K + 8 * qg;
         aok[kt] = 16 * kt + r < p.rank;
     }
+
+    // the adapter up-projection operands of this wave's row tile (used after
+    // the reduction) are loaded now, so that their latency overlaps the loop
+    bf16x8 bop[NKK > 0 ? NKK : 1];
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+        bop[kk] = wave < R ? lora_weight_operand(p, n0 + 16 * (wave < R ? wave : 0) + r, proj, kk, qg) : zero_bf16x8();
 
     floatx4 acc[R][MT], tacc[MT][NKT > 0 ? NKT : 1];
 #pragma unroll
@@ -254,7 +264,6 @@ __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams 
             out[mt] = red[(rt * MT + mt) * 64 + lane];
 #pragma unroll
         for (int kk = 0; kk < NKK; ++kk) {
-            const bf16x8 bop = lora_weight_operand(p, n0 + 16 * rt + r, proj, kk, qg);
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
                 float v[8];
@@ -265,8 +274,8 @@ __global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams 
                 }
                 bf16x8 hi, lo;
                 split_bf16x8(v, &hi, &lo);
-                out[mt] = mfma16_bf16(bop, hi, out[mt]);
-                out[mt] = mfma16_bf16(bop, lo, out[mt]);
+                out[mt] = mfma16_bf16(bop[kk], hi, out[mt]);
+                out[mt] = mfma16_bf16(bop[kk], lo, out[mt]);
             }
         }
 #pragma unroll

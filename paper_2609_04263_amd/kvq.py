@@ -58,6 +58,7 @@ def _load() -> C.CDLL:
     L.kvq_cache_destroy.restype = None
     L.kvq_project_workspace_bytes.argtypes = [I, I, C.POINTER(S)]
     L.kvq_project_qkv.argtypes = [P, I, I, P, I, I, P, P, I, C.c_float, P, P, P, P, S, P]
+    L.kvq_merge_adapter.argtypes = [P, I, I, I, P, P, I, C.c_float, P, P]
     L.kvq_append.argtypes = [P, P, P, I, Fp, P]
     L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
@@ -71,7 +72,7 @@ def _load() -> C.CDLL:
 _lib = _load()
 EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
             "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
-            "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_append",
+            "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_merge_adapter", "kvq_append",
             "kvq_decode_workspace_bytes", "kvq_decode_attn")
 
 
@@ -207,3 +208,12 @@ def project_qkv(H, W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, 
                               _ptr(Q), _ptr(K), _ptr(V), _ptr(workspace), nbytes, _stream(stream))
     if st:
         _check(st, "project_qkv")
+
+
+def merge_adapter(W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, Wout, stream=None) -> None:
+    """Wout (bf16) <- W + lora_scale * B_p A_p per projection (dense merge; Wout may be W)."""
+    d_in = W.shape[-1]
+    st = _lib.kvq_merge_adapter(_ptr(W), d_in, d_q, d_kv, _ptr(A), _ptr(Bm), rank, lora_scale, _ptr(Wout),
+                                _stream(stream))
+    if st:
+        _check(st, "merge_adapter")

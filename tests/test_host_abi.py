@@ -145,6 +145,26 @@ def test_projection_argument_checks(kvq):
     assert kvq.project_workspace_bytes(4, 8) == 4 * 24 * 4
 
 
+def test_merge_argument_checks(kvq):
+    p = FakeStorage(0, FAKE)
+    mis = FakeStorage(0, FAKE + 8)
+    cases = [
+        (_Shape(96, 96), 8, 64, 64, p),    # d_in not a multiple of 64
+        (_Shape(96, 128), 0, 64, 64, p),   # rank 0: nothing to merge
+        (_Shape(96, 128), 65, 64, 64, p),  # rank above 64
+        (_Shape(96, 128), 8, 48, 64, p),   # d_q not a multiple of 32
+        (_Shape(96, 128), 8, 64, 16, p),   # d_kv below 32
+        (_Shape(96, 128), 8, 64, 64, mis),  # misaligned output
+    ]
+    for W, rank, d_q, d_kv, out in cases:
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.merge_adapter(W, p, p, rank, 2.0, d_q, d_kv, out, stream=0)
+        assert e.value.status == kvq.ERR_ARG
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.merge_adapter(_Shape(96, 128), p, p, 8, float("nan"), 64, 64, p, stream=0)
+    assert e.value.status == kvq.ERR_ARG
+
+
 class _Shape(FakeStorage):
     def __init__(self, M, d_in):
         super().__init__(0, FAKE)
