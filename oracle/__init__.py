@@ -16,7 +16,9 @@ Adaptation".  Entry points and the passages they follow:
 * :func:`quant_sym`      -- Sec. 3.1, symmetric control (a reading).
 * :func:`fwht_f32`       -- Sec. 3.1, fixed normalized Hadamard transform.
 * :class:`Cache`         -- Sec. 3.1 physical incremental cache (append,
-  reconstruction) and Sec. 3.1-3.2 attention over the reconstruction.
+  reconstruction) and Sec. 3.1-3.2 attention over the reconstruction:
+  decode (one query per sequence) and chunked prefill (the chunk's queries,
+  causal, after the chunk is appended).
 
 A bf16 tensor is passed as a ``uint16`` numpy array of its bit patterns.
 """
@@ -91,6 +93,8 @@ def lib() -> C.CDLL:
                                   C.c_int, P, P]
         L.orc_decode_attn.argtypes = [C.POINTER(_Format), C.c_int, C.c_int, C.c_int, C.c_int, P,
                                       C.c_int, P, C.c_int, C.c_double, P]
+        L.orc_prefill_attn.argtypes = [C.POINTER(_Format), C.c_int, C.c_int, C.c_int, C.c_int, P,
+                                       C.c_int, C.c_int, P, C.c_int, C.c_double, P]
         L.orc_project.argtypes = [P, C.c_int, C.c_int, P, C.c_int, C.c_int, P, P, C.c_int,
                                   C.c_double, P, P]
         L.orc_merge_adapter.argtypes = [P, C.c_int, C.c_int, C.c_int, P, P, C.c_int, C.c_double, P, P]
@@ -244,6 +248,19 @@ class Cache:
                                    _ptr(O))
         if st:
             raise OracleError(st, "decode_attn")
+        return O
+
+    def prefill_attn(self, Q: np.ndarray, sm_scale: float) -> np.ndarray:
+        """Causal attention of the last C appended tokens' bf16 queries
+        Q [B, C, H_q, D] over the cache; fp64 [B, C, H_q, D]."""
+        Q = np.ascontiguousarray(Q, dtype=np.uint16)
+        assert Q.ndim == 4 and Q.shape[0] == self.B and Q.shape[3] == self.D
+        O = np.zeros(Q.shape, dtype=np.float64)
+        st = lib().orc_prefill_attn(C.byref(self._f), self.B, self.H, self.D, self.T_max,
+                                    _ptr(self.image), self.n, Q.shape[1], _ptr(Q), Q.shape[2],
+                                    float(sm_scale), _ptr(O))
+        if st:
+            raise OracleError(st, "prefill_attn")
         return O
 
     def section(self, i: int) -> np.ndarray:

@@ -20,6 +20,9 @@
  *                     KIVI's fp16 residual window of recent tokens.
  *   orc_dequant       Sec. 3.2: the reconstruction presented to attention.
  *   orc_decode_attn   Sec. 3.1-3.2: attention over that reconstruction, fp64.
+ *   orc_prefill_attn  Sec. 3.1 "Evaluation consumes 128-token chunks": the
+ *                     chunk's queries attend causally over the
+ *                     reconstruction after the chunk has been appended.
  *
  * Arithmetic: the coding path (Eq. (3), the symmetric code, the Hadamard
  * butterflies) is IEEE binary32, one rounded operation at a time; the file
@@ -777,6 +780,87 @@ int orc_decode_attn(const orc_format* f, int B, int H, int D, int T_max, const u
                     rotate_f64(o, dst, D);
                 else
                     memcpy(dst, o, sizeof(double) * (size_t)D);
+            }
+        }
+    }
+    free(khat);
+    free(vhat);
+    free(logit);
+    free(q);
+    return ORC_OK;
+}
+
+/* Chunked prefill attention (Sec. 3.1: evaluation consumes chunks; the
+ * chunk's states are coded and appended, then the reconstruction feeds
+ * attention).  The cache holds n tokens, the last C of which are the
+ * chunk; Q is bf16 [B][C][H_q][D] for positions n - C .. n - 1 and O is fp64
+ * [B][C][H_q][D].  Query i of the chunk (position n - C + i) attends to the
+ * reconstructed tokens 0 .. n - C + i (causal), otherwise exactly as
+ * orc_decode_attn: max-subtracted softmax of sm * (q . khat_t), q rotated
+ * first and o rotated back when the format rotates.  C = 1 is the decode
+ * attention of the newest token. */
+int orc_prefill_attn(const orc_format* f, int B, int H, int D, int T_max, const uint8_t* image, int n, int C,
+                     const uint16_t* Q, int H_q, double sm, double* O)
+{
+    image_view v;
+    int st = view_init(&v, f, B, H, D, T_max, image);
+    if (st)
+        return st;
+    if (n < 1 || n > T_max || C < 1 || C > n || H_q < H || H_q % H != 0 || !Q || !O)
+        return ORC_ERR_ARG;
+    const int G = H_q / H;
+    double* khat = (double*)malloc(sizeof(double) * (size_t)n * D);
+    double* vhat = (double*)malloc(sizeof(double) * (size_t)n * D);
+    double* logit = (double*)malloc(sizeof(double) * (size_t)n);
+    double* q = (double*)malloc(sizeof(double) * (size_t)D * 2);
+    if (!khat || !vhat || !logit || !q) {
+        free(khat);
+        free(vhat);
+        free(logit);
+        free(q);
+        return ORC_ERR_NOMEM;
+    }
+    double* o = q + D;
+    for (int b = 0; b < B; ++b) {
+        for (int h = 0; h < H; ++h) {
+            reconstruct_bh(&v, b, h, n, khat, vhat);
+            for (int i = 0; i < C; ++i) {
+                const int last = n - C + i;  /* newest token this query sees */
+                for (int hq = h * G; hq < (h + 1) * G; ++hq) {
+                    const uint16_t* qs = Q + (((size_t)b * C + i) * H_q + hq) * D;
+                    for (int d = 0; d < D; ++d)
+                        o[d] = bf16_to_f32(qs[d]);
+                    if (f->rotate)
+                        rotate_f64(o, q, D);
+                    else
+                        memcpy(q, o, sizeof(double) * (size_t)D);
+                    double mx = -INFINITY;
+                    for (int t = 0; t <= last; ++t) {
+                        double acc = 0.0;
+                        for (int d = 0; d < D; ++d)
+                            acc += q[d] * khat[(size_t)t * D + d];
+                        logit[t] = sm * acc;
+                        if (logit[t] > mx)
+                            mx = logit[t];
+                    }
+                    double z = 0.0;
+                    for (int t = 0; t <= last; ++t) {
+                        logit[t] = exp(logit[t] - mx);
+                        z += logit[t];
+                    }
+                    for (int d = 0; d < D; ++d)
+                        o[d] = 0.0;
+                    for (int t = 0; t <= last; ++t) {
+                        double p = logit[t] / z;
+                        for (int d = 0; d < D; ++d)
+                            o[d] += p * vhat[(size_t)t * D + d];
+                    }
+                    double* dst = O + (((size_t)b * C + i) * H_q + hq) * D;
+                    if (f->rotate)
+                        rotate_f64(o, dst, D);
+                    else
+                        memcpy(dst, o, sizeof(double) * (size_t)D);
+                }
             }
         }
     }
