@@ -19,6 +19,7 @@ the CPU oracle (single thread) on a bounded sample of decode steps.
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
   python bench.py --phase prefill [--workload gqa12b_b8]   (projection GEMM, MFMA roofline)
   python bench.py --phase merge [--workload llama8b_had]    (dense adapter merge, HBM roofline)
+  python bench.py --phase prefill_attn [--workload gqa12b_b8] (chunked prefill attention, MFMA roofline)
 """
 from __future__ import annotations
 
@@ -45,7 +46,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's decode steps)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--phase", choices=["decode", "prefill", "merge"], default="decode")
+    ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn"], default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=None)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -141,6 +142,8 @@ def main():
     wsa = cache.decode_workspace(Hq, device=dev)
     sm = 1.0 / float(np.sqrt(D))
     torch.cuda.synchronize()
+    if args.phase == "prefill_attn":
+        return bench_prefill_attn(args, wl, cache, sm, dev, synth, torch)
 
     def restart(timed=False):
         if snapshot is None:
@@ -295,6 +298,40 @@ def bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torc
         "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "M": M, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / BF16_PEAK_TFLOPS, "traffic": None},
+    }))
+
+
+def bench_prefill_attn(args, wl, cache, sm, dev, synth, torch):
+    """Causal attention of the last prefill chunk (C = the workload's chunk,
+    its tokens already appended) over the packed cache of `context` tokens.
+    Algorithmic flops: 4 D per (query head, visible key), i.e.
+    4 B H_q D (C (n - C) + C (C + 1) / 2), against the dense fp16 MFMA peak."""
+    B, Hq, D = wl.B, wl.H_q, wl.D
+    C, n = wl.chunk, wl.context
+    Q = synth.normal_bf16_device(wl.seed, "prefill-attn-q", (B, C, Hq, D), device=dev)
+    O = torch.empty((B, C, Hq, D), dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        cache.prefill_attn(Q, C, Hq, sm, O)
+    steps = args.steps or 20
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        cache.prefill_attn(Q, C, Hq, sm, O)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    flops = 4.0 * B * Hq * D * (C * (n - C) + C * (C + 1) / 2)
+    tflops = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "chunked prefill attention TFLOP/s", "value": tflops, "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u%d/f16" % wl.fmt["k_bits"], "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "H_q": Hq, "H_kv": wl.H_kv, "head_dim": D, "chunk": C,
+                   "context": n, "format": wl.fmt},
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / BF16_PEAK_TFLOPS, "traffic": None},
     }))

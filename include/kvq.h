@@ -203,6 +203,20 @@ kvq_status kvq_decode_workspace_bytes(const kvq_cache* cache, int H_q, size_t* b
 kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
                            void* workspace, size_t ws_bytes, void* stream);
 
+/* Chunked prefill attention (Sec. 3.1: evaluation consumes chunks; the
+ * chunk's states are coded and appended first, then the reconstruction of
+ * everything stored feeds attention).  The chunk is the newest C tokens of
+ * the cache (1 <= C <= n); query i of the chunk, at position n - C + i,
+ * attends causally to the reconstructed tokens 0 .. n - C + i, otherwise
+ * exactly as kvq_decode_attn (same head grouping, rotation and softmax).
+ *   Q  bf16 [B][C][H_q][D]
+ *   O  fp32 [B][C][H_q][D], normalized
+ * H_q a multiple of H_kv.  No workspace.  Pointers 16-byte aligned device
+ * memory owned by the caller; invalid arguments return KVQ_ERR_ARG before
+ * any launch. */
+kvq_status kvq_prefill_attn(const kvq_cache* cache, const void* Q, int C, int H_q, float sm_scale, void* O,
+                            void* stream);
+
 /* Static description of a status code. */
 const char* kvq_strerror(kvq_status status);
 

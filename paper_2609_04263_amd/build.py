@@ -29,7 +29,7 @@ LIB = os.path.join(HERE, "libkvq.so")
 ROOT = os.path.dirname(HERE)
 
 SOURCES = ["kvq_api.cpp", "append.hip", "attn.hip", "attn_d64.hip", "attn_d128.hip", "attn_d256.hip",
-           "project.hip", "merge.hip"]
+           "project.hip", "merge.hip", "prefill.hip"]
 # MFMA accumulators in VGPRs: the attention loop rescales them with VALU
 # instructions, and AGPR accumulators cost a copy each way per block.
 _VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]

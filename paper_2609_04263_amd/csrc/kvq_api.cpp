@@ -436,4 +436,44 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 
+kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, float sm_scale, void* O, void* stream)
+{
+    if (!c || !Q || !O || !aligned16(Q) || !aligned16(O) || !isfinite(sm_scale))
+        return KVQ_ERR_ARG;
+    if (H_q < c->H || H_q % c->H != 0 || C < 1 || C > c->n)
+        return KVQ_ERR_ARG;
+    const kvq_format& f = c->fmt;
+    kvq::AttnParams p = {};
+    p.nq = kvq::num_coded(f, c->n);
+    p.kc = at<uint32_t>(c, 0);
+    p.ks = at<float>(c, 1);
+    p.kz = at<float>(c, 2);
+    p.vc = at<uint32_t>(c, 3);
+    p.vs = at<float>(c, 4);
+    p.vz = at<float>(c, 5);
+    p.kr = at<uint16_t>(c, 6);
+    p.vr = at<uint16_t>(c, 7);
+    p.q = (const uint16_t*)Q;
+    p.out = (float*)O;
+    p.B = c->B;
+    p.H = c->H;
+    p.H_q = H_q;
+    p.G = H_q / c->H;
+    p.T = c->T_alloc;
+    p.n = c->n;
+    p.C = C;
+    p.ring = f.residual + f.flush;
+    p.k_bits = f.k_bits;
+    p.v_bits = f.v_bits;
+    p.k_mode = f.k_mode;
+    p.v_mode = f.v_mode;
+    p.k_axis = f.k_axis;
+    p.k_group = f.k_group;
+    p.v_group = f.v_group;
+    p.rotate = f.rotate;
+    p.sm_log2 = sm_scale * 1.4426950408889634f;
+    p.rot_c = rotation_constant(c->D);
+    return kvq::launch_prefill(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+}
+
 }  // extern "C"

@@ -101,6 +101,7 @@ struct AttnParams {
     float sm_log2;        // softmax scale * log2(e)
     float rot_c;
     size_t lds_bytes;     // dynamic LDS of the split kernel
+    int C;                // chunked prefill: query tokens (the newest C of the cache); q is [B][C][H_q][D]
 };
 // Workgroups of the split kernel that fit the device at once (all fields of p
 // that select the kernel instance and its LDS must be set).
@@ -113,5 +114,6 @@ int decode_split_bound(int B, int H);
 // Dynamic LDS of the split kernel.
 size_t decode_lds_bytes(int D, const kvq_format& f, int G);
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
+hipError_t launch_prefill(const AttnParams& p, int D, hipStream_t stream);
 
 }  // namespace kvq

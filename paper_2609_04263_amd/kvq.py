@@ -62,6 +62,7 @@ def _load() -> C.CDLL:
     L.kvq_append.argtypes = [P, P, P, I, Fp, P]
     L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
+    L.kvq_prefill_attn.argtypes = [P, P, I, I, C.c_float, P, P]
     for name in ("kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section", "kvq_cache_reset",
                  "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_project_workspace_bytes",
                  "kvq_project_qkv", "kvq_append", "kvq_decode_workspace_bytes", "kvq_decode_attn"):
@@ -73,7 +74,7 @@ _lib = _load()
 EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
             "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
             "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_merge_adapter", "kvq_append",
-            "kvq_decode_workspace_bytes", "kvq_decode_attn")
+            "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_prefill_attn")
 
 
 def lib() -> C.CDLL:
@@ -189,6 +190,14 @@ class Cache:
                                   nbytes, _stream(stream))
         if st:
             _check(st, "decode_attn")
+
+    def prefill_attn(self, Q, C_len: int, H_q: int, sm_scale: float, O, stream=None) -> None:
+        """O[B, C, H_q, D] (fp32) <- causal attention of the newest C_len tokens'
+        bf16 queries Q[B, C, H_q, D] over the cache."""
+        st = _lib.kvq_prefill_attn(self.handle, Q.data_ptr(), C_len, H_q, sm_scale, O.data_ptr(),
+                                   _stream(stream))
+        if st:
+            _check(st, "prefill_attn")
 
 
 # ------------------------------------------------------------- projection

@@ -110,6 +110,23 @@ def test_errors_leave_cache_unchanged(kvq):
             c.decode_workspace_bytes(bad)
 
 
+def test_prefill_argument_checks(kvq):
+    f = configs.make_format()
+    c = kvq.Cache(f, 2, 2, 64, 64, storage=FakeStorage(kvq.cache_bytes(f, 2, 2, 64, 64)))
+    q = FakeStorage(0, FAKE)
+    # empty cache: no chunk can be attended
+    with pytest.raises(kvq.KvqError) as e:
+        c.prefill_attn(q, 1, 4, 0.125, q, stream=0)
+    assert e.value.status == kvq.ERR_ARG
+    # misaligned output, bad head grouping
+    with pytest.raises(kvq.KvqError) as e:
+        c.prefill_attn(q, 1, 4, 0.125, FakeStorage(0, FAKE + 4), stream=0)
+    assert e.value.status == kvq.ERR_ARG
+    with pytest.raises(kvq.KvqError) as e:
+        c.prefill_attn(q, 1, 3, 0.125, q, stream=0)
+    assert e.value.status == kvq.ERR_ARG
+
+
 def test_rewind_only_without_window(kvq):
     f = configs.WORKLOADS["llama8b_kivi"].fmt
     c = kvq.Cache(f, 1, 1, 128, 64, storage=FakeStorage(kvq.cache_bytes(f, 1, 1, 128, 64)))
