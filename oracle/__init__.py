@@ -35,7 +35,7 @@ _SRC = os.path.join(_HERE, "kvq_oracle.c")
 _LIB = os.path.join(_HERE, "libkvq_oracle.so")
 
 FORMAT_FIELDS = ("k_bits", "v_bits", "k_mode", "v_mode", "k_axis", "v_axis",
-                 "k_group", "v_group", "residual", "flush", "rotate")
+                 "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16")
 
 ERRORS = {0: "ok", 1: "bad argument", 2: "bad format", 3: "capacity exceeded",
           4: "non-finite input", 5: "out of memory"}
@@ -80,6 +80,8 @@ def lib() -> C.CDLL:
         L.orc_f64_to_bf16.restype = C.c_uint16
         L.orc_quant_affine.argtypes = [P, C.c_int, C.c_int, P, P, P]
         L.orc_quant_sym.argtypes = [P, C.c_int, C.c_int, P, P]
+        L.orc_quant_affine16.argtypes = [P, C.c_int, C.c_int, P, P, P]
+        L.orc_quant_sym16.argtypes = [P, C.c_int, C.c_int, P, P]
         L.orc_pack_word.argtypes = [P, C.c_int]
         L.orc_pack_word.restype = C.c_uint32
         L.orc_unpack_word.argtypes = [C.c_uint32, C.c_int, P]
@@ -108,7 +110,7 @@ def _ptr(a: np.ndarray):
 
 
 def _fmt(fmt) -> _Format:
-    return _Format(*[int(fmt[name]) for name in FORMAT_FIELDS])
+    return _Format(*[int(fmt.get(name, 0)) for name in FORMAT_FIELDS])
 
 
 # ---------------------------------------------------------------- scalars
@@ -150,6 +152,25 @@ def quant_sym(x, bits: int):
     codes = np.zeros(x.size, dtype=np.uint8)
     s = np.zeros(1, dtype=np.float32)
     lib().orc_quant_sym(_ptr(x), x.size, bits, _ptr(codes), _ptr(s))
+    return codes, s[0]
+
+
+def quant_affine16(x, bits: int):
+    """Eq. (3) with fp16 metadata: returns (codes, scale fp16 bits, offset fp16 bits)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.zeros(x.size, dtype=np.uint8)
+    s = np.zeros(1, dtype=np.uint16)
+    z = np.zeros(1, dtype=np.uint16)
+    lib().orc_quant_affine16(_ptr(x), x.size, bits, _ptr(codes), _ptr(s), _ptr(z))
+    return codes, s[0], z[0]
+
+
+def quant_sym16(x, bits: int):
+    """Symmetric control with an fp16 scale: returns (codes, scale fp16 bits)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    codes = np.zeros(x.size, dtype=np.uint8)
+    s = np.zeros(1, dtype=np.uint16)
+    lib().orc_quant_sym16(_ptr(x), x.size, bits, _ptr(codes), _ptr(s))
     return codes, s[0]
 
 

@@ -15,6 +15,8 @@
  *   orc_quant_affine  Sec. 3.1 "Physical incremental cache", Eq. (3).
  *   orc_quant_sym     Sec. 3.1, the symmetric control (max-magnitude scale,
  *                     no offset); the exact formula is a reading (below).
+ *   orc_quant_*16     the same with the metadata stored as fp16, as the
+ *                     paper stores it (Sec. 3.1); rounding is a reading.
  *   orc_fwht_f32      Sec. 3.1, KVarN's fixed normalized Hadamard transform.
  *   orc_append        Sec. 3.1: new states are coded, packed and appended;
  *                     KIVI's fp16 residual window of recent tokens.
@@ -44,12 +46,14 @@
  *       (((u*NB + beta)*2 + e)*64 + r + 16*(P%4)) * (D/32) + P/4
  *   Vc  piece (o, d) = tokens 8o..8o+7 (octet o) of channel d, at index
  *       ((u*NB + o/4)*64 + d%16 + 16*(o%4)) * (D/16) + d/16
- *   Ks  f32 per-token K scale of group g (channels g*kg ..), at
+ *   Ks  per-token K scale of group g (channels g*kg ..), fp32 (fp16 when
+ *       meta_fp16; element i at byte i*4 or i*2 of the section), at
  *       ((u*NB + beta)*(D/kg) + g)*32 + tau
  *       f32 per-channel K scale of (32-token group beta, channel d), at
  *       (u*NB + beta)*D + d
  *   Kz  like Ks, affine K only (zero bytes for symmetric K)
- *   Vs  f32 per-token V scale of group g, at ((u*NB + beta)*(D/vg) + g)*32 + tau
+ *   Vs  per-token V scale of group g (fp32 or fp16 like Ks), at
+ *       ((u*NB + beta)*(D/vg) + g)*32 + tau
  *   Vz  like Vs, affine V only
  *   Kr  f16 [B][H][R+F][D]             fp16 residual ring (F > 0 only)
  *   Vr  f16 [B][H][R+F][D]
@@ -80,6 +84,7 @@ typedef struct {
     int k_group, v_group; /* group size: head_dim elements, or tokens for per-channel K */
     int residual, flush;  /* fp16 window: R newest tokens kept, flushed F at a time; 0,0 = none */
     int rotate;           /* 0, or head_dim: Hadamard rotation of K/V before coding */
+    int meta_fp16;        /* 0: fp32 scales and offsets; 1: fp16 (the paper's storage) */
 } orc_format;
 
 /* ------------------------------------------------------------------ */
@@ -231,6 +236,58 @@ void orc_quant_sym(const float* x, int g, int bits, uint8_t* codes, float* s_out
     *s_out = s;
 }
 
+/* fp16 metadata (Sec. 3.1 stores "an FP16 scale, and an FP16 offset").
+ * Reading: the scale and offset are computed in fp32 exactly as above, then
+ * rounded to fp16 (nearest, ties to even), the scale first clamped to
+ * [2^-24, 65504] (the 1e-8 floor lies below fp16's smallest subnormal) and
+ * the offset to [-65504, 65504]; the codes are then computed from the
+ * rounded values, so they are the best codes for the metadata actually
+ * stored.  s16 / z16 receive the fp16 bit patterns. */
+static float to_f16_value(float v, float lo, float hi)
+{
+    if (v < lo)
+        v = lo;
+    if (v > hi)
+        v = hi;
+    return orc_f16_to_f32(orc_f32_to_f16(v));
+}
+
+void orc_quant_affine16(const float* x, int g, int bits, uint8_t* codes, uint16_t* s16, uint16_t* z16)
+{
+    float s, z;
+    orc_quant_affine(x, g, bits, codes, &s, &z);
+    s = to_f16_value(s, 0x1p-24f, 65504.0f);
+    z = to_f16_value(z, -65504.0f, 65504.0f) + 0.0f;
+    const float top = (float)((1 << bits) - 1);
+    for (int i = 0; i < g; ++i) {
+        float c = rintf((x[i] - z) / s);
+        if (c < 0.0f)
+            c = 0.0f;
+        if (c > top)
+            c = top;
+        codes[i] = (uint8_t)c;
+    }
+    *s16 = orc_f32_to_f16(s);
+    *z16 = orc_f32_to_f16(z);
+}
+
+void orc_quant_sym16(const float* x, int g, int bits, uint8_t* codes, uint16_t* s16)
+{
+    float s;
+    orc_quant_sym(x, g, bits, codes, &s);
+    s = to_f16_value(s, 0x1p-24f, 65504.0f);
+    const float qmax = (float)((1 << (bits - 1)) - 1);
+    for (int i = 0; i < g; ++i) {
+        float q = rintf(x[i] / s);
+        if (q < -qmax)
+            q = -qmax;
+        if (q > qmax)
+            q = qmax;
+        codes[i] = (uint8_t)(int)(q + (float)(1 << (bits - 1)));
+    }
+    *s16 = orc_f32_to_f16(s);
+}
+
 /* Packing: the run c[0..32/b) goes into one little-endian 32-bit word,
  * element j at bits [b*j, b*j + b). */
 uint32_t orc_pack_word(const uint8_t* codes, int bits)
@@ -333,6 +390,8 @@ int orc_check_format(const orc_format* f, int D)
     }
     if (!is_pow2_in(f->v_group, 32, D))
         return ORC_ERR_FORMAT;
+    if (f->meta_fp16 != 0 && f->meta_fp16 != 1)
+        return ORC_ERR_FORMAT;
     return ORC_OK;
 }
 
@@ -353,13 +412,14 @@ int orc_layout(const orc_format* f, int B, int H, int D, int T_max, size_t off[8
     size_t T = round_up((size_t)T_max, 32);
     size_t ring = (size_t)(f->residual + f->flush);
     len[0] = bh * T * (size_t)(D * f->k_bits / 32) * 4;
+    const size_t msz = f->meta_fp16 ? 2 : 4; /* bytes per scale or offset */
     if (f->k_axis == 0)
-        len[1] = bh * T * (size_t)(D / f->k_group) * 4;
+        len[1] = bh * T * (size_t)(D / f->k_group) * msz;
     else
-        len[1] = bh * (T / 32) * (size_t)D * 4;
+        len[1] = bh * (T / 32) * (size_t)D * msz;
     len[2] = f->k_mode == 0 ? len[1] : 0;
     len[3] = bh * (T * f->v_bits / 32) * (size_t)D * 4;
-    len[4] = bh * T * (size_t)(D / f->v_group) * 4;
+    len[4] = bh * T * (size_t)(D / f->v_group) * msz;
     len[5] = f->v_mode == 0 ? len[4] : 0;
     len[6] = f->flush ? bh * ring * (size_t)D * 2 : 0;
     len[7] = len[6];
@@ -488,9 +548,28 @@ static uint16_t* ring_entry(const image_view* v, int which, int b, int h, int t)
     return (uint16_t*)(v->img + v->off[which ? 7 : 6]) + i;
 }
 
-static float* meta_f32(const image_view* v, int section)
+/* Scale or offset i of a metadata section (1, 2, 4, 5), fp32 or fp16. */
+static float meta_get(const image_view* v, int section, size_t i)
 {
-    return (float*)(v->img + v->off[section]);
+    if (v->f->meta_fp16) {
+        uint16_t h;
+        memcpy(&h, v->img + v->off[section] + 2 * i, 2);
+        return orc_f16_to_f32(h);
+    }
+    float x;
+    memcpy(&x, v->img + v->off[section] + 4 * i, 4);
+    return x;
+}
+
+/* Store a value that the section's precision represents exactly. */
+static void meta_put(const image_view* v, int section, size_t i, float x)
+{
+    if (v->f->meta_fp16) {
+        uint16_t h = orc_f32_to_f16(x);
+        memcpy(v->img + v->off[section] + 2 * i, &h, 2);
+    } else {
+        memcpy(v->img + v->off[section] + 4 * i, &x, 4);
+    }
 }
 
 /* ------------------------------------------------------------------ */
@@ -522,8 +601,18 @@ static void token_values(const image_view* v, int which, const uint16_t* X, int 
     }
 }
 
-static void code_group(int mode, int bits, const float* x, int g, uint8_t* codes, float* s, float* z)
+static void code_group(int mode, int bits, int meta16, const float* x, int g, uint8_t* codes, float* s, float* z)
 {
+    if (meta16) {
+        uint16_t s16, z16 = 0;
+        if (mode == 0)
+            orc_quant_affine16(x, g, bits, codes, &s16, &z16);
+        else
+            orc_quant_sym16(x, g, bits, codes, &s16);
+        *s = orc_f16_to_f32(s16);
+        *z = orc_f16_to_f32(z16);
+        return;
+    }
     if (mode == 0) {
         orc_quant_affine(x, g, bits, codes, s, z);
     } else {
@@ -563,10 +652,7 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
         free(codes);
         return ORC_ERR_NOMEM;
     }
-    float* Ks = meta_f32(&v, 1);
-    float* Kz = meta_f32(&v, 2);
-    float* Vs = meta_f32(&v, 4);
-    float* Vz = meta_f32(&v, 5);
+    const int m16 = f->meta_fp16;
 
     for (int b = 0; b < B; ++b) {
         for (int h = 0; h < H; ++h) {
@@ -576,11 +662,11 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                     token_values(&v, 0, K, n0, n_new, b, h, t, x);
                     for (int d0 = 0; d0 < D; d0 += f->k_group) {
                         float s, z;
-                        code_group(f->k_mode, kb, x + d0, f->k_group, codes + d0, &s, &z);
+                        code_group(f->k_mode, kb, m16, x + d0, f->k_group, codes + d0, &s, &z);
                         size_t mi = kmeta_index(&v, b, h, t, d0);
-                        Ks[mi] = s;
+                        meta_put(&v, 1, mi, s);
                         if (f->k_mode == 0)
-                            Kz[mi] = z;
+                            meta_put(&v, 2, mi, z);
                     }
                     for (int P = 0; P < D / 8; ++P)
                         piece_put(kc_piece(&v, b, h, t, P), kb, pack8(codes + 8 * P, kb));
@@ -596,11 +682,11 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                         float s, z;
                         for (int i = 0; i < 32; ++i)
                             col[i] = x[(size_t)i * D + d];
-                        code_group(f->k_mode, kb, col, 32, cc, &s, &z);
+                        code_group(f->k_mode, kb, m16, col, 32, cc, &s, &z);
                         size_t mi = kmeta_index(&v, b, h, t0, d);
-                        Ks[mi] = s;
+                        meta_put(&v, 1, mi, s);
                         if (f->k_mode == 0)
-                            Kz[mi] = z;
+                            meta_put(&v, 2, mi, z);
                         for (int i = 0; i < 32; ++i)
                             codes[(size_t)i * D + d] = cc[i];
                     }
@@ -616,11 +702,11 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                 token_values(&v, 1, V, n0, n_new, b, h, t, x);
                 for (int d0 = 0; d0 < D; d0 += f->v_group) {
                     float s, z;
-                    code_group(f->v_mode, vb, x + d0, f->v_group, codes + d0, &s, &z);
+                    code_group(f->v_mode, vb, m16, x + d0, f->v_group, codes + d0, &s, &z);
                     size_t mi = vmeta_index(&v, b, h, t, d0);
-                    Vs[mi] = s;
+                    meta_put(&v, 4, mi, s);
                     if (f->v_mode == 0)
-                        Vz[mi] = z;
+                        meta_put(&v, 5, mi, z);
                 }
                 int j = t % 8;
                 uint32_t keep = j == 0 ? 0u : ((1u << (vb * j)) - 1u);
@@ -670,10 +756,6 @@ static void reconstruct_bh(const image_view* v, int b, int h, int n, double* kha
     const orc_format* f = v->f;
     int D = v->D, nq = orc_num_coded(f, n);
     const int kb = f->k_bits, vb = f->v_bits;
-    const float* Ks = meta_f32(v, 1);
-    const float* Kz = meta_f32(v, 2);
-    const float* Vs = meta_f32(v, 4);
-    const float* Vz = meta_f32(v, 5);
     for (int t = 0; t < n; ++t) {
         for (int d = 0; d < D; ++d) {
             double kv, vv;
@@ -681,11 +763,11 @@ static void reconstruct_bh(const image_view* v, int b, int h, int n, double* kha
                 uint32_t kw = piece_get(kc_piece(v, b, h, t, d / 8), kb);
                 uint32_t kc = (kw >> (kb * (d % 8))) & ((1u << kb) - 1u);
                 size_t km = kmeta_index(v, b, h, t, d);
-                kv = dequant_code(f->k_mode, kb, kc, Ks[km], f->k_mode == 0 ? Kz[km] : 0.0f);
+                kv = dequant_code(f->k_mode, kb, kc, meta_get(v, 1, km), f->k_mode == 0 ? meta_get(v, 2, km) : 0.0f);
                 uint32_t vw = piece_get(vc_piece(v, b, h, t, d), vb);
                 uint32_t vc = (vw >> (vb * (t % 8))) & ((1u << vb) - 1u);
                 size_t vm = vmeta_index(v, b, h, t, d);
-                vv = dequant_code(f->v_mode, vb, vc, Vs[vm], f->v_mode == 0 ? Vz[vm] : 0.0f);
+                vv = dequant_code(f->v_mode, vb, vc, meta_get(v, 4, vm), f->v_mode == 0 ? meta_get(v, 5, vm) : 0.0f);
             } else {
                 kv = orc_f16_to_f32(ring_entry(v, 0, b, h, t)[d]);
                 vv = orc_f16_to_f32(ring_entry(v, 1, b, h, t)[d]);

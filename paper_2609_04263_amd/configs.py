@@ -17,10 +17,11 @@ PER_TOKEN, PER_CHANNEL = 0, 1
 
 
 def make_format(k_bits=4, v_bits=4, k_mode=AFFINE, v_mode=AFFINE, k_axis=PER_TOKEN,
-                v_axis=PER_TOKEN, k_group=64, v_group=64, residual=0, flush=0, rotate=0) -> dict:
+                v_axis=PER_TOKEN, k_group=64, v_group=64, residual=0, flush=0, rotate=0,
+                meta_fp16=0) -> dict:
     return dict(k_bits=k_bits, v_bits=v_bits, k_mode=k_mode, v_mode=v_mode, k_axis=k_axis,
                 v_axis=v_axis, k_group=k_group, v_group=v_group, residual=residual,
-                flush=flush, rotate=rotate)
+                flush=flush, rotate=rotate, meta_fp16=meta_fp16)
 
 
 @dataclass(frozen=True)
@@ -116,11 +117,12 @@ def projection_weight_bytes(d_in: int, d_q: int, d_kv: int, rank: int) -> int:
     return 2 * (N * d_in + 3 * rank * d_in + N * rank)
 
 
-def coded_bytes_per_token(D: int, bits: int, axis: int, group: int, affine: bool) -> float:
-    """Cache bytes of one coded token of one KV head: packed codes plus fp32
-    metadata (scale, and offset when affine).  Per-channel groups share one
-    scale/offset per channel across ``group`` tokens."""
-    meta = 8 if affine else 4
+def coded_bytes_per_token(D: int, bits: int, axis: int, group: int, affine: bool, meta_fp16: int = 0) -> float:
+    """Cache bytes of one coded token of one KV head: packed codes plus
+    metadata (scale, and offset when affine; fp32, or fp16 with meta_fp16).
+    Per-channel groups share one scale/offset per channel across ``group``
+    tokens."""
+    meta = (8 if affine else 4) // (2 if meta_fp16 else 1)
     if axis == PER_TOKEN:
         return D * bits / 8 + (D // group) * meta
     return D * bits / 8 + D * meta / group
@@ -140,7 +142,8 @@ def attention_bytes(wl: Workload, n: int) -> int:
     queries and the fp32 outputs.  Split-K partials are not counted."""
     f = wl.fmt
     nq = num_coded(f, n)
-    bk = coded_bytes_per_token(wl.D, f["k_bits"], f["k_axis"], f["k_group"], f["k_mode"] == AFFINE)
-    bv = coded_bytes_per_token(wl.D, f["v_bits"], f["v_axis"], f["v_group"], f["v_mode"] == AFFINE)
+    m16 = f.get("meta_fp16", 0)
+    bk = coded_bytes_per_token(wl.D, f["k_bits"], f["k_axis"], f["k_group"], f["k_mode"] == AFFINE, m16)
+    bv = coded_bytes_per_token(wl.D, f["v_bits"], f["v_axis"], f["v_group"], f["v_mode"] == AFFINE, m16)
     per_head = nq * (bk + bv) + (n - nq) * 4 * wl.D
     return int(round(wl.B * wl.H_kv * per_head)) + 2 * wl.B * wl.H_q * wl.D + 4 * wl.B * wl.H_q * wl.D

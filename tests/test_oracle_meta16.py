@@ -1,0 +1,113 @@
+"""Pins of the oracle's fp16 metadata (Sec. 3.1 stores an FP16 scale and an
+FP16 offset; the rounding rule is a reading: fp32 statistics rounded to
+nearest fp16, scale clamped to [2^-24, 65504], codes from the rounded values).
+
+* hand-worked groups whose statistics are exact in fp16 give the same codes
+  and metadata as the fp32 coder;
+* a hand-worked group whose scale is not exact in fp16: the stored scale is
+  the nearest fp16 and the codes follow it, not the fp32 scale;
+* the floor: a constant group stores the smallest fp16 subnormal, 2^-24
+  (1e-8 is not representable), and reconstructs exactly;
+* properties on random groups: metadata are the nearest fp16 of the fp32
+  statistics; every value reconstructs within half a (stored) step plus the
+  offset's rounding; codes are the nearest levels of the stored grid
+  (brute force);
+* a cache with fp16 metadata has half-size metadata sections and
+  reconstructs each token from its own fp16 scale and offset.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_04263_amd import configs, synth
+
+
+def f16(bits):
+    return oracle.f16_to_f32(np.asarray(bits, dtype=np.uint16)).astype(np.float64)
+
+
+def test_exact_statistics_match_the_fp32_coder():
+    x = np.array([-2.0, 3.0, 5.0, 11.0, 28.0], dtype=np.float32)  # s = 2, min = -2
+    c16, s16, z16 = oracle.quant_affine16(x, 4)
+    c32, s32, z32 = oracle.quant_affine(x, 4)
+    assert np.array_equal(c16, c32) and f16(s16) == s32 and f16(z16) == z32
+    cs16, ss16 = oracle.quant_sym16(np.array([-1.5, 0.5, 3.5, -3.5], dtype=np.float32), 4)  # s = 0.5
+    cs32, ss32 = oracle.quant_sym(np.array([-1.5, 0.5, 3.5, -3.5], dtype=np.float32), 4)
+    assert np.array_equal(cs16, cs32) and f16(ss16) == ss32
+
+
+def test_inexact_scale_is_rounded_and_codes_follow_it():
+    # max - min = 1, 4-bit: s32 = 1/15 = 0.0666..., fp16 nearest = 0.06665039 (0x2C44)
+    x = np.array([0.0, 0.5, 1.0], dtype=np.float32)
+    codes, s16, z16 = oracle.quant_affine16(x, 4)
+    assert s16 == 0x2C44 and z16 == 0
+    # 0.5 / 0.06665039 = 7.5018 -> 8; 1 / 0.06665039 = 15.0037 -> 15 (clipped to 15)
+    assert codes.tolist() == [0, 8, 15]
+    assert abs(f16(s16) - 1.0 / 15) < 2 ** -11 * (1.0 / 15)
+
+
+def test_constant_group_stores_fp16_floor():
+    x = np.full(8, 1.25, dtype=np.float32)
+    codes, s16, z16 = oracle.quant_affine16(x, 2)
+    assert s16 == 0x0001 and f16(z16) == 1.25          # 2^-24, the smallest subnormal
+    assert np.all(codes == 0)
+    cs, ss = oracle.quant_sym16(np.zeros(8, dtype=np.float32), 4)
+    assert ss == 0x0001 and np.all(cs == 8)
+
+
+@pytest.mark.parametrize("bits,g", [(2, 32), (4, 64), (4, 128)])
+def test_affine16_properties(bits, g):
+    rng = np.random.default_rng(bits * 1000 + g)
+    top = 2 ** bits - 1
+    for _ in range(40):
+        x = (rng.standard_normal(g) * rng.choice([1e-3, 1.0, 30.0])).astype(np.float32)
+        codes, s16, z16 = oracle.quant_affine16(x, bits)
+        _, s32, z32 = oracle.quant_affine(x, bits)
+        # metadata are the nearest fp16 of the fp32 statistics
+        assert s16 == oracle.f32_to_f16(max(s32, np.float32(2.0 ** -24)))
+        assert z16 == oracle.f32_to_f16(z32)
+        s, z = f16(s16), f16(z16)
+        xr = codes * s + z
+        # half a step of the stored grid, plus the offset's own rounding
+        assert np.all(np.abs(xr - x) <= s / 2 * (1 + 2 ** -9) + abs(z - float(z32)) + 1e-30)
+        # nearest level of the stored grid (brute force over all levels)
+        levels = np.arange(top + 1) * s + z
+        best = np.abs(x[:, None].astype(np.float64) - levels[None, :]).min(axis=1)
+        assert np.all(np.abs(xr - x) <= best * (1 + 1e-6) + 1e-12)
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+def test_sym16_properties(bits):
+    rng = np.random.default_rng(bits)
+    half = 2 ** (bits - 1)
+    for _ in range(40):
+        x = (rng.standard_normal(64) * 3).astype(np.float32)
+        codes, s16 = oracle.quant_sym16(x, bits)
+        _, s32 = oracle.quant_sym(x, bits)
+        assert s16 == oracle.f32_to_f16(s32)
+        s = f16(s16)
+        q = codes.astype(np.float64) - half
+        assert np.all(np.abs(q) <= half - 1)
+        levels = np.arange(-(half - 1), half) * s
+        best = np.abs(x[:, None].astype(np.float64) - levels[None, :]).min(axis=1)
+        assert np.all(np.abs(q * s - x) <= best * (1 + 1e-6) + 1e-12)
+
+
+def test_cache_with_fp16_metadata():
+    f32 = configs.make_format(4, 2, k_group=64, v_group=32)
+    f16_ = configs.make_format(4, 2, k_group=64, v_group=32, meta_fp16=1)
+    B, H, D, T = 1, 2, 64, 64
+    _, len32, _ = oracle.layout(f32, B, H, D, T)
+    _, len16, _ = oracle.layout(f16_, B, H, D, T)
+    assert [len16[i] * (2 if i in (1, 2, 4, 5) else 1) for i in range(8)] == list(len32)
+    K, V = synth.kv_tokens(7, B, 40, H, D)
+    c = oracle.Cache(f16_, B, H, D, T)
+    c.append(K, V)
+    kh, vh = c.dequant()
+    # token 5 of head 1 by hand: K group 0 (channels 0..63), V group 1 (channels 32..63)
+    kx = synth.bf16_bits_to_f32(K[0, 5, 1])
+    codes, s16, z16 = oracle.quant_affine16(kx, 4)
+    assert np.allclose(kh[0, 1, 5], codes * f16(s16) + f16(z16), rtol=0, atol=0)
+    vx = synth.bf16_bits_to_f32(V[0, 5, 1, 32:])
+    vcodes, vs16, vz16 = oracle.quant_affine16(vx, 2)
+    assert np.allclose(vh[0, 1, 5, 32:], vcodes * f16(vs16) + f16(vz16), rtol=0, atol=0)
