@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn"], default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--meta-fp16", action="store_true",
+                    help="store scales and offsets as fp16 (the paper's storage) instead of the workload's fp32")
     ap.add_argument("--cpu-sample-steps", type=int, default=None)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the timed region, copy a buffer of this many MiB once (a kernel of known "
@@ -103,6 +105,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     wl = configs.WORKLOADS[args.workload]
+    if args.meta_fp16:
+        import dataclasses
+        wl = dataclasses.replace(wl, name=wl.name + "+meta16", fmt=dict(wl.fmt, meta_fp16=1))
     B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
 
     def bf16(bits):

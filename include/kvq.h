@@ -62,7 +62,11 @@ enum { KVQ_PER_TOKEN = 0, KVQ_PER_CHANNEL = 1 };
  *   rotate   0, or head_dim: apply the fixed normalized Hadamard transform
  *            (KVarN, Sec. 3.1) to K and V before coding, to queries before
  *            attention and to outputs after it.
- * Scales and offsets are stored as fp32. */
+ *   meta_fp16  0: scales and offsets stored as fp32.  1: stored as fp16, as
+ *            the paper stores them (Sec. 3.1): the fp32 scale and offset
+ *            are rounded to nearest fp16 (scale clamped to [2^-24, 65504],
+ *            offset to +-65504) and the codes are computed from the rounded
+ *            values (this rounding rule is this library's reading). */
 typedef struct {
     int32_t k_bits, v_bits;
     int32_t k_mode, v_mode;
@@ -70,6 +74,7 @@ typedef struct {
     int32_t k_group, v_group;
     int32_t residual, flush;
     int32_t rotate;
+    int32_t meta_fp16;
 } kvq_format;
 
 /* Opaque host handle: format, dimensions, storage pointer, token count. */
@@ -79,11 +84,12 @@ typedef struct kvq_cache kvq_cache;
  * 256) and up to T_max tokens.  The storage image has eight sections, each
  * starting at a multiple of 256 bytes (T_alloc = T_max rounded up to 32):
  *   0 Kc key codes           D*k_bits/8 bytes per token
- *   1 Ks f32 key scales      per token: D/k_group per token; per channel: D per 32 tokens
- *   2 Kz f32 key offsets, like Ks; affine keys only (else 0 bytes)
+ *   1 Ks key scales          per token: D/k_group per token; per channel: D per 32 tokens
+ *                            (fp32, or fp16 when meta_fp16; element i at byte 4i or 2i)
+ *   2 Kz key offsets, like Ks; affine keys only (else 0 bytes)
  *   3 Vc value codes         D*v_bits/8 bytes per token
- *   4 Vs f32 value scales    D/v_group per token
- *   5 Vz f32 value offsets, like Vs; affine values only
+ *   4 Vs value scales        D/v_group per token (fp32 or fp16, like Ks)
+ *   5 Vz value offsets, like Vs; affine values only
  *   6 Kr f16 [B][H_kv][residual+flush][D]  fp16 window, slot t mod (R+F)
  *   7 Vr f16, like Kr
  * Sections 0-5 are blocked by 32-token blocks: with u = b*H_kv + h,
@@ -97,9 +103,9 @@ typedef struct kvq_cache kvq_cache;
  *       ((i*2 + e)*64 + r + 16*(P%4)) * (D/32) + P/4
  *   Vc piece (octet o = tau/8, channel d), tokens 8o..8o+7 of channel d,
  *       is at index (i*64 + d%16 + 16*o) * (D/16) + d/16
- *   Ks/Kz per token, group g: float index (i*(D/k_group) + g)*32 + tau;
+ *   Ks/Kz per token, group g: element index (i*(D/k_group) + g)*32 + tau;
  *       per channel (32-token group beta, channel d): i*D + d
- *   Vs/Vz group g: float index (i*(D/v_group) + g)*32 + tau
+ *   Vs/Vz group g: element index (i*(D/v_group) + g)*32 + tau
  * This is the order in which the decode kernel consumes the codes (a
  * 64-lane MFMA operand layout), so attention reads them without any
  * rearrangement; the paper fixes the codes and metadata, not this order. */

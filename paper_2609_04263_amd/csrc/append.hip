@@ -105,6 +105,28 @@ __device__ __forceinline__ void group_stats(const float* x, int stride, int g, i
     }
 }
 
+// fp16 metadata: the scale and offset as stored, i.e. rounded to nearest
+// fp16 (scale clamped to [2^-24, 65504], offset to +-65504); the codes are
+// then computed from these values.
+__device__ __forceinline__ void round_meta(int meta16, float* s, float* z)
+{
+    if (!meta16)
+        return;
+    const float sc = fminf(fmaxf(*s, 0x1p-24f), 65504.0f);
+    const float zc = fminf(fmaxf(*z, -65504.0f), 65504.0f);
+    *s = f16_bits_to_f32(f32_to_f16_bits(sc));
+    *z = f16_bits_to_f32(f32_to_f16_bits(zc)) + 0.0f;
+}
+
+// Scale or offset i of a metadata section: fp32, or fp16 (an exact value).
+__device__ __forceinline__ void store_meta(float* base, size_t i, float v, int meta16)
+{
+    if (meta16)
+        ((uint16_t*)base)[i] = f32_to_f16_bits(v);
+    else
+        base[i] = v;
+}
+
 __device__ __forceinline__ uint32_t code_one(float x, float s, float z, int mode, int bits)
 {
     if (mode == KVQ_AFFINE)
@@ -196,12 +218,13 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
                 continue;
             float s, z;
             group_stats(xs + i * D + gi * p.k_group, 1, p.k_group, p.k_mode, kb, &s, &z);
+            round_meta(p.meta16, &s, &z);
             ms[idx] = s;
             mz[idx] = z;
             size_t mi = (blk * ng + gi) * kBlockTok + i;
-            p.ks[mi] = s;
+            store_meta(p.ks, mi, s, p.meta16);
             if (p.k_mode == KVQ_AFFINE)
-                p.kz[mi] = z;
+                store_meta(p.kz, mi, z, p.meta16);
         }
         __syncthreads();
         for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
@@ -220,12 +243,13 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
         for (int d = threadIdx.x; d < D; d += kThreads) {
             float s, z;
             group_stats(xs + d, D, kBlockTok, p.k_mode, kb, &s, &z);
+            round_meta(p.meta16, &s, &z);
             ms[d] = s;
             mz[d] = z;
             size_t mi = blk * D + d;
-            p.ks[mi] = s;
+            store_meta(p.ks, mi, s, p.meta16);
             if (p.k_mode == KVQ_AFFINE)
-                p.kz[mi] = z;
+                store_meta(p.kz, mi, z, p.meta16);
         }
         __syncthreads();
         for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
@@ -249,12 +273,13 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
             continue;
         float s, z;
         group_stats(xs + i * D + gi * p.v_group, 1, p.v_group, p.v_mode, vb, &s, &z);
+        round_meta(p.meta16, &s, &z);
         ms[idx] = s;
         mz[idx] = z;
         size_t mi = (blk * ng + gi) * kBlockTok + i;
-        p.vs[mi] = s;
+        store_meta(p.vs, mi, s, p.meta16);
         if (p.v_mode == KVQ_AFFINE)
-            p.vz[mi] = z;
+            store_meta(p.vz, mi, z, p.meta16);
     }
     __syncthreads();
     for (int idx = threadIdx.x; idx < (kBlockTok / 8) * D; idx += kThreads) {
@@ -360,12 +385,13 @@ __global__ __launch_bounds__(D) void append_token_kernel(AppendParams p)
                 s = 1e-8f;
             z = 0.0f;
         }
+        round_meta(p.meta16, &s, &z);
         const uint32_t c = code_one(x[w], s, z, mode, bits);
         if (d % g == 0) {
             const size_t mi = (blk * ng + gi) * kBlockTok + tau;
-            (w ? p.vs : p.ks)[mi] = s;
+            store_meta(w ? p.vs : p.ks, mi, s, p.meta16);
             if (mode == KVQ_AFFINE)
-                (w ? p.vz : p.kz)[mi] = z;
+                store_meta(w ? p.vz : p.kz, mi, z, p.meta16);
         }
         if (w == 0) {
             // key piece d / 8: codes of channels 8P .. 8P + 7 at bits k_bits e

@@ -72,10 +72,11 @@ __host__ __device__ constexpr int meta_pairs(int D, int nvg)
 }
 
 // Compile-time shape of one kernel instance.
-template <int D_, int KBITS_, int VBITS_, bool PERCH_, int VGS_>
+template <int D_, int KBITS_, int VBITS_, bool PERCH_, int VGS_, bool M16_ = false>
 struct Cfg {
     static constexpr int D = D_, KBITS = KBITS_, VBITS = VBITS_, VGS = VGS_;
     static constexpr bool PERCH = PERCH_;
+    static constexpr bool M16 = M16_;           // fp16 scales and offsets
     static constexpr int NKB = D / 32;          // 32-channel K-blocks of the score MFMAs
     static constexpr int NMB = D / 16;          // 16-channel M-blocks of the value MFMAs
     static constexpr int KW = NKB * KBITS / 4;  // key code words per lane and half block
@@ -203,8 +204,9 @@ __device__ __forceinline__ void split_pairs(const float* v, half8* hi, half8* lo
 // In the wave's LDS buffer: key scales, key offsets z', value scales, value
 // offsets z' (float4 offsets in coded_block).
 struct MetaMap {
-    const float* ks;     // key scales; the other sections are at float offsets from it
+    const uint8_t* ks;   // key scales; the other sections are at byte offsets from it
     long dkz, dvs, dvz;  // kz - ks (0 for symmetric keys), vs - ks, vz - ks (vs - ks when symmetric)
+    int esz;             // bytes per scale or offset: 4 (fp32) or 2 (fp16, Cfg::M16)
     int nk, nv;          // floats per block
     int kp, np;          // key chunk pairs, all chunk pairs
     float kmul, vmul;    // sm_scale log2(e) for keys, 2^-kTau for value scales
@@ -235,10 +237,18 @@ __device__ __forceinline__ void load_block(BlockRegs<C>& r, const AttnParams& p,
         const int c = min(lane + 64 * u, mm.np - 1);
         const bool key = c < mm.kp;
         // one base pointer and selected offsets keep the loads global ones
-        const long s_off = key ? (long)ub * mm.nk + 4 * c : mm.dvs + (long)ub * mm.nv + 4 * (c - mm.kp);
+        const long s_off = (key ? (long)ub * mm.nk + 4 * c : (long)ub * mm.nv + 4 * (c - mm.kp)) * mm.esz +
+                           (key ? 0 : mm.dvs);
         const long z_off = s_off + (key ? mm.dkz : mm.dvz - mm.dvs);
-        r.ms[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + s_off));
-        r.mz[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + z_off));
+        if constexpr (!C::M16) {
+            r.ms[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + s_off));
+            r.mz[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + z_off));
+        } else {  // four fp16 values, widened when staged
+            const u32x2 s2 = __builtin_nontemporal_load((const u32x2*)(mm.ks + s_off));
+            const u32x2 z2 = __builtin_nontemporal_load((const u32x2*)(mm.ks + z_off));
+            r.ms[u] = u32x4{s2.x, s2.y, 0u, 0u};
+            r.mz[u] = u32x4{z2.x, z2.y, 0u, 0u};
+        }
     }
 }
 
@@ -358,10 +368,26 @@ struct Split {
                 const float fs = key ? mm.kmul : mm.vmul;
                 const float z0 = key ? mm.kz0 : mm.vz0, zs = key ? mm.kzs : mm.vzs;
                 const u32x4 s = r.ms[u], z = r.mz[u];
-                const float sv[4] = {__uint_as_float(s.x), __uint_as_float(s.y), __uint_as_float(s.z),
-                                     __uint_as_float(s.w)};
-                const float zv[4] = {__uint_as_float(z.x), __uint_as_float(z.y), __uint_as_float(z.z),
-                                     __uint_as_float(z.w)};
+                float sv[4], zv[4];
+                if constexpr (!C::M16) {
+                    sv[0] = __uint_as_float(s.x);
+                    sv[1] = __uint_as_float(s.y);
+                    sv[2] = __uint_as_float(s.z);
+                    sv[3] = __uint_as_float(s.w);
+                    zv[0] = __uint_as_float(z.x);
+                    zv[1] = __uint_as_float(z.y);
+                    zv[2] = __uint_as_float(z.z);
+                    zv[3] = __uint_as_float(z.w);
+                } else {
+                    sv[0] = f16_bits_to_f32((uint16_t)s.x);
+                    sv[1] = f16_bits_to_f32((uint16_t)(s.x >> 16));
+                    sv[2] = f16_bits_to_f32((uint16_t)s.y);
+                    sv[3] = f16_bits_to_f32((uint16_t)(s.y >> 16));
+                    zv[0] = f16_bits_to_f32((uint16_t)z.x);
+                    zv[1] = f16_bits_to_f32((uint16_t)(z.x >> 16));
+                    zv[2] = f16_bits_to_f32((uint16_t)z.y);
+                    zv[3] = f16_bits_to_f32((uint16_t)(z.y >> 16));
+                }
                 const int ds = key ? c : 2 * mm.kp + (c - mm.kp);
                 const int dz = key ? mm.kp + c : 2 * mm.kp + vp + (c - mm.kp);
                 wl[ds] = float4{sv[0] * fs, sv[1] * fs, sv[2] * fs, sv[3] * fs};
@@ -589,10 +615,11 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     const bool active = rep ? vg < C::NVG : hh < G;
 
     MetaMap mm;
-    mm.ks = p.ks;
-    mm.dkz = kaff ? p.kz - p.ks : 0;
-    mm.dvs = p.vs - p.ks;
-    mm.dvz = vaff ? p.vz - p.ks : mm.dvs;
+    mm.ks = (const uint8_t*)p.ks;
+    mm.dkz = kaff ? (const uint8_t*)p.kz - (const uint8_t*)p.ks : 0;
+    mm.dvs = (const uint8_t*)p.vs - (const uint8_t*)p.ks;
+    mm.dvz = vaff ? (const uint8_t*)p.vz - (const uint8_t*)p.ks : mm.dvs;
+    mm.esz = p.meta16 ? 2 : 4;
     mm.nk = kmeta;
     mm.nv = vmeta;
     mm.kp = kmeta / 4;
@@ -889,29 +916,35 @@ hipError_t launch_split(const AttnParams& p, hipStream_t stream)
 }
 
 // Calls F<Cfg<...>>::run(p, args...) for the instance that serves p.
-template <template <class> class F, int D, int KB, int VB, bool PC, int VGS = 0, class... A>
+template <template <class> class F, int D, int KB, int VB, bool PC, bool M16, int VGS = 0, class... A>
 auto by_groups(const AttnParams& p, A... args)
 {
     if constexpr ((32 << VGS) >= D) {
-        return F<Cfg<D, KB, VB, PC, VGS>>::run(p, args...);
+        return F<Cfg<D, KB, VB, PC, VGS, M16>>::run(p, args...);
     } else {
         if (p.v_group == (32 << VGS))
-            return F<Cfg<D, KB, VB, PC, VGS>>::run(p, args...);
-        return by_groups<F, D, KB, VB, PC, VGS + 1>(p, args...);
+            return F<Cfg<D, KB, VB, PC, VGS, M16>>::run(p, args...);
+        return by_groups<F, D, KB, VB, PC, M16, VGS + 1>(p, args...);
     }
+}
+
+template <template <class> class F, int D, bool M16, class... A>
+auto by_bits(const AttnParams& p, A... args)
+{
+    const bool pc = p.k_axis == KVQ_PER_CHANNEL;
+    if (p.k_bits == 4 && p.v_bits == 4)
+        return pc ? by_groups<F, D, 4, 4, true, M16>(p, args...) : by_groups<F, D, 4, 4, false, M16>(p, args...);
+    if (p.k_bits == 4 && p.v_bits == 2)
+        return pc ? by_groups<F, D, 4, 2, true, M16>(p, args...) : by_groups<F, D, 4, 2, false, M16>(p, args...);
+    if (p.k_bits == 2 && p.v_bits == 4)
+        return pc ? by_groups<F, D, 2, 4, true, M16>(p, args...) : by_groups<F, D, 2, 4, false, M16>(p, args...);
+    return pc ? by_groups<F, D, 2, 2, true, M16>(p, args...) : by_groups<F, D, 2, 2, false, M16>(p, args...);
 }
 
 template <template <class> class F, int D, class... A>
 auto by_format(const AttnParams& p, A... args)
 {
-    const bool pc = p.k_axis == KVQ_PER_CHANNEL;
-    if (p.k_bits == 4 && p.v_bits == 4)
-        return pc ? by_groups<F, D, 4, 4, true>(p, args...) : by_groups<F, D, 4, 4, false>(p, args...);
-    if (p.k_bits == 4 && p.v_bits == 2)
-        return pc ? by_groups<F, D, 4, 2, true>(p, args...) : by_groups<F, D, 4, 2, false>(p, args...);
-    if (p.k_bits == 2 && p.v_bits == 4)
-        return pc ? by_groups<F, D, 2, 4, true>(p, args...) : by_groups<F, D, 2, 4, false>(p, args...);
-    return pc ? by_groups<F, D, 2, 2, true>(p, args...) : by_groups<F, D, 2, 2, false>(p, args...);
+    return p.meta16 ? by_bits<F, D, true>(p, args...) : by_bits<F, D, false>(p, args...);
 }
 
 template <class C>

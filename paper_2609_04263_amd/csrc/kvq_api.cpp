@@ -36,6 +36,8 @@ kvq_status check_format(const kvq_format* f, int D)
         return KVQ_ERR_FORMAT;
     if (!pow2_in(f->v_group, 32, D))
         return KVQ_ERR_FORMAT;
+    if (f->meta_fp16 != 0 && f->meta_fp16 != 1)
+        return KVQ_ERR_FORMAT;
     return KVQ_OK;
 }
 
@@ -54,10 +56,11 @@ kvq_status layout(const kvq_format* f, int B, int H, int D, int T_max, size_t of
     const size_t bh = (size_t)B * H, T = round_up((size_t)T_max, 32);
     const size_t ring = (size_t)(f->residual + f->flush);
     len[0] = bh * T * (size_t)(D * f->k_bits / 32) * 4;
-    len[1] = f->k_axis == KVQ_PER_TOKEN ? bh * T * (size_t)(D / f->k_group) * 4 : bh * (T / 32) * (size_t)D * 4;
+    const size_t msz = f->meta_fp16 ? 2 : 4;  // bytes per scale or offset
+    len[1] = f->k_axis == KVQ_PER_TOKEN ? bh * T * (size_t)(D / f->k_group) * msz : bh * (T / 32) * (size_t)D * msz;
     len[2] = f->k_mode == KVQ_AFFINE ? len[1] : 0;
     len[3] = bh * (T * f->v_bits / 32) * (size_t)D * 4;
-    len[4] = bh * T * (size_t)(D / f->v_group) * 4;
+    len[4] = bh * T * (size_t)(D / f->v_group) * msz;
     len[5] = f->v_mode == KVQ_AFFINE ? len[4] : 0;
     len[6] = f->flush ? bh * ring * (size_t)D * 2 : 0;
     len[7] = len[6];
@@ -370,6 +373,7 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int n_new, con
     p.v_group = f.v_group;
     p.rotate = f.rotate;
     p.rot_c = rotation_constant(c->D);
+    p.meta16 = f.meta_fp16;
     if (kvq::launch_append(p, c->D, (hipStream_t)stream) != hipSuccess)
         return KVQ_ERR_DEVICE;
     c->n = n1;
@@ -430,6 +434,7 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.rotate = f.rotate;
     p.sm_log2 = sm_scale * 1.4426950408889634f;
     p.rot_c = rotation_constant(c->D);
+    p.meta16 = f.meta_fp16;
     p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.G);
     kvq::decode_plan(c->B, c->H, kvq::decode_target_groups(p, c->D), p.nq, &p.S_q, &p.bps);
     p.S_tot = p.S_q + (f.flush ? 1 : 0);
@@ -473,6 +478,7 @@ kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, f
     p.rotate = f.rotate;
     p.sm_log2 = sm_scale * 1.4426950408889634f;
     p.rot_c = rotation_constant(c->D);
+    p.meta16 = f.meta_fp16;
     return kvq::launch_prefill(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 

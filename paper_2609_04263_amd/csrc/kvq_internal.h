@@ -43,6 +43,7 @@ struct AppendParams {
     int k_bits, v_bits, k_mode, v_mode, k_axis, k_group, v_group;
     int rotate;           // 0 or D
     float rot_c;          // binary32 value nearest D^(-1/2)
+    int meta16;           // scales and offsets stored as fp16 (ks..vz then point at halves)
 };
 hipError_t launch_append(const AppendParams& p, int D, hipStream_t stream);
 
@@ -102,6 +103,7 @@ struct AttnParams {
     float rot_c;
     size_t lds_bytes;     // dynamic LDS of the split kernel
     int C;                // chunked prefill: query tokens (the newest C of the cache); q is [B][C][H_q][D]
+    int meta16;           // scales and offsets stored as fp16 (ks..vz then point at halves)
 };
 // Workgroups of the split kernel that fit the device at once (all fields of p
 // that select the kernel instance and its LDS must be set).

@@ -75,6 +75,31 @@ __device__ __forceinline__ float dq(int mode, int bits, uint32_t c, float s, flo
     return mode == KVQ_AFFINE ? (float)c * s + z : ((float)c - (float)(1 << (bits - 1))) * s;
 }
 
+// scale or offset i of a raw metadata range (fp32, or fp16 with meta16)
+__device__ __forceinline__ float meta(const uint8_t* sec, int i, bool m16)
+{
+    return m16 ? f16_bits_to_f32(((const uint16_t*)sec)[i]) : ((const float*)sec)[i];
+}
+
+// eight consecutive scales or offsets from element i (a multiple of 8)
+__device__ __forceinline__ void meta8(const uint8_t* sec, int i, bool m16, float* v)
+{
+    if (m16) {
+        const u32x4 h = *(const u32x4*)(sec + 2 * i);
+        const uint32_t w[4] = {h.x, h.y, h.z, h.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            v[e] = f16_bits_to_f32((uint16_t)(w[e >> 1] >> (16 * (e & 1))));
+    } else {
+        const floatx4 a = *(const floatx4*)(sec + 4 * i), b = *(const floatx4*)(sec + 4 * i + 16);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[e] = a[e];
+            v[e + 4] = b[e];
+        }
+    }
+}
+
 // eight codes of piece idx of a raw code range (4-bit: one u32; 2-bit: one u16)
 __device__ __forceinline__ uint32_t piece(const uint8_t* sec, int idx, int bits)
 {
@@ -201,8 +226,9 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
     // Byte ranges of one block's raw data, in the order they sit in LDS: Kc,
     // Ks, Kz, Vc, Vs, Vz (Kz, Vz empty for symmetric codes).  Kept in scalars
     // (selects, no indexed arrays) so nothing lands in scratch memory.
-    const int kmeta = p.k_axis == KVQ_PER_TOKEN ? (D / p.k_group) * 32 * 4 : D * 4;
-    const int vmeta = (D / p.v_group) * 32 * 4;
+    const int msz = p.meta16 ? 2 : 4;  // bytes per scale or offset
+    const int kmeta = p.k_axis == KVQ_PER_TOKEN ? (D / p.k_group) * 32 * msz : D * msz;
+    const int vmeta = (D / p.v_group) * 32 * msz;
     const int len0 = 4 * D * kbits, len1 = kmeta, len2 = kaff ? kmeta : 0;
     const int len3 = 4 * D * vbits, len4 = vmeta, len5 = vaff ? vmeta : 0;
     const int st1 = len0, st2 = st1 + len1, st3 = st2 + len2, st4 = st3 + len3, st5 = st4 + len4;
@@ -243,11 +269,12 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
         }
     };
     const uint8_t* rkc = raw;
-    const float* rks = (const float*)(raw + st1);
-    const float* rkz = (const float*)(raw + st2);
+    const uint8_t* rks = raw + st1;
+    const uint8_t* rkz = raw + st2;
     const uint8_t* rvc = raw + st3;
-    const float* rvs = (const float*)(raw + st4);
-    const float* rvz = (const float*)(raw + st5);
+    const uint8_t* rvs = raw + st4;
+    const uint8_t* rvz = raw + st5;
+    const bool m16 = p.meta16 != 0;
 
     fetch_raw(0);
     store_raw();
@@ -269,7 +296,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
                     const uint32_t mask = (1u << kbits) - 1u;
                     if (p.k_axis == KVQ_PER_TOKEN) {
                         const int mi = ((8 * P) / p.k_group) * 32 + tau;
-                        const float sc = rks[mi], z = kaff ? rkz[mi] : 0.0f;
+                        const float sc = meta(rks, mi, m16), z = kaff ? meta(rkz, mi, m16) : 0.0f;
 #pragma unroll
                         for (int e = 0; e < 8; ++e)
                             v[e] = dq(p.k_mode, kbits, (w >> (kbits * e)) & mask, sc, z);
@@ -277,7 +304,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
 #pragma unroll
                         for (int e = 0; e < 8; ++e) {
                             const int mi = 8 * P + e;
-                            v[e] = dq(p.k_mode, kbits, (w >> (kbits * e)) & mask, rks[mi], kaff ? rkz[mi] : 0.0f);
+                            v[e] = dq(p.k_mode, kbits, (w >> (kbits * e)) & mask, meta(rks, mi, m16),
+                                      kaff ? meta(rkz, mi, m16) : 0.0f);
                         }
                     }
                 } else {
@@ -295,17 +323,15 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
                 const int idx = (d % 16 + 16 * o) * (D / 16) + d / 16;
                 const uint32_t w = t0 < p.nq ? piece(rvc, idx, vbits) : 0u;
                 const uint32_t mask = (1u << vbits) - 1u;
-                // the octet's eight scales (and offsets) are consecutive floats
+                // the octet's eight scales (and offsets) are consecutive
                 const int mi = (d / p.v_group) * 32 + 8 * o;
-                const floatx4 s0 = *(const floatx4*)(rvs + mi), s1 = *(const floatx4*)(rvs + mi + 4);
-                floatx4 z0 = {0.f, 0.f, 0.f, 0.f}, z1 = z0;
-                if (vaff) {
-                    z0 = *(const floatx4*)(rvz + mi);
-                    z1 = *(const floatx4*)(rvz + mi + 4);
-                }
+                float sv[8], zv[8];
+                meta8(rvs, mi, m16, sv);
+                if (vaff)
+                    meta8(rvz, mi, m16, zv);
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const float sc = e < 4 ? s0[e] : s1[e - 4], z = e < 4 ? z0[e] : z1[e - 4];
+                    const float sc = sv[e], z = vaff ? zv[e] : 0.0f;
                     v[e] = t0 + e < p.nq ? dq(p.v_mode, vbits, (w >> (vbits * e)) & mask, sc, z) : 0.0f;
                 }
                 *(u32x4*)(vh + d * VP + 8 * o) = __builtin_bit_cast(u32x4, pack_half8(v));

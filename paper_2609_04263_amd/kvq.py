@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvq.so")
 
 FORMAT_FIELDS = ("k_bits", "v_bits", "k_mode", "v_mode", "k_axis", "v_axis",
-                 "k_group", "v_group", "residual", "flush", "rotate")
+                 "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16")
 
 OK, ERR_ARG, ERR_FORMAT, ERR_CAPACITY, ERR_WORKSPACE, ERR_DEVICE = range(6)
 
@@ -35,7 +35,7 @@ class Format(C.Structure):
     def of(cls, fmt) -> "Format":
         if isinstance(fmt, Format):
             return fmt
-        return cls(*[int(fmt[name]) for name in FORMAT_FIELDS])
+        return cls(*[int(fmt.get(name, 0)) for name in FORMAT_FIELDS])
 
 
 def _load() -> C.CDLL:

@@ -32,6 +32,10 @@ CASES = {
     "had_affine_window": (configs.make_format(4, 4, k_group=64, v_group=64, residual=32, flush=32,
                                               rotate=256), 256),
     "g256": (configs.make_format(4, 4, k_group=256, v_group=256), 256),
+    # fp16 scales and offsets, as the paper stores them
+    "tiny_meta16": (dict(configs.WORKLOADS["tiny_b16"].fmt, meta_fp16=1), 64),
+    "kivi_meta16": (dict(configs.WORKLOADS["llama8b_kivi"].fmt, meta_fp16=1), 128),
+    "hadamard_meta16": (dict(configs.WORKLOADS["llama8b_had"].fmt, meta_fp16=1), 128),
 }
 
 

@@ -42,6 +42,7 @@ FORMATS = [wl.fmt for wl in configs.WORKLOADS.values()] + [
     configs.make_format(2, 4, k_mode=1, k_group=32, v_group=128),
     configs.make_format(4, 2, k_axis=1, k_group=32, v_group=64, residual=64, flush=64),
     configs.make_format(4, 4, k_group=256, v_group=256),
+    configs.make_format(2, 4, k_axis=1, k_group=32, v_group=64, residual=128, flush=32, meta_fp16=1),
 ]
 
 
