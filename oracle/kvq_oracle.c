@@ -38,8 +38,9 @@
  * tau = t % 32 of block beta = t / 32.
  *
  * Codes are stored in pieces of eight codes, code j of a piece at bits
- * [bits*j, bits*j + bits) (a piece is a u32 for 4-bit codes, a u16 for
- * 2-bit codes; piece i of a section starts at byte i * bits).  The pieces of
+ * [bits*j, bits*j + bits) (a piece is a u64 for 8-bit codes, a u32 for
+ * 4-bit codes, a u16 for 2-bit codes; piece i of a section starts at byte
+ * i * bits).  The pieces of
  * a block are ordered for the consumer, a 64-lane MFMA layout: token tau has
  * row r = 4*(tau/8) + tau%4 in half e = (tau/4)%2 of its block.
  *   Kc  piece (t, P) = channels 8P..8P+7 of token t, P < D/8, at index
@@ -369,7 +370,7 @@ int orc_check_format(const orc_format* f, int D)
         return ORC_ERR_ARG;
     if (D != 64 && D != 128 && D != 256)
         return ORC_ERR_FORMAT;
-    if ((f->k_bits != 2 && f->k_bits != 4) || (f->v_bits != 2 && f->v_bits != 4))
+    if ((f->k_bits != 2 && f->k_bits != 4 && f->k_bits != 8) || (f->v_bits != 2 && f->v_bits != 4 && f->v_bits != 8))
         return ORC_ERR_FORMAT;
     if ((f->k_mode != 0 && f->k_mode != 1) || (f->v_mode != 0 && f->v_mode != 1))
         return ORC_ERR_FORMAT;
@@ -494,34 +495,25 @@ static uint8_t* vc_piece(const image_view* v, int b, int h, int t, int d)
     return v->img + v->off[3] + i * (size_t)v->f->v_bits;
 }
 
-/* A piece holds eight codes of `bits` bits: 32 bits for 4-bit codes, 16 for 2-bit. */
-static uint32_t piece_get(const uint8_t* p, int bits)
+/* A piece holds eight codes of `bits` bits: 64 bits for 8-bit codes, 32 for
+ * 4-bit, 16 for 2-bit (little-endian, code j at bits [bits*j, +bits)). */
+static uint64_t piece_get(const uint8_t* p, int bits)
 {
-    if (bits == 4) {
-        uint32_t w;
-        memcpy(&w, p, 4);
-        return w;
-    }
-    uint16_t hw;
-    memcpy(&hw, p, 2);
-    return hw;
+    uint64_t w = 0;
+    memcpy(&w, p, (size_t)bits);
+    return w;
 }
 
-static void piece_put(uint8_t* p, int bits, uint32_t val)
+static void piece_put(uint8_t* p, int bits, uint64_t val)
 {
-    if (bits == 4) {
-        memcpy(p, &val, 4);
-    } else {
-        uint16_t hw = (uint16_t)val;
-        memcpy(p, &hw, 2);
-    }
+    memcpy(p, &val, (size_t)bits);
 }
 
-static uint32_t pack8(const uint8_t* codes, int bits)
+static uint64_t pack8(const uint8_t* codes, int bits)
 {
-    uint32_t w = 0;
+    uint64_t w = 0;
     for (int j = 0; j < 8; ++j)
-        w |= (uint32_t)codes[j] << (bits * j);
+        w |= (uint64_t)codes[j] << (bits * j);
     return w;
 }
 
@@ -709,10 +701,10 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                         meta_put(&v, 5, mi, z);
                 }
                 int j = t % 8;
-                uint32_t keep = j == 0 ? 0u : ((1u << (vb * j)) - 1u);
+                uint64_t keep = j == 0 ? 0u : ((1ull << (vb * j)) - 1u);
                 for (int d = 0; d < D; ++d) {
                     uint8_t* pc = vc_piece(&v, b, h, t, d);
-                    piece_put(pc, vb, (piece_get(pc, vb) & keep) | ((uint32_t)codes[d] << (vb * j)));
+                    piece_put(pc, vb, (piece_get(pc, vb) & keep) | ((uint64_t)codes[d] << (vb * j)));
                 }
             }
             /* fp16 residual ring: slot t mod (R + F) holds the newest token
@@ -760,12 +752,12 @@ static void reconstruct_bh(const image_view* v, int b, int h, int n, double* kha
         for (int d = 0; d < D; ++d) {
             double kv, vv;
             if (t < nq) {
-                uint32_t kw = piece_get(kc_piece(v, b, h, t, d / 8), kb);
-                uint32_t kc = (kw >> (kb * (d % 8))) & ((1u << kb) - 1u);
+                uint64_t kw = piece_get(kc_piece(v, b, h, t, d / 8), kb);
+                uint32_t kc = (uint32_t)(kw >> (kb * (d % 8))) & ((1u << kb) - 1u);
                 size_t km = kmeta_index(v, b, h, t, d);
                 kv = dequant_code(f->k_mode, kb, kc, meta_get(v, 1, km), f->k_mode == 0 ? meta_get(v, 2, km) : 0.0f);
-                uint32_t vw = piece_get(vc_piece(v, b, h, t, d), vb);
-                uint32_t vc = (vw >> (vb * (t % 8))) & ((1u << vb) - 1u);
+                uint64_t vw = piece_get(vc_piece(v, b, h, t, d), vb);
+                uint32_t vc = (uint32_t)(vw >> (vb * (t % 8))) & ((1u << vb) - 1u);
                 size_t vm = vmeta_index(v, b, h, t, d);
                 vv = dequant_code(f->v_mode, vb, vc, meta_get(v, 4, vm), f->v_mode == 0 ? meta_get(v, 5, vm) : 0.0f);
             } else {

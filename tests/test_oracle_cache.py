@@ -26,6 +26,7 @@ FMTS = {
     "sym4_window": configs.make_format(4, 4, k_mode=1, v_mode=1, k_group=32, v_group=64,
                                        residual=32, flush=32),
     "affine4_g64_meta16": configs.make_format(4, 4, k_group=64, v_group=64, meta_fp16=1),
+    "affine8_g64": configs.make_format(8, 8, k_group=64, v_group=64),
     "kivi_meta16": dict(configs.WORKLOADS["llama8b_kivi"].fmt, meta_fp16=1),
 }
 
@@ -39,8 +40,8 @@ def floats(img, off, count):
 
 
 def pieces(img, off, ln, bits):
-    """Section as an array of eight-code pieces (u32 for 4-bit, u16 for 2-bit)."""
-    dt = np.uint32 if bits == 4 else np.uint16
+    """Section as an array of eight-code pieces (u64 for 8-bit, u32 for 4-bit, u16 for 2-bit)."""
+    dt = {8: np.uint64, 4: np.uint32, 2: np.uint16}[bits]
     return np.frombuffer(img[off:off + ln].tobytes(), dtype=dt)
 
 
@@ -96,6 +97,28 @@ def test_per_token_affine_slots_decode_by_hand():
         for h in range(H):
             for d in range(D):
                 assert vc[vc_index(b, h, 36, d, H, NB, D)] >> (4 * (37 % 8)) == 0
+
+
+def test_eight_bit_pieces_decode_by_hand():
+    f = FMTS["affine8_g64"]
+    B, H, D, T = 1, 2, 64, 64
+    K, V = synth.kv_tokens(15, B, 45, H, D)
+    c = oracle.Cache(f, B, H, D, T)
+    c.append(K, V)
+    off, ln, _ = oracle.layout(f, B, H, D, T)
+    assert ln[0] == B * H * T * D and ln[3] == B * H * T * D   # one byte per code
+    NB = 2
+    kc = pieces(c.image, off[0], ln[0], 8)
+    vc = pieces(c.image, off[3], ln[3], 8)
+    for h in range(H):
+        for t in (0, 13, 31, 32, 44):
+            codes, _, _ = oracle.quant_affine(f32(K[0, t, h]), 8)
+            vcodes, _, _ = oracle.quant_affine(f32(V[0, t, h]), 8)
+            for P in range(D // 8):
+                piece = int(kc[kc_index(0, h, t, P, H, NB, D)])
+                assert [(piece >> (8 * j)) & 255 for j in range(8)] == list(codes[8 * P:8 * P + 8])
+            for d in range(D):
+                assert (int(vc[vc_index(0, h, t, d, H, NB, D)]) >> (8 * (t % 8))) & 255 == vcodes[d]
 
 
 def test_two_bit_pieces_decode_by_hand():

@@ -24,7 +24,7 @@ def test_pack_byte_images():
     assert oracle.pack_word([0] * 15 + [3], 2) == 0xC0000000
 
 
-@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("bits", [2, 4, 8])
 def test_pack_round_trip_every_value_at_every_position(bits):
     n = 32 // bits
     for pos, val in itertools.product(range(n), range(2 ** bits)):

@@ -58,7 +58,7 @@ def test_affine_signed_zero_offset_is_positive_zero():
     assert np.float32(z).view(np.uint32) == 0
 
 
-@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("bits", [2, 4, 8])
 @pytest.mark.parametrize("g", [32, 64, 128])
 def test_affine_properties_on_random_groups(bits, g):
     rng = np.random.default_rng(bits * 1000 + g)
@@ -123,7 +123,7 @@ def test_symmetric_zero_group():
     assert np.all(codes == 8)
 
 
-@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("bits", [2, 4, 8])
 @pytest.mark.parametrize("g", [32, 128])
 def test_symmetric_properties_on_random_groups(bits, g):
     rng = np.random.default_rng(50 + bits + g)
