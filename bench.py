@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--meta-fp16", action="store_true",
                     help="store scales and offsets as fp16 (the paper's storage) instead of the workload's fp32")
+    ap.add_argument("--bits8", action="store_true",
+                    help="8-bit key and value codes (the 8-bit ablation) in the workload's groups and modes")
     ap.add_argument("--cpu-sample-steps", type=int, default=None)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the timed region, copy a buffer of this many MiB once (a kernel of known "
@@ -108,6 +110,9 @@ def main():
     if args.meta_fp16:
         import dataclasses
         wl = dataclasses.replace(wl, name=wl.name + "+meta16", fmt=dict(wl.fmt, meta_fp16=1))
+    if args.bits8:
+        import dataclasses
+        wl = dataclasses.replace(wl, name=wl.name + "+k8v8", fmt=dict(wl.fmt, k_bits=8, v_bits=8))
     B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
 
     def bf16(bits):

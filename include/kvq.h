@@ -44,7 +44,8 @@ enum { KVQ_AFFINE = 0, KVQ_SYMMETRIC = 1 };
 enum { KVQ_PER_TOKEN = 0, KVQ_PER_CHANNEL = 1 };
 
 /* Cache format (Sec. 3.1).
- *   *_bits   2 or 4: code width.
+ *   *_bits   2, 4 or 8: code width (8 only as k_bits = v_bits = 8, the
+ *            8-bit ablation of Sec. 4 and Sec. 5.4).
  *   *_mode   KVQ_AFFINE: Eq. (3), s = max((max-min)/(2^b-1), 1e-8),
  *            c = clip(round_half_even((x-min)/s), 0, 2^b-1), offset = min.
  *            KVQ_SYMMETRIC (the symmetric control, "max-magnitude scale, no
@@ -96,7 +97,7 @@ typedef struct kvq_cache kvq_cache;
  * NB = T_alloc/32, token t at position tau = t%32 of block beta = t/32, and
  * i = u*NB + beta:
  *   Codes come in pieces of eight codes (code j at bits [bits*j, +bits); a
- *   piece is 32 bits for 4-bit codes, 16 bits for 2-bit codes; piece index
+ *   piece is 64 bits for 8-bit codes, 32 for 4-bit, 16 for 2-bit; piece index
  *   x starts at byte x*bits of its section).  Token tau has row
  *   r = 4*(tau/8) + tau%4 and half e = (tau/4)%2 of its block.
  *   Kc piece (t, P), channels 8P..8P+7 of token t, is at index

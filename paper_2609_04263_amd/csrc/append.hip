@@ -48,17 +48,28 @@ __device__ __forceinline__ size_t value_piece(size_t blk, int o, int d)
     return (blk * 64 + (d & 15) + 16 * o) * (D / 16) + (d >> 4);
 }
 
-__device__ __forceinline__ void store_piece(void* base, size_t i, int bits, uint32_t v)
+// A piece holds eight codes of `bits` bits: 16, 32 or 64 bits wide.
+__device__ __forceinline__ void store_piece(void* base, size_t i, int bits, uint64_t v)
 {
-    if (bits == 4)
-        ((uint32_t*)base)[i] = v;
+    if (bits == 8)
+        ((uint64_t*)base)[i] = v;
+    else if (bits == 4)
+        ((uint32_t*)base)[i] = (uint32_t)v;
     else
         ((uint16_t*)base)[i] = (uint16_t)v;
 }
 
-__device__ __forceinline__ uint32_t load_piece(const void* base, size_t i, int bits)
+__device__ __forceinline__ uint64_t load_piece(const void* base, size_t i, int bits)
 {
+    if (bits == 8)
+        return ((const uint64_t*)base)[i];
     return bits == 4 ? ((const uint32_t*)base)[i] : ((const uint16_t*)base)[i];
+}
+
+// Mask of the low `n` codes of a piece (n < 8).
+__device__ __forceinline__ uint64_t low_codes(int bits, int n)
+{
+    return (1ull << (bits * n)) - 1ull;
 }
 
 __device__ __forceinline__ uint32_t code_affine(float x, float mn, float s, float top)
@@ -233,9 +244,9 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
                 continue;
             int gi = (8 * P) / p.k_group;
             float s = ms[i * ng + gi], z = mz[i * ng + gi];
-            uint32_t word = 0;
+            uint64_t word = 0;
             for (int e = 0; e < 8; ++e)
-                word |= code_one(xs[i * D + 8 * P + e], s, z, p.k_mode, kb) << (kb * e);
+                word |= (uint64_t)code_one(xs[i * D + 8 * P + e], s, z, p.k_mode, kb) << (kb * e);
             store_piece(p.kc, key_piece<D>(blk, i, P), kb, word);
         }
     } else {
@@ -254,10 +265,10 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
         __syncthreads();
         for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
             int i = idx / PPT, P = idx % PPT;
-            uint32_t word = 0;
+            uint64_t word = 0;
             for (int e = 0; e < 8; ++e) {
                 int d = 8 * P + e;
-                word |= code_one(xs[i * D + d], ms[d], mz[d], p.k_mode, kb) << (kb * e);
+                word |= (uint64_t)code_one(xs[i * D + d], ms[d], mz[d], p.k_mode, kb) << (kb * e);
             }
             store_piece(p.kc, key_piece<D>(blk, i, P), kb, word);
         }
@@ -288,10 +299,10 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
         if (tfirst + 8 <= lo || tfirst >= hi)
             continue;
         const size_t pi = value_piece<D>(blk, o, d);
-        uint32_t word = 0;
+        uint64_t word = 0;
         if (tfirst < lo) {  // keep the bits of tokens appended earlier
             int keep_n = lo - tfirst;
-            word = load_piece(p.vc, pi, vb) & ((1u << (vb * keep_n)) - 1u);
+            word = load_piece(p.vc, pi, vb) & low_codes(vb, keep_n);
         }
         int gi = d / p.v_group;
         for (int e = 0; e < 8; ++e) {
@@ -299,7 +310,8 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
             if (t < lo || t >= hi)
                 continue;
             int i = t - tb;
-            word |= code_one(xs[i * D + d], ms[i * ng + gi], mz[i * ng + gi], p.v_mode, vb) << (vb * e);
+            word |= (uint64_t)code_one(xs[i * D + d], ms[i * ng + gi], mz[i * ng + gi], p.v_mode, vb)
+                    << (vb * e);
         }
         store_piece(p.vc, pi, vb, word);
     }
@@ -346,7 +358,7 @@ __global__ __launch_bounds__(D) void append_token_kernel(AppendParams p)
     const size_t vpi = value_piece<D>(blk, tau >> 3, d);
     const size_t in = ((size_t)b * p.H + h) * D + d;  // n_new == 1
     float x[2] = {bf16_to_f32(p.kin[in]), bf16_to_f32(p.vin[in])};
-    const uint32_t old = load_piece(p.vc, vpi, p.v_bits);
+    const uint64_t old = load_piece(p.vc, vpi, p.v_bits);
     if (p.rotate) {
         xs[0][d] = x[0];
         xs[1][d] = x[1];
@@ -394,16 +406,20 @@ __global__ __launch_bounds__(D) void append_token_kernel(AppendParams p)
                 store_meta(w ? p.vz : p.kz, mi, z, p.meta16);
         }
         if (w == 0) {
-            // key piece d / 8: codes of channels 8P .. 8P + 7 at bits k_bits e
-            uint32_t piece = c << (bits * (d & 7));
-            piece |= __shfl_xor(piece, 1);
-            piece |= __shfl_xor(piece, 2);
-            piece |= __shfl_xor(piece, 4);
+            // key piece d / 8: codes of channels 8P .. 8P + 7 at bits k_bits e,
+            // OR-reduced as two 32-bit halves
+            const uint64_t mine = (uint64_t)c << (bits * (d & 7));
+            uint32_t lo32 = (uint32_t)mine, hi32 = (uint32_t)(mine >> 32);
+#pragma unroll
+            for (int off = 1; off < 8; off <<= 1) {
+                lo32 |= __shfl_xor(lo32, off);
+                hi32 |= __shfl_xor(hi32, off);
+            }
             if ((d & 7) == 0)
-                store_piece(p.kc, key_piece<D>(blk, tau, d >> 3), bits, piece);
+                store_piece(p.kc, key_piece<D>(blk, tau, d >> 3), bits, ((uint64_t)hi32 << 32) | lo32);
         } else {
-            const uint32_t keep = j == 0 ? 0u : ((1u << (bits * j)) - 1u);
-            store_piece(p.vc, vpi, bits, (old & keep) | (c << (bits * j)));
+            const uint64_t keep = low_codes(bits, j);
+            store_piece(p.vc, vpi, bits, (old & keep) | ((uint64_t)c << (bits * j)));
         }
     }
 }

@@ -131,12 +131,17 @@ __device__ __forceinline__ void gload_words(const uint32_t* p, uint32_t* w)
 
 // ------------------------------------------------------------ code operands
 
-// Operand bias B0 of a code width: A = B0 + c exactly in binary16.
+// Operand bias B0 of a code width: A = B0 + c exactly in binary16.  The
+// operand's rounding error on the other MFMA side (q, or p s) is multiplied
+// by A and cancels only against the exact offset term, so |A| is kept small:
+// 8-bit codes are centred (c - 128) rather than biased by 1024.
 template <int BITS>
 __device__ constexpr float code_bias()
 {
-    return BITS == 4 ? 16.0f : 4.0f;
+    return BITS == 8 ? -128.0f : BITS == 4 ? 16.0f : 4.0f;
 }
+
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 // Bit constants of the conversion, kept in registers (a VOP3 operation
 // cannot take two literals on gfx950).
@@ -147,10 +152,12 @@ struct CodeBits {
 template <int BITS>
 __device__ __forceinline__ CodeBits code_bits()
 {
+    // 8-bit: code at mantissa bits 0..7 under exponent 2^10 (1024 + c),
+    //        then -1152 added as a packed pair (mask holds binary16 -1152);
     // 4-bit: code at mantissa bits 6..9 under exponent 2^4 (16 + c);
     // 2-bit: code at mantissa bits 8..9 under exponent 2^2 (4 + c).
-    uint32_t mask = BITS == 4 ? 0x03C003C0u : 0x03000300u;
-    uint32_t magic = BITS == 4 ? 0x4C004C00u : 0x44004400u;
+    uint32_t mask = BITS == 8 ? 0xE480E480u : BITS == 4 ? 0x03C003C0u : 0x03000300u;
+    uint32_t magic = BITS == 8 ? 0x64006400u : BITS == 4 ? 0x4C004C00u : 0x44004400u;
     // opaque to constant folding, so both stay in registers
     asm volatile("" : "+v"(mask), "+v"(magic));
     return CodeBits{mask, magic};
@@ -163,7 +170,20 @@ template <int BITS>
 __device__ __forceinline__ half8 biased_codes(const uint32_t* w, int k, const CodeBits& cb)
 {
     u32x4 v;
-    if constexpr (BITS == 4) {
+    if constexpr (BITS == 8) {
+        // a piece is two words (codes 0..3, codes 4..7): byte j of each to
+        // bytes 0 and 2 of dword j, then (1024 + c) - 1152 = c - 128, exact
+        const uint32_t lo = w[2 * k], hi = w[2 * k + 1];
+        const f16x2 nb = __builtin_bit_cast(f16x2, cb.mask);
+        auto centred = [&](uint32_t sel) {
+            const uint32_t x = __builtin_amdgcn_perm(hi, lo, sel) | cb.magic;
+            return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, x) + nb);
+        };
+        v.x = centred(0x0c040c00u);
+        v.y = centred(0x0c050c01u);
+        v.z = centred(0x0c060c02u);
+        v.w = centred(0x0c070c03u);
+    } else if constexpr (BITS == 4) {
         const uint32_t x = w[k];
         v.x = ((x << 6) & cb.mask) | cb.magic;
         v.y = ((x << 2) & cb.mask) | cb.magic;
@@ -932,6 +952,8 @@ template <template <class> class F, int D, bool M16, class... A>
 auto by_bits(const AttnParams& p, A... args)
 {
     const bool pc = p.k_axis == KVQ_PER_CHANNEL;
+    if (p.k_bits == 8)  // 8-bit codes come as K and V both 8-bit
+        return pc ? by_groups<F, D, 8, 8, true, M16>(p, args...) : by_groups<F, D, 8, 8, false, M16>(p, args...);
     if (p.k_bits == 4 && p.v_bits == 4)
         return pc ? by_groups<F, D, 4, 4, true, M16>(p, args...) : by_groups<F, D, 4, 4, false, M16>(p, args...);
     if (p.k_bits == 4 && p.v_bits == 2)

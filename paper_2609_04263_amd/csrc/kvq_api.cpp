@@ -21,7 +21,9 @@ kvq_status check_format(const kvq_format* f, int D)
         return KVQ_ERR_ARG;
     if (D != 64 && D != 128 && D != 256)
         return KVQ_ERR_FORMAT;
-    if ((f->k_bits != 2 && f->k_bits != 4) || (f->v_bits != 2 && f->v_bits != 4))
+    if ((f->k_bits != 2 && f->k_bits != 4 && f->k_bits != 8) || (f->v_bits != 2 && f->v_bits != 4 && f->v_bits != 8))
+        return KVQ_ERR_FORMAT;
+    if ((f->k_bits == 8) != (f->v_bits == 8))  // 8-bit codes: keys and values both
         return KVQ_ERR_FORMAT;
     if ((f->k_mode != KVQ_AFFINE && f->k_mode != KVQ_SYMMETRIC) ||
         (f->v_mode != KVQ_AFFINE && f->v_mode != KVQ_SYMMETRIC))

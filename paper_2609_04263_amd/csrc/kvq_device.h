@@ -49,41 +49,8 @@ __device__ __forceinline__ float f16_bits_to_f32(uint16_t h)
     return (float)__builtin_bit_cast(_Float16, h);
 }
 
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-
-// Eight packed codes -> eight exact fp16 MFMA operand values c - offset, in
-// the element order (c0, c4, c1, c5, c2, c6, c3, c7).  For 4-bit codes `w`
-// is a whole word; for 2-bit codes the eight codes are the low 16 bits of
-// `w`.  0x6400 is binary16 1024.0, whose unit in the last place is 1, so
-// OR-ing a code c < 1024 into the mantissa gives exactly 1024 + c; one packed
-// fp16 subtract per pair (exact: the result is a small integer) removes
-// 1024 + offset.  offset is 0 for affine codes and 2^(bits-1) for symmetric
-// codes, whose stored value is q + 2^(bits-1).
-template <int BITS>
-__device__ __forceinline__ half8 codes_to_half8(uint32_t w, half2_t bias)
-{
-    uint32_t y;
-    uint32_t mask;
-    if (BITS == 4) {
-        y = w;
-        mask = 0x000F000Fu;
-    } else {
-        y = (w & 0xFFFFu) | ((w & 0xFFFFu) << 8);  // codes 4..7 land at bits 16..23
-        mask = 0x00030003u;
-    }
-    half2_t h0 = __builtin_bit_cast(half2_t, ((y >> (0 * BITS)) & mask) | 0x64006400u) - bias;
-    half2_t h1 = __builtin_bit_cast(half2_t, ((y >> (1 * BITS)) & mask) | 0x64006400u) - bias;
-    half2_t h2 = __builtin_bit_cast(half2_t, ((y >> (2 * BITS)) & mask) | 0x64006400u) - bias;
-    half2_t h3 = __builtin_bit_cast(half2_t, ((y >> (3 * BITS)) & mask) | 0x64006400u) - bias;
-    u32x4 v;
-    v.x = __builtin_bit_cast(uint32_t, h0);
-    v.y = __builtin_bit_cast(uint32_t, h1);
-    v.z = __builtin_bit_cast(uint32_t, h2);
-    v.w = __builtin_bit_cast(uint32_t, h3);
-    return __builtin_bit_cast(half8, v);
-}
-
-// Position e of an MFMA operand built by codes_to_half8 holds code PERM4[e].
+// Position e of a code operand holds code perm4(e) of its piece: dword j of
+// the operand carries codes j and j + 4.
 __device__ constexpr int perm4(int e)
 {
     return (e & 1) ? 4 + (e >> 1) : (e >> 1);

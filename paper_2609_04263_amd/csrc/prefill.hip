@@ -47,12 +47,12 @@ constexpr int rows_per_tile()
     return kWaves * 16 * qn<D>();
 }
 
-// Raw bytes of one 32-token block: codes (4 D pieces of at most 4 bytes) and
-// metadata (at most D floats per section) of K and V.
-template <int D>
+// Raw bytes of one 32-token block: codes (4 D pieces of at most 4 bytes, 8
+// for 8-bit codes) and metadata (at most D floats per section) of K and V.
+template <int D, bool W8>
 constexpr int raw_bytes()
 {
-    return 2 * 4 * D * 4 + 4 * D * 4;
+    return 2 * 4 * D * (W8 ? 8 : 4) + 4 * D * 4;
 }
 
 // LDS (bytes): K hi/lo [32][D + 8], V^T [D][40] (fp16), then the raw block;
@@ -63,11 +63,11 @@ constexpr size_t kv_bytes()
     return 2 * 32 * (D + 8) * 2 + D * 40 * 2;
 }
 
-template <int D>
+template <int D, bool W8>
 constexpr size_t lds_bytes()
 {
     constexpr size_t rot = (size_t)rows_per_tile<D>() * D * 4;
-    return (kv_bytes<D>() > rot ? kv_bytes<D>() : rot) + raw_bytes<D>();
+    return (kv_bytes<D>() > rot ? kv_bytes<D>() : rot) + raw_bytes<D, W8>();
 }
 
 __device__ __forceinline__ float dq(int mode, int bits, uint32_t c, float s, float z)
@@ -100,12 +100,31 @@ __device__ __forceinline__ void meta8(const uint8_t* sec, int i, bool m16, float
     }
 }
 
-// eight codes of piece idx of a raw code range (4-bit: one u32; 2-bit: one u16)
-__device__ __forceinline__ uint32_t piece(const uint8_t* sec, int idx, int bits)
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+// Eight codes of piece idx of a raw code range (8-bit: two u32; 4-bit: one
+// u32; 2-bit: one u16), as the words holding codes 0..3 and 4..7 (the same
+// word unless the codes are 8-bit).
+struct Piece {
+    uint32_t lo, hi;
+};
+
+template <bool W8>
+__device__ __forceinline__ Piece piece(const uint8_t* sec, int idx, int bits)
 {
-    if (bits == 4)
-        return ((const uint32_t*)sec)[idx];
-    return ((const uint16_t*)sec)[idx];
+    if constexpr (W8) {
+        const u32x2 w = ((const u32x2*)sec)[idx];
+        return Piece{w.x, w.y};
+    }
+    const uint32_t w = bits == 4 ? ((const uint32_t*)sec)[idx] : ((const uint16_t*)sec)[idx];
+    return Piece{w, w};
+}
+
+// Code e (0..7) of a piece.
+__device__ __forceinline__ uint32_t code_of(const Piece& w, int bits, int e)
+{
+    const uint32_t x = e < 4 ? w.lo : w.hi;
+    return (x >> ((bits * e) & 31)) & ((1u << bits) - 1u);
 }
 
 
@@ -136,7 +155,9 @@ __device__ void fwht_rows(float* x, int rows, float c)
     __syncthreads();
 }
 
-template <int D>
+// W8: both code widths are 8 bits (a raw block twice as large); otherwise
+// 2 or 4 bits each.
+template <int D, bool W8>
 __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
 {
     constexpr int QN = qn<D>(), RT = rows_per_tile<D>(), NKS = D / 32, NCT = D / 16;
@@ -145,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
     uint16_t* kh = (uint16_t*)plds;
     uint16_t* kl = kh + 32 * KP;
     uint16_t* vh = kl + 32 * KP;
-    constexpr size_t kRawOff = lds_bytes<D>() - raw_bytes<D>();
+    constexpr size_t kRawOff = lds_bytes<D, W8>() - raw_bytes<D, W8>();
     uint8_t* raw = plds + kRawOff;
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -220,7 +241,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
     const int NB = p.T >> 5;
     const size_t ub0 = (size_t)unit * NB;
     const int nkb = newest / 32 + 1;
-    const int kbits = p.k_bits, vbits = p.v_bits;
+    const int kbits = W8 ? 8 : p.k_bits, vbits = W8 ? 8 : p.v_bits;
     const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
 
     // Byte ranges of one block's raw data, in the order they sit in LDS: Kc,
@@ -234,7 +255,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
     const int st1 = len0, st2 = st1 + len1, st3 = st2 + len2, st4 = st3 + len3, st5 = st4 + len4;
     const int st6 = st5 + len5;
     // this thread's 16-byte units of a block's raw data
-    constexpr int UPT = (raw_bytes<D>() / 16 + kThreads - 1) / kThreads;
+    constexpr int UPT = (raw_bytes<D, W8>() / 16 + kThreads - 1) / kThreads;
     u32x4 pre[UPT];
     auto fetch_raw = [&](int blk) {
         const size_t ibf = ub0 + blk;
@@ -292,19 +313,18 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
                 if (t < p.nq) {
                     const int row = 4 * (tau / 8) + tau % 4, half = (tau / 4) % 2;
                     const int idx = (half * 64 + row + 16 * (P % 4)) * (D / 32) + P / 4;
-                    const uint32_t w = piece(rkc, idx, kbits);
-                    const uint32_t mask = (1u << kbits) - 1u;
+                    const Piece w = piece<W8>(rkc, idx, kbits);
                     if (p.k_axis == KVQ_PER_TOKEN) {
                         const int mi = ((8 * P) / p.k_group) * 32 + tau;
                         const float sc = meta(rks, mi, m16), z = kaff ? meta(rkz, mi, m16) : 0.0f;
 #pragma unroll
                         for (int e = 0; e < 8; ++e)
-                            v[e] = dq(p.k_mode, kbits, (w >> (kbits * e)) & mask, sc, z);
+                            v[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), sc, z);
                     } else {
 #pragma unroll
                         for (int e = 0; e < 8; ++e) {
                             const int mi = 8 * P + e;
-                            v[e] = dq(p.k_mode, kbits, (w >> (kbits * e)) & mask, meta(rks, mi, m16),
+                            v[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), meta(rks, mi, m16),
                                       kaff ? meta(rkz, mi, m16) : 0.0f);
                         }
                     }
@@ -321,8 +341,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
                 float v[8];
                 const int t0 = 32 * blk + 8 * o;
                 const int idx = (d % 16 + 16 * o) * (D / 16) + d / 16;
-                const uint32_t w = t0 < p.nq ? piece(rvc, idx, vbits) : 0u;
-                const uint32_t mask = (1u << vbits) - 1u;
+                const Piece w = t0 < p.nq ? piece<W8>(rvc, idx, vbits) : Piece{0u, 0u};
                 // the octet's eight scales (and offsets) are consecutive
                 const int mi = (d / p.v_group) * 32 + 8 * o;
                 float sv[8], zv[8];
@@ -332,7 +351,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const float sc = sv[e], z = vaff ? zv[e] : 0.0f;
-                    v[e] = t0 + e < p.nq ? dq(p.v_mode, vbits, (w >> (vbits * e)) & mask, sc, z) : 0.0f;
+                    v[e] = t0 + e < p.nq ? dq(p.v_mode, vbits, code_of(w, vbits, e), sc, z) : 0.0f;
                 }
                 *(u32x4*)(vh + d * VP + 8 * o) = __builtin_bit_cast(u32x4, pack_half8(v));
             }
@@ -495,7 +514,10 @@ hipError_t launch(const AttnParams& p, hipStream_t stream)
 {
     constexpr int RT = rows_per_tile<D>();
     const dim3 grid((p.C * p.G + RT - 1) / RT, p.B * p.H);
-    hipLaunchKernelGGL(prefill_kernel<D>, grid, dim3(kThreads), lds_bytes<D>(), stream, p);
+    const bool w8 = p.k_bits == 8;  // 8-bit codes come as K and V both 8-bit
+    void (*kern)(AttnParams) = w8 ? prefill_kernel<D, true> : prefill_kernel<D, false>;
+    const size_t lds = w8 ? lds_bytes<D, true>() : lds_bytes<D, false>();
+    hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, p);
     return hipGetLastError();
 }
 

@@ -4,8 +4,8 @@ Both sides code the same bf16 K/V.  The GPU appends in ragged chunks
 (1 token, partial 32-token blocks, a bulk chunk) while the oracle appends
 everything at once, so byte equality also checks chunking invariance of the
 kernels.  Formats cover every workload plus 2-bit affine, symmetric codes
-with an fp16 window, per-channel keys with a 64-token window and
-head_dim-wide groups.
+with an fp16 window, per-channel keys with a 64-token window,
+head_dim-wide groups, fp16 metadata and 8-bit codes.
 """
 import numpy as np
 import pytest
@@ -36,6 +36,13 @@ CASES = {
     "tiny_meta16": (dict(configs.WORKLOADS["tiny_b16"].fmt, meta_fp16=1), 64),
     "kivi_meta16": (dict(configs.WORKLOADS["llama8b_kivi"].fmt, meta_fp16=1), 128),
     "hadamard_meta16": (dict(configs.WORKLOADS["llama8b_had"].fmt, meta_fp16=1), 128),
+    # 8-bit codes (the 8-bit ablation): the tiny model's format, symmetric
+    # codes with a window at D = 256, per-channel keys with fp16 metadata
+    "affine8": (configs.make_format(8, 8, k_group=64, v_group=64), 64),
+    "sym8_window_d256": (configs.make_format(8, 8, k_mode=1, v_mode=1, k_group=64, v_group=128,
+                                             residual=32, flush=32), 256),
+    "perch8_meta16": (configs.make_format(8, 8, k_axis=1, k_group=32, v_group=32, residual=32,
+                                          flush=32, meta_fp16=1), 128),
 }
 
 

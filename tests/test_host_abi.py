@@ -43,7 +43,19 @@ FORMATS = [wl.fmt for wl in configs.WORKLOADS.values()] + [
     configs.make_format(4, 2, k_axis=1, k_group=32, v_group=64, residual=64, flush=64),
     configs.make_format(4, 4, k_group=256, v_group=256),
     configs.make_format(2, 4, k_axis=1, k_group=32, v_group=64, residual=128, flush=32, meta_fp16=1),
+    configs.make_format(8, 8, k_group=64, v_group=128),
+    configs.make_format(8, 8, k_mode=1, k_axis=1, k_group=32, v_group=32, residual=32, flush=32,
+                        meta_fp16=1),
 ]
+
+
+@pytest.mark.parametrize("kb,vb", [(8, 4), (4, 8), (8, 2), (3, 3), (16, 16)])
+def test_code_widths_outside_the_kernels_are_rejected(kvq, kb, vb):
+    # 8-bit codes are served only as K and V both 8-bit
+    f = configs.make_format(kb, vb, k_group=64, v_group=64)
+    with pytest.raises(kvq.KvqError) as e:
+        kvq.cache_bytes(f, 1, 1, 64, 32)
+    assert e.value.status == kvq.ERR_FORMAT
 
 
 @pytest.mark.parametrize("fi", range(len(FORMATS)))
