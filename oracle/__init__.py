@@ -35,7 +35,9 @@ _SRC = os.path.join(_HERE, "kvq_oracle.c")
 _LIB = os.path.join(_HERE, "libkvq_oracle.so")
 
 FORMAT_FIELDS = ("k_bits", "v_bits", "k_mode", "v_mode", "k_axis", "v_axis",
-                 "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16")
+                 "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16", "sink")
+
+N_SECTIONS = 10  # Kc Ks Kz Vc Vs Vz Kr Vr Kq Vq
 
 ERRORS = {0: "ok", 1: "bad argument", 2: "bad format", 3: "capacity exceeded",
           4: "non-finite input", 5: "out of memory"}
@@ -204,10 +206,10 @@ def check_format(fmt, D: int) -> int:
 
 
 def layout(fmt, B: int, H: int, D: int, T_max: int):
-    """(offsets[8], lengths[8], total bytes) of the storage image."""
+    """(offsets[10], lengths[10], total bytes) of the storage image."""
     f = _fmt(fmt)
-    off = np.zeros(8, dtype=np.uint64)
-    ln = np.zeros(8, dtype=np.uint64)
+    off = np.zeros(N_SECTIONS, dtype=np.uint64)
+    ln = np.zeros(N_SECTIONS, dtype=np.uint64)
     tot = np.zeros(1, dtype=np.uint64)
     st = lib().orc_layout(C.byref(f), B, H, D, T_max, _ptr(off), _ptr(ln), _ptr(tot))
     if st:

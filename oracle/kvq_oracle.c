@@ -19,7 +19,8 @@
  *                     paper stores it (Sec. 3.1); rounding is a reading.
  *   orc_fwht_f32      Sec. 3.1, KVarN's fixed normalized Hadamard transform.
  *   orc_append        Sec. 3.1: new states are coded, packed and appended;
- *                     KIVI's fp16 residual window of recent tokens.
+ *                     KIVI's fp16 residual window of recent tokens;
+ *                     KVarN's fp16 sink tokens (the first S tokens).
  *   orc_dequant       Sec. 3.2: the reconstruction presented to attention.
  *   orc_decode_attn   Sec. 3.1-3.2: attention over that reconstruction, fp64.
  *   orc_prefill_attn  Sec. 3.1 "Evaluation consumes 128-token chunks": the
@@ -32,10 +33,19 @@
  * reconstruction and attention accumulate in binary64.
  *
  * Storage image (the byte layout the GPU library must reproduce exactly):
- * sections Kc, Ks, Kz, Vc, Vs, Vz, Kr, Vr, each starting at a multiple of
- * 256 bytes.  T_alloc = T_max rounded up to a multiple of 32; NB = T_alloc/32
- * blocks of 32 tokens per (b, h); u = b*H + h; token t is position
- * tau = t % 32 of block beta = t / 32.
+ * sections Kc, Ks, Kz, Vc, Vs, Vz, Kr, Vr, Kq, Vq, each starting at a
+ * multiple of 256 bytes.
+ *
+ * Sink tokens (a reading of KVarN's protected first tokens, Sec. 3.1): with
+ * sink = S > 0 the first S tokens of a sequence are kept as fp16 rows
+ * (rotated first when the format rotates) and never coded.  Tokens from S
+ * on form the coded tail: tail token i is token S + i, and every rule below
+ * (blocks, the residual window, the ring slot) applies to the tail indices
+ * as it would to a cache without sinks.  Below, t is a tail index.
+ *
+ * T_alloc = max(T_max - S, 0) rounded up to a multiple of 32; NB =
+ * T_alloc/32 blocks of 32 tokens per (b, h); u = b*H + h; token t is
+ * position tau = t % 32 of block beta = t / 32.
  *
  * Codes are stored in pieces of eight codes, code j of a piece at bits
  * [bits*j, bits*j + bits) (a piece is a u64 for 8-bit codes, a u32 for
@@ -58,6 +68,8 @@
  *   Vz  like Vs, affine V only
  *   Kr  f16 [B][H][R+F][D]             fp16 residual ring (F > 0 only)
  *   Vr  f16 [B][H][R+F][D]
+ *   Kq  f16 [B][H][S][D]               fp16 sink tokens (S > 0 only)
+ *   Vq  f16 [B][H][S][D]
  * The paper fixes the codes, their width and the metadata (Sec. 3.1), not
  * the order of the packed bytes; this order is the one the decode kernel
  * reads, so the packed cache is streamed without rearrangement.
@@ -86,6 +98,7 @@ typedef struct {
     int residual, flush;  /* fp16 window: R newest tokens kept, flushed F at a time; 0,0 = none */
     int rotate;           /* 0, or head_dim: Hadamard rotation of K/V before coding */
     int meta_fp16;        /* 0: fp32 scales and offsets; 1: fp16 (the paper's storage) */
+    int sink;             /* 0, or S (a multiple of 32): the first S tokens kept as fp16 */
 } orc_format;
 
 /* ------------------------------------------------------------------ */
@@ -393,6 +406,8 @@ int orc_check_format(const orc_format* f, int D)
         return ORC_ERR_FORMAT;
     if (f->meta_fp16 != 0 && f->meta_fp16 != 1)
         return ORC_ERR_FORMAT;
+    if (f->sink < 0 || f->sink % 32 != 0)
+        return ORC_ERR_FORMAT;
     return ORC_OK;
 }
 
@@ -401,8 +416,14 @@ static size_t round_up(size_t v, size_t a)
     return (v + a - 1) / a * a;
 }
 
-/* Byte offsets and lengths of the eight sections; see the file header. */
-int orc_layout(const orc_format* f, int B, int H, int D, int T_max, size_t off[8], size_t len[8], size_t* total)
+/* Tail slots allocated per (b, h): T_max - S rounded up to 32. */
+static size_t tail_alloc(const orc_format* f, int T_max)
+{
+    return T_max > f->sink ? round_up((size_t)(T_max - f->sink), 32) : 0;
+}
+
+/* Byte offsets and lengths of the ten sections; see the file header. */
+int orc_layout(const orc_format* f, int B, int H, int D, int T_max, size_t off[10], size_t len[10], size_t* total)
 {
     int st = orc_check_format(f, D);
     if (st)
@@ -410,7 +431,7 @@ int orc_layout(const orc_format* f, int B, int H, int D, int T_max, size_t off[8
     if (B < 1 || H < 1 || T_max < 1)
         return ORC_ERR_ARG;
     size_t bh = (size_t)B * H;
-    size_t T = round_up((size_t)T_max, 32);
+    size_t T = tail_alloc(f, T_max);
     size_t ring = (size_t)(f->residual + f->flush);
     len[0] = bh * T * (size_t)(D * f->k_bits / 32) * 4;
     const size_t msz = f->meta_fp16 ? 2 : 4; /* bytes per scale or offset */
@@ -424,8 +445,10 @@ int orc_layout(const orc_format* f, int B, int H, int D, int T_max, size_t off[8
     len[5] = f->v_mode == 0 ? len[4] : 0;
     len[6] = f->flush ? bh * ring * (size_t)D * 2 : 0;
     len[7] = len[6];
+    len[8] = bh * (size_t)f->sink * (size_t)D * 2;
+    len[9] = len[8];
     size_t o = 0;
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 10; ++i) {
         off[i] = o;
         o = round_up(o + len[i], 256);
     }
@@ -433,11 +456,12 @@ int orc_layout(const orc_format* f, int B, int H, int D, int T_max, size_t off[8
     return ORC_OK;
 }
 
-/* Tokens held as codes when n tokens are cached: all of them without a
- * residual window, else floor(max(0, n - R) / F) * F (the newest R..R+F-1
- * tokens stay fp16). */
+/* Tokens held as codes when n tokens are cached, counted over the tail of
+ * m = max(0, n - S) tokens after the sink: all m without a residual window,
+ * else floor(max(0, m - R) / F) * F (the newest R..R+F-1 stay fp16). */
 int orc_num_coded(const orc_format* f, int n)
 {
+    n = n > f->sink ? n - f->sink : 0;
     if (f->flush == 0)
         return n;
     int over = n - f->residual;
@@ -450,12 +474,12 @@ typedef struct {
     const orc_format* f;
     int B, H, D, T;     /* T = T_alloc */
     uint8_t* img;
-    size_t off[8];
+    size_t off[10];
 } image_view;
 
 static int view_init(image_view* v, const orc_format* f, int B, int H, int D, int T_max, const uint8_t* img)
 {
-    size_t len[8], total;
+    size_t len[10], total;
     int st = orc_layout(f, B, H, D, T_max, v->off, len, &total);
     if (st)
         return st;
@@ -463,7 +487,7 @@ static int view_init(image_view* v, const orc_format* f, int B, int H, int D, in
     v->B = B;
     v->H = H;
     v->D = D;
-    v->T = (int)round_up((size_t)T_max, 32);
+    v->T = (int)tail_alloc(f, T_max);
     v->img = (uint8_t*)img;
     return ORC_OK;
 }
@@ -540,6 +564,13 @@ static uint16_t* ring_entry(const image_view* v, int which, int b, int h, int t)
     return (uint16_t*)(v->img + v->off[which ? 7 : 6]) + i;
 }
 
+/* fp16 row of sink token t (t < S). */
+static uint16_t* sink_entry(const image_view* v, int which, int b, int h, int t)
+{
+    size_t i = (((size_t)b * v->H + h) * (size_t)v->f->sink + (size_t)t) * v->D;
+    return (uint16_t*)(v->img + v->off[which ? 9 : 8]) + i;
+}
+
 /* Scale or offset i of a metadata section (1, 2, 4, 5), fp32 or fp16. */
 static float meta_get(const image_view* v, int section, size_t i)
 {
@@ -568,10 +599,12 @@ static void meta_put(const image_view* v, int section, size_t i, float x)
 /* Append (Sec. 3.1: new states are packed and appended)                */
 /* ------------------------------------------------------------------ */
 
-/* The D values of token t, (b, h), for K (which = 0) or V (which = 1), as
- * the coder sees them: the bf16 input (rotated in binary32 when the format
- * rotates); with a residual window, rounded to fp16, or read back from the
- * fp16 ring for tokens appended by an earlier call. */
+/* The D values of tail token t, (b, h), for K (which = 0) or V (which = 1),
+ * as the coder sees them: the bf16 input (rotated in binary32 when the
+ * format rotates); with a residual window, rounded to fp16, or read back
+ * from the fp16 ring for tokens appended by an earlier call.  n0 is the tail
+ * index of the call's first input token (negative when the call starts in
+ * the sink). */
 static void token_values(const image_view* v, int which, const uint16_t* X, int n0, int n_new, int b, int h, int t,
                          float* out)
 {
@@ -635,6 +668,8 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
         if (!isfinite(bf16_to_f32(K[i])) || !isfinite(bf16_to_f32(V[i])))
             return ORC_ERR_NONFINITE;
 
+    /* sink tokens [n0, min(S, n1)); tail indices [n0t, n1t) for the rest */
+    const int S = f->sink, n0t = n0 - S, n1t = n1 - S;
     const int q0 = orc_num_coded(f, n0), q1 = orc_num_coded(f, n1);
     const int kb = f->k_bits, vb = f->v_bits;
     float* x = (float*)malloc(sizeof(float) * (size_t)D * 32);
@@ -651,7 +686,7 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
             /* K, groups along head_dim: each coded token on its own. */
             if (f->k_axis == 0) {
                 for (int t = q0; t < q1; ++t) {
-                    token_values(&v, 0, K, n0, n_new, b, h, t, x);
+                    token_values(&v, 0, K, n0t, n_new, b, h, t, x);
                     for (int d0 = 0; d0 < D; d0 += f->k_group) {
                         float s, z;
                         code_group(f->k_mode, kb, m16, x + d0, f->k_group, codes + d0, &s, &z);
@@ -667,7 +702,7 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                 /* K, groups of 32 tokens per channel (KIVI keys). */
                 for (int t0 = q0; t0 < q1; t0 += 32) {
                     for (int i = 0; i < 32; ++i)
-                        token_values(&v, 0, K, n0, n_new, b, h, t0 + i, x + (size_t)i * D);
+                        token_values(&v, 0, K, n0t, n_new, b, h, t0 + i, x + (size_t)i * D);
                     float col[32];
                     uint8_t cc[32];
                     for (int d = 0; d < D; ++d) {
@@ -691,7 +726,7 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
              * token t keeps the bits of earlier tokens in its piece and
              * clears those of t and later tokens before inserting t's code. */
             for (int t = q0; t < q1; ++t) {
-                token_values(&v, 1, V, n0, n_new, b, h, t, x);
+                token_values(&v, 1, V, n0t, n_new, b, h, t, x);
                 for (int d0 = 0; d0 < D; d0 += f->v_group) {
                     float s, z;
                     code_group(f->v_mode, vb, m16, x + d0, f->v_group, codes + d0, &s, &z);
@@ -707,14 +742,29 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
                     piece_put(pc, vb, (piece_get(pc, vb) & keep) | ((uint64_t)codes[d] << (vb * j)));
                 }
             }
+            /* sink tokens: the fp16 of the (rotated) input, row t */
+            for (int which = 0; which < 2; ++which) {
+                for (int t = n0; t < n1 && t < S; ++t) {
+                    const uint16_t* src = (which ? V : K) + (((size_t)b * n_new + (t - n0)) * H + h) * D;
+                    for (int d = 0; d < D; ++d)
+                        x[d] = bf16_to_f32(src[d]);
+                    if (f->rotate)
+                        orc_fwht_f32(x, D);
+                    uint16_t* r = sink_entry(&v, which, b, h, t);
+                    for (int d = 0; d < D; ++d)
+                        r[d] = orc_f32_to_f16(x[d]);
+                }
+            }
             /* fp16 residual ring: slot t mod (R + F) holds the newest token
              * with that residue (written after the coder has read it). */
             if (f->flush) {
                 int ring = f->residual + f->flush;
-                int t_lo = n1 - ring > n0 ? n1 - ring : n0;
+                int t_lo = n0t > 0 ? n0t : 0;
+                if (n1t - ring > t_lo)
+                    t_lo = n1t - ring;
                 for (int which = 0; which < 2; ++which) {
-                    for (int t = t_lo; t < n1; ++t) {
-                        token_values(&v, which, which ? V : K, n0, n_new, b, h, t, x);
+                    for (int t = t_lo; t < n1t; ++t) {
+                        token_values(&v, which, which ? V : K, n0t, n_new, b, h, t, x);
                         uint16_t* r = ring_entry(&v, which, b, h, t);
                         for (int d = 0; d < D; ++d)
                             r[d] = orc_f32_to_f16(x[d]);
@@ -741,28 +791,33 @@ static double dequant_code(int mode, int bits, uint32_t c, float s, float z)
 }
 
 /* Reconstruction of tokens [0, n) of (b, h) into khat, vhat [n][D] (fp64):
- * coded tokens from codes and metadata, residual tokens from the fp16 ring.
+ * sink tokens from their fp16 rows; tail token i = t - S from codes and
+ * metadata while i is below the coded count, else from the fp16 ring.
  * Values stay in the rotated basis when the format rotates. */
 static void reconstruct_bh(const image_view* v, int b, int h, int n, double* khat, double* vhat)
 {
     const orc_format* f = v->f;
-    int D = v->D, nq = orc_num_coded(f, n);
+    int D = v->D, nq = orc_num_coded(f, n), S = f->sink;
     const int kb = f->k_bits, vb = f->v_bits;
     for (int t = 0; t < n; ++t) {
+        const int i = t - S; /* tail index */
         for (int d = 0; d < D; ++d) {
             double kv, vv;
-            if (t < nq) {
-                uint64_t kw = piece_get(kc_piece(v, b, h, t, d / 8), kb);
+            if (t < S) {
+                kv = orc_f16_to_f32(sink_entry(v, 0, b, h, t)[d]);
+                vv = orc_f16_to_f32(sink_entry(v, 1, b, h, t)[d]);
+            } else if (i < nq) {
+                uint64_t kw = piece_get(kc_piece(v, b, h, i, d / 8), kb);
                 uint32_t kc = (uint32_t)(kw >> (kb * (d % 8))) & ((1u << kb) - 1u);
-                size_t km = kmeta_index(v, b, h, t, d);
+                size_t km = kmeta_index(v, b, h, i, d);
                 kv = dequant_code(f->k_mode, kb, kc, meta_get(v, 1, km), f->k_mode == 0 ? meta_get(v, 2, km) : 0.0f);
-                uint64_t vw = piece_get(vc_piece(v, b, h, t, d), vb);
-                uint32_t vc = (uint32_t)(vw >> (vb * (t % 8))) & ((1u << vb) - 1u);
-                size_t vm = vmeta_index(v, b, h, t, d);
+                uint64_t vw = piece_get(vc_piece(v, b, h, i, d), vb);
+                uint32_t vc = (uint32_t)(vw >> (vb * (i % 8))) & ((1u << vb) - 1u);
+                size_t vm = vmeta_index(v, b, h, i, d);
                 vv = dequant_code(f->v_mode, vb, vc, meta_get(v, 4, vm), f->v_mode == 0 ? meta_get(v, 5, vm) : 0.0f);
             } else {
-                kv = orc_f16_to_f32(ring_entry(v, 0, b, h, t)[d]);
-                vv = orc_f16_to_f32(ring_entry(v, 1, b, h, t)[d]);
+                kv = orc_f16_to_f32(ring_entry(v, 0, b, h, i)[d]);
+                vv = orc_f16_to_f32(ring_entry(v, 1, b, h, i)[d]);
             }
             khat[(size_t)t * D + d] = kv;
             vhat[(size_t)t * D + d] = vv;

@@ -18,10 +18,10 @@ PER_TOKEN, PER_CHANNEL = 0, 1
 
 def make_format(k_bits=4, v_bits=4, k_mode=AFFINE, v_mode=AFFINE, k_axis=PER_TOKEN,
                 v_axis=PER_TOKEN, k_group=64, v_group=64, residual=0, flush=0, rotate=0,
-                meta_fp16=0) -> dict:
+                meta_fp16=0, sink=0) -> dict:
     return dict(k_bits=k_bits, v_bits=v_bits, k_mode=k_mode, v_mode=v_mode, k_axis=k_axis,
                 v_axis=v_axis, k_group=k_group, v_group=v_group, residual=residual,
-                flush=flush, rotate=rotate, meta_fp16=meta_fp16)
+                flush=flush, rotate=rotate, meta_fp16=meta_fp16, sink=sink)
 
 
 @dataclass(frozen=True)

@@ -99,7 +99,7 @@ def test_cache_with_fp16_metadata():
     B, H, D, T = 1, 2, 64, 64
     _, len32, _ = oracle.layout(f32, B, H, D, T)
     _, len16, _ = oracle.layout(f16_, B, H, D, T)
-    assert [len16[i] * (2 if i in (1, 2, 4, 5) else 1) for i in range(8)] == list(len32)
+    assert [len16[i] * (2 if i in (1, 2, 4, 5) else 1) for i in range(10)] == list(len32)
     K, V = synth.kv_tokens(7, B, 40, H, D)
     c = oracle.Cache(f16_, B, H, D, T)
     c.append(K, V)
