@@ -52,6 +52,8 @@ def parse():
                     help="store scales and offsets as fp16 (the paper's storage) instead of the workload's fp32")
     ap.add_argument("--bits8", action="store_true",
                     help="8-bit key and value codes (the 8-bit ablation) in the workload's groups and modes")
+    ap.add_argument("--sink", type=int, default=0,
+                    help="keep the first SINK tokens as fp16 rows (KVarN's sink tokens; a multiple of 32)")
     ap.add_argument("--cpu-sample-steps", type=int, default=None)
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the timed region, copy a buffer of this many MiB once (a kernel of known "
@@ -113,6 +115,9 @@ def main():
     if args.bits8:
         import dataclasses
         wl = dataclasses.replace(wl, name=wl.name + "+k8v8", fmt=dict(wl.fmt, k_bits=8, v_bits=8))
+    if args.sink:
+        import dataclasses
+        wl = dataclasses.replace(wl, name=wl.name + "+sink%d" % args.sink, fmt=dict(wl.fmt, sink=args.sink))
     B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
 
     def bf16(bits):

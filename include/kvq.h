@@ -67,7 +67,14 @@ enum { KVQ_PER_TOKEN = 0, KVQ_PER_CHANNEL = 1 };
  *            the paper stores them (Sec. 3.1): the fp32 scale and offset
  *            are rounded to nearest fp16 (scale clamped to [2^-24, 65504],
  *            offset to +-65504) and the codes are computed from the rounded
- *            values (this rounding rule is this library's reading). */
+ *            values (this rounding rule is this library's reading).
+ *   sink     0, or S, a multiple of 32: KVarN's protected first tokens
+ *            (Sec. 3.1).  Tokens t < S are kept as fp16 rows (rotated first
+ *            when the format rotates) and never coded; tokens from S on
+ *            form the coded tail, tail token i = t - S, and every rule
+ *            above (groups, the window, the ring slot, the coded count
+ *            over n - S tail tokens) applies to tail indices.  The storage
+ *            rule is this library's reading of the paper. */
 typedef struct {
     int32_t k_bits, v_bits;
     int32_t k_mode, v_mode;
@@ -76,14 +83,17 @@ typedef struct {
     int32_t residual, flush;
     int32_t rotate;
     int32_t meta_fp16;
+    int32_t sink;
 } kvq_format;
 
 /* Opaque host handle: format, dimensions, storage pointer, token count. */
 typedef struct kvq_cache kvq_cache;
 
 /* Bytes of cache storage for B sequences, H_kv heads of size D (64, 128 or
- * 256) and up to T_max tokens.  The storage image has eight sections, each
- * starting at a multiple of 256 bytes (T_alloc = T_max rounded up to 32):
+ * 256) and up to T_max tokens.  The storage image has ten sections, each
+ * starting at a multiple of 256 bytes (T_alloc = max(T_max - sink, 0)
+ * rounded up to 32, the tail capacity; "token" in sections 0-7 is a tail
+ * token):
  *   0 Kc key codes           D*k_bits/8 bytes per token
  *   1 Ks key scales          per token: D/k_group per token; per channel: D per 32 tokens
  *                            (fp32, or fp16 when meta_fp16; element i at byte 4i or 2i)
@@ -93,6 +103,8 @@ typedef struct kvq_cache kvq_cache;
  *   5 Vz value offsets, like Vs; affine values only
  *   6 Kr f16 [B][H_kv][residual+flush][D]  fp16 window, slot t mod (R+F)
  *   7 Vr f16, like Kr
+ *   8 Kq f16 [B][H_kv][sink][D]  fp16 sink tokens, row t (sink > 0 only)
+ *   9 Vq f16, like Kq
  * Sections 0-5 are blocked by 32-token blocks: with u = b*H_kv + h,
  * NB = T_alloc/32, token t at position tau = t%32 of block beta = t/32, and
  * i = u*NB + beta:
@@ -118,14 +130,14 @@ kvq_status kvq_cache_bytes(const kvq_format* fmt, int B, int H_kv, int D, int T_
 kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_max, void* storage,
                           size_t bytes, kvq_cache** out);
 
-/* Byte offset and length of storage section 0..7 (see kvq_cache_bytes). */
+/* Byte offset and length of storage section 0..9 (see kvq_cache_bytes). */
 kvq_status kvq_cache_section(const kvq_cache* cache, int index, size_t* offset, size_t* length);
 
 /* n = 0: start a new window (the paper resets the cache per evaluation
  * window, Sec. 4).  Storage is not cleared; slots at or past n are dead. */
 kvq_status kvq_cache_reset(kvq_cache* cache);
 
-/* Tokens cached (n) and tokens held as codes (n_coded <= n). */
+/* Tokens cached (n) and tokens held as codes (n_coded <= n - min(n, sink)). */
 kvq_status kvq_cache_len(const kvq_cache* cache, int* n, int* n_coded);
 
 /* Shrink n to n_new <= n without touching storage.  Valid only for formats

@@ -129,7 +129,9 @@ def coded_bytes_per_token(D: int, bits: int, axis: int, group: int, affine: bool
 
 
 def num_coded(fmt: dict, n: int) -> int:
-    """Tokens held as codes when n are cached (the rest sit in the fp16 window)."""
+    """Tokens held as codes when n are cached (the rest sit in the fp16 sink
+    or the fp16 window)."""
+    n = max(0, n - fmt.get("sink", 0))
     if fmt["flush"] == 0:
         return n
     over = n - fmt["residual"]
@@ -138,8 +140,9 @@ def num_coded(fmt: dict, n: int) -> int:
 
 def attention_bytes(wl: Workload, n: int) -> int:
     """Algorithmic HBM bytes of one decode-attention step over n cached tokens:
-    coded tokens (codes + metadata), fp16 residual tokens (K and V), the bf16
-    queries and the fp32 outputs.  Split-K partials are not counted."""
+    coded tokens (codes + metadata), fp16 sink and window tokens (K and V),
+    the bf16 queries and the fp32 outputs.  Split-K partials are not
+    counted."""
     f = wl.fmt
     nq = num_coded(f, n)
     m16 = f.get("meta_fp16", 0)

@@ -426,7 +426,8 @@ __global__ __launch_bounds__(D) void append_token_kernel(AppendParams p)
 
 // fp16 window: slot t mod (R + F) <- fp16 of token t (rotated first when
 // the format rotates), for t in [ring_lo, n0 + n_new).  Runs after the coder
-// of the same call, which may still read the slots being replaced.
+// of the same call, which may still read the slots being replaced.  The
+// sink rows are written by the same kernel with ring = sink (slot t).
 template <int D>
 __global__ __launch_bounds__(kThreads) void append_ring_kernel(AppendParams p)
 {
@@ -475,7 +476,29 @@ hipError_t launch_append_d(const AppendParams& p, hipStream_t stream)
     return hipSuccess;
 }
 
+template <int D>
+hipError_t launch_rows_d(const AppendParams& p, int hi, hipStream_t stream)
+{
+    if (hi > p.ring_lo)
+        hipLaunchKernelGGL(append_ring_kernel<D>, dim3(hi - p.ring_lo, p.B * p.H), dim3(kThreads), 0, stream, p);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_append_rows(const AppendParams& p, int D, int hi, hipStream_t stream)
+{
+    switch (D) {
+    case 64:
+        return launch_rows_d<64>(p, hi, stream);
+    case 128:
+        return launch_rows_d<128>(p, hi, stream);
+    case 256:
+        return launch_rows_d<256>(p, hi, stream);
+    default:
+        return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_append(const AppendParams& p, int D, hipStream_t stream)
 {

@@ -513,19 +513,20 @@ struct Split {
         }
     }
 
-    // One block of the fp16 window (tokens t0 .. t0 + 31, those >= n masked),
-    // read straight from the ring slots.
-    __device__ __forceinline__ void ring_block(const AttnParams& p, int unit, int t0, int lane, bool qlo_on)
+    // One block of fp16 tokens (t0 .. t0 + 31, those >= n masked) read
+    // straight from rows [unit][rows][D] at slot t mod rows: the window ring
+    // (rows = R + F) or the sink (rows = sink, slot t).
+    __device__ __forceinline__ void fp16_block(const AttnParams& p, const uint16_t* kr, const uint16_t* vr, int ring,
+                                               int n, int unit, int t0, int lane, bool qlo_on)
     {
         constexpr int D = C::D;
         const int hh = lane & 15, qg = lane >> 4;
-        const int n = p.n, ring = p.ring;
         const size_t rbase = (size_t)unit * ring;
         float l[8];
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
             const int tA = t0 + 8 * (hh >> 2) + 4 * h2 + (hh & 3);
-            const uint16_t* krow = p.kr + (rbase + (size_t)(tA % ring)) * D;
+            const uint16_t* krow = kr + (rbase + (size_t)(tA % ring)) * D;
             half8 a[NKB];
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) {
@@ -576,7 +577,7 @@ struct Split {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int sl = slot[perm4(e)];
-                const uint16_t raw = sl >= 0 ? p.vr[(rbase + (size_t)sl) * D + d] : (uint16_t)0;
+                const uint16_t raw = sl >= 0 ? vr[(rbase + (size_t)sl) * D + d] : (uint16_t)0;
                 va[mb][e] = __builtin_bit_cast(_Float16, raw);
             }
         }
@@ -619,7 +620,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     const int hh = lane & 15, qg = lane >> 4;
     const int split = blockIdx.x, unit = blockIdx.y;
     const int b = unit / p.H, j = unit % p.H, G = p.G;
-    const bool ring_split = p.ring && split == p.S_q;
+    const bool ring_split = (p.ring || p.sink) && split == p.S_q;  // the fp16 split: sink and window
     const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
     const bool qlo_on = p.rotate != 0;
     const int NB = p.T >> 5;
@@ -751,9 +752,13 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
             blk += kWaves;
         }
     } else {
-        const int nr = p.n - p.nq;
-        for (int rblk = wave; 32 * rblk < nr; rblk += kWaves)
-            S.ring_block(p, unit, p.nq + 32 * rblk, lane, qlo_on);
+        const int nsb = (p.n_sink + 31) >> 5, nrb = (p.n - p.nq + 31) >> 5;
+        for (int rb = wave; rb < nsb + nrb; rb += kWaves) {
+            if (rb < nsb)
+                S.fp16_block(p, p.kq, p.vq, p.sink, p.n_sink, unit, 32 * rb, lane, qlo_on);
+            else
+                S.fp16_block(p, p.kr, p.vr, p.ring, p.n, unit, p.nq + 32 * (rb - nsb), lane, qlo_on);
+        }
     }
 
     // ---- merge the four waves of this split in LDS

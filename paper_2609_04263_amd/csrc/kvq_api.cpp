@@ -40,6 +40,8 @@ kvq_status check_format(const kvq_format* f, int D)
         return KVQ_ERR_FORMAT;
     if (f->meta_fp16 != 0 && f->meta_fp16 != 1)
         return KVQ_ERR_FORMAT;
+    if (f->sink < 0 || f->sink % 32 != 0)
+        return KVQ_ERR_FORMAT;
     return KVQ_OK;
 }
 
@@ -48,14 +50,21 @@ size_t round_up(size_t v, size_t a)
     return (v + a - 1) / a * a;
 }
 
-kvq_status layout(const kvq_format* f, int B, int H, int D, int T_max, size_t off[8], size_t len[8], size_t* total)
+// Tail capacity per (b, h): T_max - sink rounded up to 32 (0 when the sink
+// covers T_max).
+size_t tail_alloc(const kvq_format& f, int T_max)
+{
+    return T_max > f.sink ? round_up((size_t)(T_max - f.sink), 32) : 0;
+}
+
+kvq_status layout(const kvq_format* f, int B, int H, int D, int T_max, size_t off[10], size_t len[10], size_t* total)
 {
     kvq_status st = check_format(f, D);
     if (st != KVQ_OK)
         return st;
     if (B < 1 || H < 1 || T_max < 1)
         return KVQ_ERR_ARG;
-    const size_t bh = (size_t)B * H, T = round_up((size_t)T_max, 32);
+    const size_t bh = (size_t)B * H, T = tail_alloc(*f, T_max);
     const size_t ring = (size_t)(f->residual + f->flush);
     len[0] = bh * T * (size_t)(D * f->k_bits / 32) * 4;
     const size_t msz = f->meta_fp16 ? 2 : 4;  // bytes per scale or offset
@@ -66,8 +75,10 @@ kvq_status layout(const kvq_format* f, int B, int H, int D, int T_max, size_t of
     len[5] = f->v_mode == KVQ_AFFINE ? len[4] : 0;
     len[6] = f->flush ? bh * ring * (size_t)D * 2 : 0;
     len[7] = len[6];
+    len[8] = bh * (size_t)f->sink * (size_t)D * 2;
+    len[9] = len[8];
     size_t o = 0;
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 10; ++i) {
         off[i] = o;
         o = round_up(o + len[i], 256);
     }
@@ -95,7 +106,7 @@ float rotation_constant(int D)
 // cache can need (the split count of a call never exceeds it).
 size_t decode_workspace_layout(const kvq_cache* c, int H_q, size_t* off_ml)
 {
-    int S_max = kvq::decode_split_bound(c->B, c->H) + (c->fmt.flush ? 1 : 0);
+    int S_max = kvq::decode_split_bound(c->B, c->H) + (c->fmt.flush || c->fmt.sink ? 1 : 0);
     size_t rows = (size_t)c->B * H_q;
     size_t o_ml = round_up(rows * S_max * c->D * sizeof(float), 256);
     if (off_ml)
@@ -113,8 +124,14 @@ T* at(const kvq_cache* c, int section)
 
 namespace kvq {
 
+int num_tail(const kvq_format& f, int n)
+{
+    return n > f.sink ? n - f.sink : 0;
+}
+
 int num_coded(const kvq_format& f, int n)
 {
+    n = num_tail(f, n);
     if (f.flush == 0)
         return n;
     int over = n - f.residual;
@@ -148,7 +165,7 @@ kvq_status kvq_cache_bytes(const kvq_format* fmt, int B, int H_kv, int D, int T_
 {
     if (!bytes)
         return KVQ_ERR_ARG;
-    size_t off[8], len[8];
+    size_t off[10], len[10];
     return layout(fmt, B, H_kv, D, T_max, off, len, bytes);
 }
 
@@ -157,7 +174,7 @@ kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_m
 {
     if (!out || !storage || ((uintptr_t)storage & 255u))
         return KVQ_ERR_ARG;
-    size_t off[8], len[8], total;
+    size_t off[10], len[10], total;
     kvq_status st = layout(fmt, B, H_kv, D, T_max, off, len, &total);
     if (st != KVQ_OK)
         return st;
@@ -171,7 +188,7 @@ kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_m
     c->H = H_kv;
     c->D = D;
     c->T_max = T_max;
-    c->T_alloc = (int)round_up((size_t)T_max, 32);
+    c->T_alloc = (int)tail_alloc(*fmt, T_max);
     c->base = (uint8_t*)storage;
     c->bytes = bytes;
     memcpy(c->off, off, sizeof(off));
@@ -183,7 +200,7 @@ kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_m
 
 kvq_status kvq_cache_section(const kvq_cache* c, int index, size_t* offset, size_t* length)
 {
-    if (!c || index < 0 || index > 7 || !offset || !length)
+    if (!c || index < 0 || index > 9 || !offset || !length)
         return KVQ_ERR_ARG;
     *offset = c->off[index];
     *length = c->len[index];
@@ -359,13 +376,7 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int n_new, con
     p.B = c->B;
     p.H = c->H;
     p.T = c->T_alloc;
-    p.n0 = c->n;
     p.n_new = n_new;
-    p.q0 = kvq::num_coded(f, c->n);
-    p.q1 = kvq::num_coded(f, c->n + n_new);
-    p.ring = f.residual + f.flush;
-    int n1 = c->n + n_new;
-    p.ring_lo = p.ring ? (n1 - p.ring > c->n ? n1 - p.ring : c->n) : n1;
     p.k_bits = f.k_bits;
     p.v_bits = f.v_bits;
     p.k_mode = f.k_mode;
@@ -376,8 +387,29 @@ kvq_status kvq_append(kvq_cache* c, const void* K, const void* V, int n_new, con
     p.rotate = f.rotate;
     p.rot_c = rotation_constant(c->D);
     p.meta16 = f.meta_fp16;
-    if (kvq::launch_append(p, c->D, (hipStream_t)stream) != hipSuccess)
-        return KVQ_ERR_DEVICE;
+    const int n0 = c->n, n1 = n0 + n_new, S = f.sink;
+    if (n0 < S) {
+        // sink tokens [n0, min(S, n1)): fp16 rows t of sections 8 and 9
+        kvq::AppendParams ps = p;
+        ps.kr = at<uint16_t>(c, 8);
+        ps.vr = at<uint16_t>(c, 9);
+        ps.n0 = n0;
+        ps.ring = S;
+        ps.ring_lo = n0;
+        if (kvq::launch_append_rows(ps, c->D, n1 < S ? n1 : S, (hipStream_t)stream) != hipSuccess)
+            return KVQ_ERR_DEVICE;
+    }
+    if (n1 > S) {
+        // the tail, in tail indices; n0 - S < 0 when the call starts in the sink
+        p.n0 = n0 - S;
+        p.q0 = kvq::num_coded(f, n0);
+        p.q1 = kvq::num_coded(f, n1);
+        p.ring = f.residual + f.flush;
+        const int t0 = n0 > S ? n0 - S : 0, t1 = n1 - S;
+        p.ring_lo = p.ring ? (t1 - p.ring > t0 ? t1 - p.ring : t0) : t1;
+        if (kvq::launch_append(p, c->D, (hipStream_t)stream) != hipSuccess)
+            return KVQ_ERR_DEVICE;
+    }
     c->n = n1;
     return KVQ_OK;
 }
@@ -415,6 +447,8 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.vz = at<float>(c, 5);
     p.kr = at<uint16_t>(c, 6);
     p.vr = at<uint16_t>(c, 7);
+    p.kq = at<uint16_t>(c, 8);
+    p.vq = at<uint16_t>(c, 9);
     p.q = (const uint16_t*)Q;
     p.part_o = (float*)workspace;
     p.part_ml = (float*)((uint8_t*)workspace + off_ml);
@@ -424,8 +458,10 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.H_q = H_q;
     p.G = H_q / c->H;
     p.T = c->T_alloc;
-    p.n = c->n;
+    p.n = kvq::num_tail(f, c->n);
     p.ring = f.residual + f.flush;
+    p.sink = f.sink;
+    p.n_sink = c->n < f.sink ? c->n : f.sink;
     p.k_bits = f.k_bits;
     p.v_bits = f.v_bits;
     p.k_mode = f.k_mode;
@@ -438,8 +474,19 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.rot_c = rotation_constant(c->D);
     p.meta16 = f.meta_fp16;
     p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.G);
-    kvq::decode_plan(c->B, c->H, kvq::decode_target_groups(p, c->D), p.nq, &p.S_q, &p.bps);
-    p.S_tot = p.S_q + (f.flush ? 1 : 0);
+    // With many splits per unit, the fp16 split (sink and window) of every
+    // unit takes a slot of the one resident round that the coded splits are
+    // planned to fill (one split fewer costs little; workgroups left for a
+    // second round cost a whole split).  With few splits per unit, a split
+    // fewer would lengthen every split, and the short fp16 splits free their
+    // slots early instead.
+    const bool fp16_split = f.flush || f.sink;
+    const int units = c->B * c->H;
+    int groups = kvq::decode_target_groups(p, c->D);
+    if (fp16_split && groups >= 4 * units)
+        groups -= units;
+    kvq::decode_plan(c->B, c->H, groups, p.nq, &p.S_q, &p.bps);
+    p.S_tot = p.S_q + (fp16_split ? 1 : 0);
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 
@@ -460,6 +507,8 @@ kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, f
     p.vz = at<float>(c, 5);
     p.kr = at<uint16_t>(c, 6);
     p.vr = at<uint16_t>(c, 7);
+    p.kq = at<uint16_t>(c, 8);
+    p.vq = at<uint16_t>(c, 9);
     p.q = (const uint16_t*)Q;
     p.out = (float*)O;
     p.B = c->B;
@@ -467,9 +516,13 @@ kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, f
     p.H_q = H_q;
     p.G = H_q / c->H;
     p.T = c->T_alloc;
-    p.n = c->n;
+    // chunk positions are tail indices (token minus sink): the tail length
+    // n - sink is negative when the cache ends inside the sink
+    p.n = c->n - f.sink;
     p.C = C;
     p.ring = f.residual + f.flush;
+    p.sink = f.sink;
+    p.n_sink = c->n < f.sink ? c->n : f.sink;
     p.k_bits = f.k_bits;
     p.v_bits = f.v_bits;
     p.k_mode = f.k_mode;

@@ -14,13 +14,16 @@ struct kvq_cache {
     int B, H, D, T_max, T_alloc;
     uint8_t* base;
     size_t bytes;
-    size_t off[8], len[8];
+    size_t off[10], len[10];
     int n;
 };
 
 namespace kvq {
 
-// Tokens held as codes at length n (floor(max(0, n - R)/F) * F with a window).
+// Tail tokens (past the sink) at length n.
+int num_tail(const kvq_format& f, int n);
+// Tokens held as codes at length n: the tail count m, or floor(max(0, m -
+// R)/F) * F with a window.
 int num_coded(const kvq_format& f, int n);
 
 // ---------------------------------------------------------------- append
@@ -46,6 +49,9 @@ struct AppendParams {
     int meta16;           // scales and offsets stored as fp16 (ks..vz then point at halves)
 };
 hipError_t launch_append(const AppendParams& p, int D, hipStream_t stream);
+// fp16 rows [p.ring_lo, hi) of kr/vr with row stride p.ring and slot t mod
+// p.ring, from input token t - p.n0 (the sink tokens: ring = sink).
+hipError_t launch_append_rows(const AppendParams& p, int D, int hi, hipStream_t stream);
 
 // ------------------------------------------------------------- projection
 struct ProjParams {
@@ -87,15 +93,18 @@ struct AttnParams {
     const float* vz;
     const uint16_t* kr;
     const uint16_t* vr;
+    const uint16_t* kq;   // fp16 sink rows [B][H][sink][D]
+    const uint16_t* vq;
     const uint16_t* q;    // bf16 [B][H_q][D]
     float* part_o;        // fp32 [B*H_q][S_tot][D]  unnormalized partial outputs
     float* part_ml;       // fp32 [B*H_q][S_tot][2]  (running max in log2 units, sum)
     float* out;           // fp32 [B][H_q][D]
     int B, H, H_q, G, T;  // T = T_alloc
-    int n, nq;
+    int n, nq;            // tail tokens (past the sink; prefill: n - sink, negative inside the sink), coded tokens
     int ring;
+    int sink, n_sink;     // sink rows per (b, h), and those holding tokens (min(length, sink))
     int S_q;              // splits over coded tokens
-    int S_tot;            // S_q (+1 when a window exists)
+    int S_tot;            // S_q (+1 when a window or a sink exists: the fp16 split)
     int bps;              // 32-token blocks per split
     int k_bits, v_bits, k_mode, v_mode, k_axis, k_group, v_group;
     int rotate;

@@ -24,6 +24,9 @@
 //      the eight k-slots 8 q .. 8 q + 7 its next MFMA operand needs when the
 //      keys of slot 8 q + e are taken as 4 q + e (e < 4) and 16 + 4 q + e - 4:
 //      V^T is read in that key order, so probabilities never cross lanes.
+// Sink tokens (fp16 rows) are walked first as blocks of their own, so every
+// query row holds a finite running maximum before the coded tail; fp16
+// window tokens past the coded ones are read from the ring in step 1.
 // Rotated formats transform the queries (FWHT in LDS) and the outputs back.
 
 #include "kvq_internal.h"
@@ -175,6 +178,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
     const int G = p.G, C = p.C;
     const int rows = C * G;
     const int r0 = blockIdx.x * RT;
+    // Positions are tail indices (token minus sink); sink tokens sit at
+    // -sink .. -1, so a chunk that starts in the sink has negative positions.
     const int first_pos = p.n - C;  // position of chunk token 0
 
     // ---- queries: lane's columns are rows r0 + 16 (QN wave + c) + col
@@ -214,13 +219,15 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
         __syncthreads();  // the K/V buffers overwrite the query rows
     }
 
-    // position of each of this lane's query columns (-1: no such row)
+    // position of each of this lane's query columns (kNoRow: no such row,
+    // every key masked)
+    constexpr int kNoRow = -(1 << 30);
     int qpos[QN];
-    int newest = -1;
+    int newest;
 #pragma unroll
     for (int c = 0; c < QN; ++c) {
         const int R = r0 + 16 * (QN * wave + c) + col;
-        qpos[c] = R < rows ? first_pos + R / G : -1;
+        qpos[c] = R < rows ? first_pos + R / G : kNoRow;
     }
     {
         const int Rlast = min(r0 + RT, rows) - 1;
@@ -240,7 +247,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
 
     const int NB = p.T >> 5;
     const size_t ub0 = (size_t)unit * NB;
-    const int nkb = newest / 32 + 1;
+    const int nkb = newest >= 0 ? newest / 32 + 1 : 0;  // coded-tail blocks
+    // sink blocks holding a token no later than the newest query
+    const int nsb = min((p.n_sink + 31) >> 5, (newest + p.sink) / 32 + 1);
+    const int sb0 = p.sink >> 5;  // sink block j is tail block j - sb0
     const int kbits = W8 ? 8 : p.k_bits, vbits = W8 ? 8 : p.v_bits;
     const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
 
@@ -297,12 +307,49 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
     const uint8_t* rvz = raw + st5;
     const bool m16 = p.meta16 != 0;
 
-    fetch_raw(0);
-    store_raw();
+    if (nkb > 0) {
+        fetch_raw(0);
+        store_raw();
+    }
     __syncthreads();
-    for (int blk = 0; blk < nkb; ++blk) {
-        if (blk + 1 < nkb)
+    for (int it = 0; it < nsb + nkb; ++it) {
+        const int blk = it < nsb ? it - sb0 : it - nsb;
+        if (blk >= 0 && blk + 1 < nkb)
             fetch_raw(blk + 1);  // lands while this block is computed
+        if (blk < 0) {
+            // ---- a sink block: fp16 rows, tokens past n_sink zero
+            const size_t sbase = (size_t)unit * p.sink;
+            for (int pc = threadIdx.x; pc < 4 * D; pc += kThreads) {
+                {
+                    const int tau = pc / (D / 8), P = pc % (D / 8);
+                    const int t = p.sink + 32 * blk + tau;
+                    float v[8];
+                    if (t < p.n_sink) {
+                        const u32x4 rw = *(const u32x4*)(p.kq + (sbase + t) * D + 8 * P);
+                        const uint32_t w4[4] = {rw.x, rw.y, rw.z, rw.w};
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            v[e] = f16_bits_to_f32((uint16_t)(w4[e >> 1] >> (16 * (e & 1))));
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e)
+                            v[e] = 0.0f;
+                    }
+                    split8(v, kh + tau * KP + 8 * P, kl + tau * KP + 8 * P);
+                }
+                {
+                    const int o = pc / D, d = pc % D;
+                    const int t0 = p.sink + 32 * blk + 8 * o;
+                    uint16_t hv[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        hv[e] = t0 + e < p.n_sink ? p.vq[(sbase + t0 + e) * D + d] : (uint16_t)0;
+                    *(u32x4*)(vh + d * VP + 8 * o) =
+                        u32x4{hv[0] | ((uint32_t)hv[1] << 16), hv[2] | ((uint32_t)hv[3] << 16),
+                              hv[4] | ((uint32_t)hv[5] << 16), hv[6] | ((uint32_t)hv[7] << 16)};
+                }
+            }
+        } else {
         // ---- reconstruct the block into LDS: 4 D pieces of K and of V
         for (int pc = threadIdx.x; pc < 4 * D; pc += kThreads) {
             // K piece: token tau = pc / (D / 8), channels 8 P .. 8 P + 7
@@ -392,6 +439,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
                 }
             }
         }
+        }  // coded-tail block
         __syncthreads();
 
         // ---- scores S^T (keys x query rows), two 16-key tiles
@@ -462,7 +510,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
             for (int c = 0; c < QN; ++c)
                 acc[c][t] = mfma16(ah, ph[c], acc[c][t]);
         }
-        if (blk + 1 < nkb)
+        if (blk >= 0 && blk + 1 < nkb)
             store_raw();  // the raw block was consumed before the barrier above
         __syncthreads();  // the next block overwrites K, V and the raw copy
     }

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libkvq.so")
 
 FORMAT_FIELDS = ("k_bits", "v_bits", "k_mode", "v_mode", "k_axis", "v_axis",
-                 "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16")
+                 "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16", "sink")
 
 OK, ERR_ARG, ERR_FORMAT, ERR_CAPACITY, ERR_WORKSPACE, ERR_DEVICE = range(6)
 

@@ -5,7 +5,7 @@ Both sides code the same bf16 K/V.  The GPU appends in ragged chunks
 everything at once, so byte equality also checks chunking invariance of the
 kernels.  Formats cover every workload plus 2-bit affine, symmetric codes
 with an fp16 window, per-channel keys with a 64-token window,
-head_dim-wide groups, fp16 metadata and 8-bit codes.
+head_dim-wide groups, fp16 metadata, 8-bit codes and fp16 sink tokens.
 """
 import numpy as np
 import pytest
@@ -43,6 +43,12 @@ CASES = {
                                              residual=32, flush=32), 256),
     "perch8_meta16": (configs.make_format(8, 8, k_axis=1, k_group=32, v_group=32, residual=32,
                                           flush=32, meta_fp16=1), 128),
+    # fp16 sink tokens: KVarN's K4V2 g128 with 128 sinks, a sink before a
+    # KIVI window, a 64-token sink at D = 64
+    "kvarn_sink": (configs.make_format(4, 2, k_group=128, v_group=128, rotate=128, sink=128), 128),
+    "sink32_window": (configs.make_format(2, 2, k_axis=1, k_group=32, v_group=32, residual=64,
+                                          flush=32, sink=32), 128),
+    "sink64": (configs.make_format(4, 4, k_group=64, v_group=64, sink=64), 64),
 }
 
 
@@ -61,7 +67,7 @@ def run_case(name, B, H, n, cuts, seed):
     assert gc.length() == (n, ref.n_coded)
     img = image(gc)
     assert img.size == ref.image.size
-    for i in range(8):
+    for i in range(10):
         o, ln = ref.offsets[i], ref.lengths[i]
         a, b = img[o:o + ln], ref.image[o:o + ln]
         if not np.array_equal(a, b):
@@ -76,7 +82,7 @@ def test_append_ragged_chunks_match_oracle(name):
     run_case(name, B=2, H=3, n=n, cuts=[0, 1, 2, 31, 64, 100, 131, 200, n], seed=31)
 
 
-@pytest.mark.parametrize("name", ["tiny_b16", "kivi", "hadamard"])
+@pytest.mark.parametrize("name", ["tiny_b16", "kivi", "hadamard", "kvarn_sink", "sink32_window"])
 def test_append_token_by_token(name):
     n = 170
     run_case(name, B=1, H=2, n=n, cuts=list(range(n + 1)), seed=32)
