@@ -20,6 +20,7 @@ the CPU oracle (single thread) on a bounded sample of decode steps.
   python bench.py --phase prefill [--workload gqa12b_b8]   (projection GEMM, MFMA roofline)
   python bench.py --phase merge [--workload llama8b_had]    (dense adapter merge, HBM roofline)
   python bench.py --phase prefill_attn [--workload gqa12b_b8] (chunked prefill attention, MFMA roofline)
+  python bench.py --phase append [--workload gqa12b_b8]     (one prefill chunk appended, HBM roofline)
 """
 from __future__ import annotations
 
@@ -46,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's decode steps)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn"], default="decode")
+    ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn", "append"], default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--meta-fp16", action="store_true",
                     help="store scales and offsets as fp16 (the paper's storage) instead of the workload's fp32")
@@ -135,6 +136,8 @@ def main():
         return bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch)
     if args.phase == "merge":
         return bench_merge(args, wl, W, A, Bm, kvq, torch)
+    if args.phase == "append":
+        return bench_append(args, wl, dev, synth, kvq, configs, torch)
 
     # ---------------------------------------------------------------- setup
     T_max = wl.context + wl.decode_steps
@@ -377,6 +380,46 @@ def bench_merge(args, wl, W, A, Bm, kvq, torch):
         "config": {"workload": wl.name, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS, "traffic": None},
+    }))
+
+
+def bench_append(args, wl, dev, synth, kvq, configs, torch):
+    """Quantize-and-pack append of one prefill chunk (the workload's chunk
+    tokens per sequence) into an empty cache: HBM roofline.  Algorithmic
+    bytes: read the bf16 K and V once; write the codes and metadata of the
+    coded tokens and the fp16 rows of sink and window tokens."""
+    B, H, D, n = wl.B, wl.H_kv, wl.D, wl.chunk
+    K = synth.normal_bf16_device(wl.seed, "append-k", (B, n, H, D), device=dev)
+    V = synth.normal_bf16_device(wl.seed, "append-v", (B, n, H, D), device=dev)
+    cache = kvq.Cache(wl.fmt, B, H, D, n, device=dev)
+    for _ in range(args.warmup):
+        cache.reset()
+        cache.append(K, V)
+    steps = args.steps or 50
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        cache.reset()  # host-only: the next append rewrites every live byte
+        cache.append(K, V)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    f = wl.fmt
+    nq = configs.num_coded(f, n)
+    m16 = f.get("meta_fp16", 0)
+    bk = configs.coded_bytes_per_token(D, f["k_bits"], f["k_axis"], f["k_group"], f["k_mode"] == configs.AFFINE, m16)
+    bv = configs.coded_bytes_per_token(D, f["v_bits"], f["v_axis"], f["v_group"], f["v_mode"] == configs.AFFINE, m16)
+    nbytes = 2 * 2 * B * n * H * D + B * H * (nq * (bk + bv) + (n - nq) * 4 * D)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "prefill-chunk append GB/s", "value": gbs, "unit": "GB/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u%d/f16" % f["k_bits"], "data": "synthetic",
+        "config": {"workload": wl.name, "B": B, "tokens": n, "H_kv": H, "head_dim": D, "format": f},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None, "bytes_per_launch": nbytes},
     }))
 
 

@@ -169,98 +169,241 @@ __device__ void fwht_rows(float* xs, int rows, const int* use, float c)
     __syncthreads();
 }
 
-// Stage the block's rows of K (which = 0) or V (which = 1) as the coder sees
-// them.  Row i is token tb + i; rows outside [q0, q1) are zero.
-template <int D>
-__device__ void stage_rows(const AppendParams& p, int which, int b, int h, int tb, float* xs, int* from_input)
+// Statistics of one per-token group held by `lanes` consecutive lanes,
+// eight values each (lanes = group size / 8: a power of two, at most 32, so
+// a group never straddles a wave).  min, max and max-magnitude are exact in
+// any order, so the shuffle tree gives the serial loop's values.
+__device__ __forceinline__ void piece_group_stats(const float* x, int lanes, int mode, int bits, float* s_out,
+                                                  float* z_out)
 {
-    const uint16_t* in = which ? p.vin : p.kin;
-    const uint16_t* ring = which ? p.vr : p.kr;
-    for (int idx = threadIdx.x; idx < kBlockTok * D; idx += kThreads) {
-        int i = idx / D, d = idx % D, t = tb + i;
-        float v = 0.0f;
-        if (t >= p.q0 && t < p.q1) {
-            if (t >= p.n0)
-                v = bf16_to_f32(in[(((size_t)b * p.n_new + (t - p.n0)) * p.H + h) * D + d]);
-            else
-                v = f16_bits_to_f32(ring[(((size_t)b * p.H + h) * p.ring + t % p.ring) * D + d]);
+    if (mode == KVQ_AFFINE) {
+        float mn = x[0], mx = x[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) {
+            mn = fminf(mn, x[e]);
+            mx = fmaxf(mx, x[e]);
         }
-        xs[idx] = v;
-    }
-    if (threadIdx.x < kBlockTok) {
-        int t = tb + threadIdx.x;
-        from_input[threadIdx.x] = (t >= p.q0 && t < p.q1 && t >= p.n0) ? 1 : 0;
-    }
-    __syncthreads();
-    if (p.rotate)
-        fwht_rows<D>(xs, kBlockTok, from_input, p.rot_c);
-    if (p.ring) {
-        for (int idx = threadIdx.x; idx < kBlockTok * D; idx += kThreads)
-            if (from_input[idx / D])
-                xs[idx] = f16_bits_to_f32(f32_to_f16_bits(xs[idx]));
-        __syncthreads();
+        for (int off = 1; off < lanes; off <<= 1) {
+            mn = fminf(mn, __shfl_xor(mn, off));
+            mx = fmaxf(mx, __shfl_xor(mx, off));
+        }
+        const float top = (float)((1 << bits) - 1);
+        float s = (mx - mn) / top;
+        if (!(s >= 1e-8f))
+            s = 1e-8f;
+        *s_out = s;
+        *z_out = mn + 0.0f;  // canonical +0 for a signed-zero minimum
+    } else {
+        float ma = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            ma = fmaxf(ma, fabsf(x[e]));
+        for (int off = 1; off < lanes; off <<= 1)
+            ma = fmaxf(ma, __shfl_xor(ma, off));
+        const float qmax = (float)((1 << (bits - 1)) - 1);
+        float s = ma / qmax;
+        if (!(s >= 1e-8f))
+            s = 1e-8f;
+        *s_out = s;
+        *z_out = 0.0f;
     }
 }
 
+// Staging of the block's rows of K (which = 0) or V (which = 1) as the coder
+// sees them.  Row i is token tb + i; rows outside [q0, q1) are zero.  Thread
+// j moves eight channels of one row per step (one 16-byte load); the D / 8
+// threads of a row are consecutive lanes of one wave.
 template <int D>
+struct RowStage {
+    static constexpr int kSteps = kBlockTok * (D / 8) / kThreads;
+    static_assert(kSteps >= 1 && kBlockTok * (D / 8) % kThreads == 0, "uniform staging steps");
+    u32x4 w[kSteps];
+
+    __device__ static int row(int k) { return ((int)threadIdx.x + kThreads * k) / (D / 8); }
+    __device__ static int chan(int k) { return 8 * (((int)threadIdx.x + kThreads * k) % (D / 8)); }
+
+    // Issue the loads (bf16 input for tokens of this call, fp16 window slots
+    // for tokens appended earlier).
+    __device__ void load(const AppendParams& p, int which, int b, int h, int tb)
+    {
+        const uint16_t* in = which ? p.vin : p.kin;
+        const uint16_t* ring = which ? p.vr : p.kr;
+#pragma unroll
+        for (int k = 0; k < kSteps; ++k) {
+            const int t = tb + row(k), d8 = chan(k);
+            w[k] = u32x4{0u, 0u, 0u, 0u};
+            if (t >= p.q0 && t < p.q1)
+                w[k] = t >= p.n0 ? *(const u32x4*)(in + (((size_t)b * p.n_new + (t - p.n0)) * p.H + h) * D + d8)
+                                 : *(const u32x4*)(ring + (((size_t)b * p.H + h) * p.ring + t % p.ring) * D + d8);
+        }
+    }
+
+    // Widen to fp32; for tokens of this call, rotate (the butterflies of
+    // fwht_rows: half widths 1, 2, 4 inside a thread's eight values, 8 .. D/2
+    // across lanes, then one multiply by rot_c) and round to fp16 when a
+    // window exists; store() writes the rows to xs.  Every butterfly adds or
+    // subtracts the same two values as the serial transform, so results are
+    // identical.
+    __device__ void store(const AppendParams& p, int tb, float* xs) const
+    {
+#pragma unroll
+        for (int k = 0; k < kSteps; ++k) {
+            float v[8];
+            widen(p, tb, k, v);
+            float* dst = xs + row(k) * D + chan(k);
+            *(float4*)dst = make_float4(v[0], v[1], v[2], v[3]);
+            *(float4*)(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        }
+    }
+
+    // The eight values of step k as the coder sees them.
+    __device__ __forceinline__ void widen(const AppendParams& p, int tb, int k, float* v) const
+    {
+        {
+            const int t = tb + row(k);
+            const bool fresh = !(t >= p.q0 && t < p.q1) || t >= p.n0;  // bf16 (zero rows: zero words)
+            const uint32_t ww[4] = {w[k].x, w[k].y, w[k].z, w[k].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                if (fresh) {
+                    v[2 * q] = __uint_as_float(ww[q] << 16);
+                    v[2 * q + 1] = __uint_as_float(ww[q] & 0xFFFF0000u);
+                } else {
+                    v[2 * q] = f16_bits_to_f32((uint16_t)ww[q]);
+                    v[2 * q + 1] = f16_bits_to_f32((uint16_t)(ww[q] >> 16));
+                }
+            }
+            const bool input = t >= p.q0 && t < p.q1 && t >= p.n0;
+            if (p.rotate) {
+                float r[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    r[e] = v[e];
+#pragma unroll
+                for (int hw = 1; hw < 8; hw <<= 1) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        if (e & hw)
+                            continue;
+                        const float a = r[e], c = r[e + hw];
+                        r[e] = a + c;
+                        r[e + hw] = a - c;
+                    }
+                }
+                const int lane_bits = chan(k) >> 3;  // this thread's piece index within the row
+#pragma unroll
+                for (int hl = 1; hl < D / 8; hl <<= 1) {
+                    const bool upper = (lane_bits & hl) != 0;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float other = __shfl_xor(r[e], hl);
+                        r[e] = upper ? other - r[e] : r[e] + other;
+                    }
+                }
+                if (input) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        v[e] = r[e] * p.rot_c;
+                }
+            }
+            if (p.ring && input) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    v[e] = f16_bits_to_f32(f32_to_f16_bits(v[e]));
+            }
+        }
+    }
+};
+
+// 16-byte copy of `bytes` (a multiple of 16) from LDS to global memory.
+__device__ __forceinline__ void copy_out(const uint8_t* src, uint8_t* dst, int bytes)
+{
+    for (int off = 16 * (int)threadIdx.x; off < bytes; off += 16 * kThreads)
+        *(u32x4*)(dst + off) = *(const u32x4*)(src + off);
+}
+
+// One workgroup per (32-token block, sequence and KV head).  Per-token
+// groups: each thread takes the eight channels of one piece, the group's
+// statistics are reduced across the group's lanes, and the thread codes its
+// piece (keys: a piece as is; values: bytes, then packed along tokens).
+// Per-channel keys: one thread per channel over the block.  A block that
+// this call writes whole is assembled in LDS and stored with contiguous
+// 16-byte stores (each section holds a block's bytes as one range); a block
+// shared with earlier or later calls is written piece by piece.
+template <int D, bool PERCH>
 __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
 {
-    __shared__ float xs[kBlockTok * D];
-    __shared__ float ms[kBlockTok * 8 > D ? kBlockTok * 8 : D];
-    __shared__ float mz[kBlockTok * 8 > D ? kBlockTok * 8 : D];
-    __shared__ int from_input[kBlockTok];
+    __shared__ __attribute__((aligned(16))) float xs[PERCH ? kBlockTok * D : 4];  // per-channel keys only
+    __shared__ __attribute__((aligned(16))) uint8_t vcode[kBlockTok * D];  // value codes [token][D]
+    __shared__ __attribute__((aligned(16))) uint8_t ob[kBlockTok * D];     // a block's pieces (<= 8-bit codes)
+    __shared__ __attribute__((aligned(16))) float mb[2][kBlockTok * 8];    // its scales, offsets (<= 1 KB each)
+    __shared__ float ms[D];
+    __shared__ float mz[D];
+    static_assert(kBlockTok * 8 >= D, "per-channel metadata fits the staging buffer");
 
     const int unit = blockIdx.y;
     const int b = unit / p.H, h = unit % p.H;
     const int tb = (p.q0 / kBlockTok + (int)blockIdx.x) * kBlockTok;
     const int lo = max(p.q0, tb), hi = min(p.q1, tb + kBlockTok);
+    const bool full = lo == tb && hi == tb + kBlockTok;
     const size_t bh = (size_t)unit;
+    const int msz = p.meta16 ? 2 : 4;
 
     // ------------------------------------------------------------ keys
     const size_t blk = bh * (size_t)(p.T / kBlockTok) + (size_t)(tb / kBlockTok);
-    stage_rows<D>(p, 0, b, h, tb, xs, from_input);
+    RowStage<D> kst, vst;
+    kst.load(p, 0, b, h, tb);
+    vst.load(p, 1, b, h, tb);  // in flight while the keys are coded
+    if constexpr (PERCH) {
+        kst.store(p, tb, xs);
+        __syncthreads();
+    }
     const int kb = p.k_bits;
     constexpr int PPT = D / 8;  // pieces per token
-    if (p.k_axis == KVQ_PER_TOKEN) {
-        const int ng = D / p.k_group;
-        for (int idx = threadIdx.x; idx < kBlockTok * ng; idx += kThreads) {
-            int i = idx / ng, gi = idx % ng, t = tb + i;
-            if (t < lo || t >= hi)
-                continue;
+    float* kss = full ? mb[0] : p.ks;  // where scales and offsets go, and their block base
+    float* kzs = full ? mb[1] : p.kz;
+    void* kcs = full ? (void*)ob : (void*)p.kc;
+    const size_t kcb = full ? 0 : blk;
+    int kmeta;  // metadata elements per block
+    if constexpr (!PERCH) {
+        const int lanes = p.k_group / 8, ng = D / p.k_group;
+        kmeta = ng * kBlockTok;
+        const size_t mbase = full ? 0 : blk * (size_t)kmeta;
+#pragma unroll
+        for (int k = 0; k < RowStage<D>::kSteps; ++k) {
+            const int i = RowStage<D>::row(k), P = RowStage<D>::chan(k) / 8, t = tb + i;
+            float x[8];
+            kst.widen(p, tb, k, x);
             float s, z;
-            group_stats(xs + i * D + gi * p.k_group, 1, p.k_group, p.k_mode, kb, &s, &z);
+            piece_group_stats(x, lanes, p.k_mode, kb, &s, &z);
             round_meta(p.meta16, &s, &z);
-            ms[idx] = s;
-            mz[idx] = z;
-            size_t mi = (blk * ng + gi) * kBlockTok + i;
-            store_meta(p.ks, mi, s, p.meta16);
-            if (p.k_mode == KVQ_AFFINE)
-                store_meta(p.kz, mi, z, p.meta16);
-        }
-        __syncthreads();
-        for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
-            int i = idx / PPT, P = idx % PPT, t = tb + i;
             if (t < lo || t >= hi)
                 continue;
-            int gi = (8 * P) / p.k_group;
-            float s = ms[i * ng + gi], z = mz[i * ng + gi];
+            if (P % lanes == 0) {
+                const size_t mi = mbase + (size_t)(P / lanes) * kBlockTok + i;
+                store_meta(kss, mi, s, p.meta16);
+                if (p.k_mode == KVQ_AFFINE)
+                    store_meta(kzs, mi, z, p.meta16);
+            }
             uint64_t word = 0;
+#pragma unroll
             for (int e = 0; e < 8; ++e)
-                word |= (uint64_t)code_one(xs[i * D + 8 * P + e], s, z, p.k_mode, kb) << (kb * e);
-            store_piece(p.kc, key_piece<D>(blk, i, P), kb, word);
+                word |= (uint64_t)code_one(x[e], s, z, p.k_mode, kb) << (kb * e);
+            store_piece(kcs, key_piece<D>(kcb, i, P), kb, word);
         }
     } else {
         // Per-channel keys: the block is one whole 32-token group.
+        kmeta = D;
+        const size_t mbase = full ? 0 : blk * (size_t)D;
         for (int d = threadIdx.x; d < D; d += kThreads) {
             float s, z;
             group_stats(xs + d, D, kBlockTok, p.k_mode, kb, &s, &z);
             round_meta(p.meta16, &s, &z);
             ms[d] = s;
             mz[d] = z;
-            size_t mi = blk * D + d;
-            store_meta(p.ks, mi, s, p.meta16);
+            store_meta(kss, mbase + d, s, p.meta16);
             if (p.k_mode == KVQ_AFFINE)
-                store_meta(p.kz, mi, z, p.meta16);
+                store_meta(kzs, mbase + d, z, p.meta16);
         }
         __syncthreads();
         for (int idx = threadIdx.x; idx < kBlockTok * PPT; idx += kThreads) {
@@ -270,27 +413,46 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
                 int d = 8 * P + e;
                 word |= (uint64_t)code_one(xs[i * D + d], ms[d], mz[d], p.k_mode, kb) << (kb * e);
             }
-            store_piece(p.kc, key_piece<D>(blk, i, P), kb, word);
+            store_piece(kcs, key_piece<D>(kcb, i, P), kb, word);
         }
     }
     __syncthreads();
+    if (full) {
+        copy_out(ob, (uint8_t*)p.kc + blk * (size_t)(4 * D * kb), 4 * D * kb);
+        copy_out((const uint8_t*)mb[0], (uint8_t*)p.ks + blk * (size_t)(kmeta * msz), kmeta * msz);
+        if (p.k_mode == KVQ_AFFINE)
+            copy_out((const uint8_t*)mb[1], (uint8_t*)p.kz + blk * (size_t)(kmeta * msz), kmeta * msz);
+    }
 
     // ---------------------------------------------------------- values
-    stage_rows<D>(p, 1, b, h, tb, xs, from_input);
-    const int vb = p.v_bits, ng = D / p.v_group;
-    for (int idx = threadIdx.x; idx < kBlockTok * ng; idx += kThreads) {
-        int i = idx / ng, gi = idx % ng, t = tb + i;
-        if (t < lo || t >= hi)
-            continue;
-        float s, z;
-        group_stats(xs + i * D + gi * p.v_group, 1, p.v_group, p.v_mode, vb, &s, &z);
-        round_meta(p.meta16, &s, &z);
-        ms[idx] = s;
-        mz[idx] = z;
-        size_t mi = (blk * ng + gi) * kBlockTok + i;
-        store_meta(p.vs, mi, s, p.meta16);
-        if (p.v_mode == KVQ_AFFINE)
-            store_meta(p.vz, mi, z, p.meta16);
+    __syncthreads();  // the key copies have read ob and mb
+    const int vb = p.v_bits;
+    const int vlanes = p.v_group / 8, vmeta = (D / p.v_group) * kBlockTok;
+    {
+        float* vss = full ? mb[0] : p.vs;
+        float* vzs = full ? mb[1] : p.vz;
+        const size_t mbase = full ? 0 : blk * (size_t)vmeta;
+#pragma unroll
+        for (int k = 0; k < RowStage<D>::kSteps; ++k) {
+            const int i = RowStage<D>::row(k), P = RowStage<D>::chan(k) / 8, t = tb + i;
+            float x[8];
+            vst.widen(p, tb, k, x);
+            float s, z;
+            piece_group_stats(x, vlanes, p.v_mode, vb, &s, &z);
+            round_meta(p.meta16, &s, &z);
+            if (t >= lo && t < hi && P % vlanes == 0) {
+                const size_t mi = mbase + (size_t)(P / vlanes) * kBlockTok + i;
+                store_meta(vss, mi, s, p.meta16);
+                if (p.v_mode == KVQ_AFFINE)
+                    store_meta(vzs, mi, z, p.meta16);
+            }
+            uint32_t c[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                c[e] = code_one(x[e], s, z, p.v_mode, vb);
+            *(uint2*)(vcode + i * D + 8 * P) =
+                make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24), c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
+        }
     }
     __syncthreads();
     for (int idx = threadIdx.x; idx < (kBlockTok / 8) * D; idx += kThreads) {
@@ -298,22 +460,28 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
         int tfirst = tb + 8 * o;
         if (tfirst + 8 <= lo || tfirst >= hi)
             continue;
-        const size_t pi = value_piece<D>(blk, o, d);
         uint64_t word = 0;
-        if (tfirst < lo) {  // keep the bits of tokens appended earlier
+        if (tfirst < lo) {  // keep the bits of tokens appended earlier (never in a full block)
             int keep_n = lo - tfirst;
-            word = load_piece(p.vc, pi, vb) & low_codes(vb, keep_n);
+            word = load_piece(p.vc, value_piece<D>(blk, o, d), vb) & low_codes(vb, keep_n);
         }
-        int gi = d / p.v_group;
         for (int e = 0; e < 8; ++e) {
             int t = tfirst + e;
             if (t < lo || t >= hi)
                 continue;
-            int i = t - tb;
-            word |= (uint64_t)code_one(xs[i * D + d], ms[i * ng + gi], mz[i * ng + gi], p.v_mode, vb)
-                    << (vb * e);
+            word |= (uint64_t)vcode[(t - tb) * D + d] << (vb * e);
         }
-        store_piece(p.vc, pi, vb, word);
+        if (full)
+            store_piece(ob, value_piece<D>(0, o, d), vb, word);
+        else
+            store_piece(p.vc, value_piece<D>(blk, o, d), vb, word);
+    }
+    if (full) {
+        __syncthreads();
+        copy_out(ob, (uint8_t*)p.vc + blk * (size_t)(4 * D * vb), 4 * D * vb);
+        copy_out((const uint8_t*)mb[0], (uint8_t*)p.vs + blk * (size_t)(vmeta * msz), vmeta * msz);
+        if (p.v_mode == KVQ_AFFINE)
+            copy_out((const uint8_t*)mb[1], (uint8_t*)p.vz + blk * (size_t)(vmeta * msz), vmeta * msz);
     }
 }
 
@@ -462,8 +630,11 @@ hipError_t launch_append_d(const AppendParams& p, hipStream_t stream)
         return hipGetLastError();
     }
     if (p.q1 > p.q0) {
-        int nblk = (p.q1 + kBlockTok - 1) / kBlockTok - p.q0 / kBlockTok;
-        hipLaunchKernelGGL(append_code_kernel<D>, dim3(nblk, units), dim3(kThreads), 0, stream, p);
+        const int nblk = (p.q1 + kBlockTok - 1) / kBlockTok - p.q0 / kBlockTok;
+        if (p.k_axis == KVQ_PER_CHANNEL)
+            hipLaunchKernelGGL((append_code_kernel<D, true>), dim3(nblk, units), dim3(kThreads), 0, stream, p);
+        else
+            hipLaunchKernelGGL((append_code_kernel<D, false>), dim3(nblk, units), dim3(kThreads), 0, stream, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
