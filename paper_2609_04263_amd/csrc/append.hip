@@ -3,9 +3,11 @@
 // symmetric control, bit-packed and appended; KIVI keeps an fp16 window).
 //
 // Bit-exactness: codes and metadata must equal the CPU reference bit for
-// bit, so this file is compiled with -ffp-contract=off and the coder uses
-// exactly one IEEE binary32 operation per step: subtract, correctly rounded
-// divide, round-half-even (v_rndne_f32), clamp.  Min/max are exact.
+// bit, so this file is compiled with -ffp-contract=off and the coder takes
+// exactly the reference's IEEE binary32 steps: subtract, correctly rounded
+// divide, round half to even, clamp (the rounded quotient comes from a
+// reciprocal product wherever that provably gives the same code; see
+// rint_quotient).  Min/max are exact.
 //
 // One workgroup (256 threads) codes one aligned block of 32 tokens of one
 // (sequence, KV head): the block's K rows are staged in LDS as fp32 (rotated
@@ -72,16 +74,32 @@ __device__ __forceinline__ uint64_t low_codes(int bits, int n)
     return (1ull << (bits * n)) - 1ull;
 }
 
-__device__ __forceinline__ uint32_t code_affine(float x, float mn, float s, float top)
+// rint(fl(d / s)), the correctly rounded quotient rounded half to even,
+// with r the hardware reciprocal of s (within 1 ulp).  d r is within about
+// 1.5 2^-23 relative of d / s, so for |d / s| <= 256 (every code here) it
+// is within 2^-14 of fl(d / s); rint can differ only if that interval
+// contains a half-integer, so the exact division runs only where d r lies
+// within 2^-10 of one.
+__device__ __forceinline__ float rint_quotient(float d, float s, float r)
 {
-    float c = __builtin_rintf((x - mn) / s);
+    const float q = d * r;
+    float c = __builtin_rintf(q);
+    const float f = q - floorf(q);
+    if (fabsf(f - 0.5f) < 0x1p-10f)
+        c = __builtin_rintf(d / s);
+    return c;
+}
+
+__device__ __forceinline__ uint32_t code_affine(float x, float mn, float s, float r, float top)
+{
+    float c = rint_quotient(x - mn, s, r);
     c = fminf(fmaxf(c, 0.0f), top);
     return (uint32_t)c;
 }
 
-__device__ __forceinline__ uint32_t code_sym(float x, float s, float qmax, float half)
+__device__ __forceinline__ uint32_t code_sym(float x, float s, float r, float qmax, float half)
 {
-    float q = __builtin_rintf(x / s);
+    float q = rint_quotient(x, s, r);
     q = fminf(fmaxf(q, -qmax), qmax);
     return (uint32_t)(int)(q + half);
 }
@@ -138,11 +156,12 @@ __device__ __forceinline__ void store_meta(float* base, size_t i, float v, int m
         base[i] = v;
 }
 
-__device__ __forceinline__ uint32_t code_one(float x, float s, float z, int mode, int bits)
+// Code of x in a group with scale s (r = its hardware reciprocal) and offset z.
+__device__ __forceinline__ uint32_t code_one(float x, float s, float r, float z, int mode, int bits)
 {
     if (mode == KVQ_AFFINE)
-        return code_affine(x, z, s, (float)((1 << bits) - 1));
-    return code_sym(x, s, (float)((1 << (bits - 1)) - 1), (float)(1 << (bits - 1)));
+        return code_affine(x, z, s, r, (float)((1 << bits) - 1));
+    return code_sym(x, s, r, (float)((1 << (bits - 1)) - 1), (float)(1 << (bits - 1)));
 }
 
 // Fixed normalized Hadamard transform of `rows` rows of D fp32 values in LDS:
@@ -385,10 +404,11 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
                 if (p.k_mode == KVQ_AFFINE)
                     store_meta(kzs, mi, z, p.meta16);
             }
+            const float r = __builtin_amdgcn_rcpf(s);
             uint64_t word = 0;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                word |= (uint64_t)code_one(x[e], s, z, p.k_mode, kb) << (kb * e);
+                word |= (uint64_t)code_one(x[e], s, r, z, p.k_mode, kb) << (kb * e);
             store_piece(kcs, key_piece<D>(kcb, i, P), kb, word);
         }
     } else {
@@ -411,7 +431,8 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
             uint64_t word = 0;
             for (int e = 0; e < 8; ++e) {
                 int d = 8 * P + e;
-                word |= (uint64_t)code_one(xs[i * D + d], ms[d], mz[d], p.k_mode, kb) << (kb * e);
+                word |= (uint64_t)code_one(xs[i * D + d], ms[d], __builtin_amdgcn_rcpf(ms[d]), mz[d], p.k_mode, kb)
+                        << (kb * e);
             }
             store_piece(kcs, key_piece<D>(kcb, i, P), kb, word);
         }
@@ -446,10 +467,11 @@ __global__ __launch_bounds__(kThreads) void append_code_kernel(AppendParams p)
                 if (p.v_mode == KVQ_AFFINE)
                     store_meta(vzs, mi, z, p.meta16);
             }
+            const float r = __builtin_amdgcn_rcpf(s);
             uint32_t c[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e)
-                c[e] = code_one(x[e], s, z, p.v_mode, vb);
+                c[e] = code_one(x[e], s, r, z, p.v_mode, vb);
             *(uint2*)(vcode + i * D + 8 * P) =
                 make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24), c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
         }
@@ -566,7 +588,7 @@ __global__ __launch_bounds__(D) void append_token_kernel(AppendParams p)
             z = 0.0f;
         }
         round_meta(p.meta16, &s, &z);
-        const uint32_t c = code_one(x[w], s, z, mode, bits);
+        const uint32_t c = code_one(x[w], s, __builtin_amdgcn_rcpf(s), z, mode, bits);
         if (d % g == 0) {
             const size_t mi = (blk * ng + gi) * kBlockTok + tau;
             store_meta(w ? p.vs : p.ks, mi, s, p.meta16);

@@ -94,6 +94,27 @@ def test_append_bulk_multi_block(name):
     run_case(name, B=2, H=2, n=n, cuts=[0, n], seed=33)
 
 
+@pytest.mark.parametrize("name", ["tiny_b16", "affine2_g128", "sym4_window", "kivi", "affine8",
+                                  "tiny_meta16", "kvarn_sink"])
+def test_append_exact_rounding_ties(name):
+    """Half-integer inputs whose groups hold 0 and 15 (keys) or -7 and 7
+    (values): scales of 1 at 4 bits, so many quotients are exact ties (round
+    half to even) or fall next to one."""
+    from paper_2609_04263_amd import kvq
+    fmt, D = CASES[name]
+    B, H, n = 2, 2, 150
+    b, t, h, d = np.meshgrid(np.arange(B), np.arange(n), np.arange(H), np.arange(D), indexing="ij")
+    idx = 7 * d + 3 * t + 5 * h + 11 * b
+    K = synth.to_bf16_bits(((idx % 31) / 2.0).astype(np.float32))
+    V = synth.to_bf16_bits(((idx % 29 - 14) / 2.0).astype(np.float32))
+    ref = oracle.Cache(fmt, B, H, D, n)
+    ref.append(K, V)
+    gc = kvq.Cache(fmt, B, H, D, n)
+    for lo, hi in ((0, 1), (1, 70), (70, n)):
+        gc.append(dev_bf16(K[:, lo:hi]), dev_bf16(V[:, lo:hi]))
+    assert np.array_equal(image(gc), ref.image)
+
+
 def test_append_after_reset_rewrites_live_region():
     from paper_2609_04263_amd import kvq
     fmt, D = CASES["tiny_b16"]
