@@ -392,6 +392,13 @@ def bench_append(args, wl, dev, synth, kvq, configs, torch):
     K = synth.normal_bf16_device(wl.seed, "append-k", (B, n, H, D), device=dev)
     V = synth.normal_bf16_device(wl.seed, "append-v", (B, n, H, D), device=dev)
     cache = kvq.Cache(wl.fmt, B, H, D, n, device=dev)
+    if args.copy_probe_mb:
+        # one elementwise kernel that reads and writes exactly this many bytes
+        src = torch.empty(args.copy_probe_mb << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.add(src, 1, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         cache.reset()
         cache.append(K, V)
