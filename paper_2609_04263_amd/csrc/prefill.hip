@@ -4,9 +4,11 @@
 //
 // One workgroup per (sequence, KV head, tile of query rows); query rows are
 // the (chunk token, head of the KV group) pairs in token-major order.  Each
-// of the four waves owns 16 QN query rows; the workgroup walks the 32-token
-// key blocks up to its newest query's position:
-//   1. the block is reconstructed into LDS (all 256 threads, one eight-code
+// of the eight waves owns 16 QN query rows (the block reconstruction below
+// is shared by all of them, so a workgroup takes as many rows as the
+// registers allow: 128 / 256 / 512 at D = 256 / 128 / 64); the workgroup
+// walks the 32-token key blocks up to its newest query's position:
+//   1. the block is reconstructed into LDS (all 512 threads, one eight-code
 //      piece of K and one of V each per step) from a raw copy of its codes
 //      and metadata that was fetched into LDS while the previous block was
 //      computed (each section of the cache is blocked by 32 tokens, so a
@@ -35,7 +37,7 @@
 namespace kvq {
 namespace pre {
 
-constexpr int kWaves = 4, kThreads = 256;
+constexpr int kWaves = 8, kThreads = 512;
 
 // query rows per wave (16 QN): the accumulators take D QN / 4 registers
 template <int D>
