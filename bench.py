@@ -97,7 +97,7 @@ def main():
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
               "the decode path shards over (sequence, KV head) units with no exchange; "
-              "multi-GPU runs are not part of this build.", file=sys.stderr)
+              "multi-GPU runs are not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
