@@ -173,6 +173,22 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
                            const void* A, const void* Bm, int rank, float lora_scale, void* Q,
                            void* K, void* V, void* workspace, size_t ws_bytes, void* stream);
 
+/* Projection fused with the append of its K and V (Sec. 3 and 3.1: the new
+ * states are projected, then coded, packed and appended): the same Q as
+ * kvq_project_qkv, and the cache image kvq_append of its bf16 K and V would
+ * write, without the bf16 K and V ever reaching memory.  The rows of H are
+ * (sequence, token) pairs, sequence-major: M = B * n_new, n_new new tokens
+ * of each of the cache's B sequences.  Arguments as kvq_project_qkv, plus
+ * the cache (d_kv = H_kv * D).  Supported: M >= 256 (the tiled path), d_q
+ * and d_kv multiples of 256, n_new and the cache length multiples of 32,
+ * formats with per-token key groups and no window, rotation or sink;
+ * otherwise KVQ_ERR_FORMAT (format) or KVQ_ERR_ARG (shapes) and nothing
+ * changes.  On success the cache length grows by n_new. */
+kvq_status kvq_project_append(const void* H, int M, int d_in, const void* W, int d_q, int d_kv,
+                              const void* A, const void* Bm, int rank, float lora_scale, void* Q,
+                              kvq_cache* cache, int n_new, void* workspace, size_t ws_bytes,
+                              void* stream);
+
 /* Dense-merge deployment of the adapter (Sec. 3.4 "Deployment overhead": the
  * dense-base update can be folded into the weights, leaving the projection
  * shapes unchanged and removing the adapter branch at inference):

@@ -327,6 +327,84 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
     return kvq::launch_project(p, s) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 
+kvq_status kvq_project_append(const void* H, int M, int d_in, const void* W, int d_q, int d_kv, const void* A,
+                              const void* Bm, int rank, float lora_scale, void* Q, kvq_cache* c, int n_new,
+                              void* workspace, size_t ws_bytes, void* stream)
+{
+    if (!c || n_new < 0)
+        return KVQ_ERR_ARG;
+    const kvq_format& f = c->fmt;
+    if (f.k_axis != KVQ_PER_TOKEN || f.flush != 0 || f.rotate != 0 || f.sink != 0)
+        return KVQ_ERR_FORMAT;
+    if (M < 256 || d_in < 64 || d_in % 64 != 0 || d_q % 256 != 0 || d_kv % 256 != 0 || d_kv != c->H * c->D)
+        return KVQ_ERR_ARG;
+    if (n_new % 32 != 0 || c->n % 32 != 0 || (long long)c->B * n_new != M)
+        return KVQ_ERR_ARG;
+    if (rank < 0 || rank > 64 || !isfinite(lora_scale))
+        return KVQ_ERR_ARG;
+    if (!H || !W || !Q || !aligned16(H) || !aligned16(W) || !aligned16(Q))
+        return KVQ_ERR_ARG;
+    if (rank > 0) {
+        if (!A || !Bm || !aligned16(A) || !aligned16(Bm) || !workspace || !aligned16(workspace))
+            return KVQ_ERR_ARG;
+        if (ws_bytes < (size_t)M * 3 * rank * sizeof(float))
+            return KVQ_ERR_WORKSPACE;
+    }
+    if ((long long)c->n + n_new > c->T_max)
+        return KVQ_ERR_CAPACITY;
+    hipStream_t s = (hipStream_t)stream;
+    if (rank > 0) {
+        kvq::ProjParams a = {};
+        a.x = (const uint16_t*)H;
+        a.w = (const uint16_t*)A;
+        a.yf = (float*)workspace;
+        a.M = M;
+        a.K = d_in;
+        a.N = 3 * rank;
+        a.n1 = a.n2 = 3 * rank;
+        a.rank = 0;
+        a.scale = lora_scale;
+        if (kvq::launch_project(a, s) != hipSuccess)
+            return KVQ_ERR_DEVICE;
+    }
+    kvq::ProjParams p = {};
+    p.x = (const uint16_t*)H;
+    p.w = (const uint16_t*)W;
+    p.bm = (const uint16_t*)Bm;
+    p.t = (const float*)workspace;
+    p.y0 = (uint16_t*)Q;
+    p.M = M;
+    p.K = d_in;
+    p.N = d_q + 2 * d_kv;
+    p.n1 = d_q;
+    p.n2 = d_q + d_kv;
+    p.rank = rank;
+    p.scale = 1.0f;
+    p.fuse = 1;
+    p.kc = at<uint32_t>(c, 0);
+    p.ks = at<float>(c, 1);
+    p.kz = at<float>(c, 2);
+    p.vc = at<uint32_t>(c, 3);
+    p.vs = at<float>(c, 4);
+    p.vz = at<float>(c, 5);
+    p.cH = c->H;
+    p.cD = c->D;
+    p.cT = c->T_alloc;
+    p.cn0 = c->n;
+    p.cn_new = n_new;
+    p.k_bits = f.k_bits;
+    p.v_bits = f.v_bits;
+    p.k_mode = f.k_mode;
+    p.v_mode = f.v_mode;
+    p.k_group = f.k_group;
+    p.v_group = f.v_group;
+    p.meta16 = f.meta_fp16;
+    if (kvq::launch_project(p, s) != hipSuccess)
+        return KVQ_ERR_DEVICE;
+    c->n += n_new;
+    return KVQ_OK;
+}
+
 kvq_status kvq_merge_adapter(const void* W, int d_in, int d_q, int d_kv, const void* A, const void* Bm, int rank,
                              float lora_scale, void* Wout, void* stream)
 {

@@ -69,6 +69,19 @@ struct ProjParams {
     int rank;
     float scale;          // multiplies the fp32 output (activation pass); the adapter scale (fused path)
     int nxcd;             // XCDs the large-M tile order spreads over (set at launch)
+    // Fused append (large-M path only): with fuse set, the K and V tiles are
+    // coded into the cache instead of stored.  Rows are (sequence, token)
+    // pairs, cn_new tokens per sequence starting at cache position cn0 (a
+    // multiple of 32); per-token groups, no window, rotation or sink.
+    int fuse;
+    uint32_t* kc;
+    float* ks;
+    float* kz;
+    uint32_t* vc;
+    float* vs;
+    float* vz;
+    int cH, cD, cT, cn0, cn_new;  // KV heads, head size, T_alloc, first position, tokens per sequence
+    int k_bits, v_bits, k_mode, v_mode, k_group, v_group, meta16;
 };
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
 

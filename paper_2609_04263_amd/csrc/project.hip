@@ -18,6 +18,7 @@
 
 #include <atomic>
 
+#include "coder.h"
 #include "kvq_device.h"
 #include "kvq_internal.h"
 
@@ -485,6 +486,86 @@ __device__ __forceinline__ int gemm_swz(int row)
     return (row & 7) ^ ((row >> 3) & 1);
 }
 
+// Fused append of one 32-row slice pair of a K or V tile (the tile's two
+// row halves, rows m0 + 128 h + 32 mi .. + 31, 256 columns, fp32 in the four
+// waves' LDS regions): the outputs are rounded to bf16 as the unfused path
+// stores them and coded as the append kernel codes them (per-token groups:
+// statistics reduced over the group's lanes, one piece per thread); key
+// pieces and metadata go straight to the cache, value codes through LDS to
+// be packed along tokens.  A slice is 32 tokens of one sequence starting on
+// a cache block.
+__device__ void fused_code_slices(const ProjParams& p, uint8_t* glds, int m0, int n0, int mi, int tid)
+{
+    const bool isv = n0 >= p.n2;
+    const int col0 = n0 - (isv ? p.n2 : p.n1);
+    const int D = p.cD, NB = p.cT / 32;
+    const int bits = isv ? p.v_bits : p.k_bits, mode = isv ? p.v_mode : p.k_mode;
+    const int g = isv ? p.v_group : p.k_group, lanes = g / 8, ng = D / g;
+    float* sdst = isv ? p.vs : p.ks;
+    float* zdst = isv ? p.vz : p.kz;
+    uint8_t* vcode = glds + 4 * 32 * 128 * sizeof(float);  // [2][32][256] value codes
+    for (int step = 0; step < 8; ++step) {
+        const int idx = tid + kThreads * step;
+        const int hh = idx >> 10, i = (idx >> 5) & 31, P = idx & 31;
+        const float* src = (const float*)glds + (2 * hh + (P >> 4)) * (32 * 128) + i * 128 + 8 * (P & 15);
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            x[e] = bf16_to_f32(f32_to_bf16(src[e]));
+        float s, z;
+        piece_group_stats(x, lanes, mode, bits, &s, &z);
+        round_meta(p.meta16, &s, &z);
+        const int m = m0 + 128 * hh + 32 * mi + i;
+        if (m >= p.M)
+            continue;
+        const int t = p.cn0 + m % p.cn_new, tau = t & 31;
+        const int kvc = col0 + 8 * P, h = kvc / D, Ph = (kvc % D) / 8;
+        const size_t blk = ((size_t)(m / p.cn_new) * p.cH + h) * NB + t / 32;
+        if (Ph % lanes == 0) {
+            const size_t mi_ = (blk * ng + Ph / lanes) * 32 + tau;
+            store_meta(sdst, mi_, s, p.meta16);
+            if (mode == KVQ_AFFINE)
+                store_meta(zdst, mi_, z, p.meta16);
+        }
+        const float r = __builtin_amdgcn_rcpf(s);
+        uint32_t c[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            c[e] = code_one(x[e], s, r, z, mode, bits);
+        if (!isv) {
+            uint64_t word = 0;
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                word |= (uint64_t)c[e] << (bits * e);
+            const int row = 4 * (tau >> 3) + (tau & 3), half = (tau >> 2) & 1;
+            store_piece(p.kc, ((blk * 2 + half) * 64 + row + 16 * (Ph & 3)) * (size_t)(D / 32) + (Ph >> 2), bits,
+                        word);
+        } else {
+            *(uint2*)(vcode + (hh * 32 + i) * 256 + 8 * P) =
+                make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24), c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
+        }
+    }
+    if (!isv)
+        return;
+    __syncthreads();
+    // value pieces (octet o, column c): eight tokens of one channel
+    for (int step = 0; step < 8; ++step) {
+        const int idx = tid + kThreads * step;
+        const int hh = idx >> 10, o = (idx >> 8) & 3, cc = idx & 255;
+        const int m = m0 + 128 * hh + 32 * mi + 8 * o;
+        if (m >= p.M)
+            continue;
+        uint64_t word = 0;
+        for (int e = 0; e < 8; ++e)
+            word |= (uint64_t)vcode[(hh * 32 + 8 * o + e) * 256 + cc] << (bits * e);
+        const int t = p.cn0 + m % p.cn_new;
+        const int kvc = col0 + cc, h = kvc / D, d = kvc % D;
+        const size_t blk = ((size_t)(m / p.cn_new) * p.cH + h) * NB + t / 32;
+        store_piece(p.vc, (blk * 64 + (d & 15) + 16 * ((t & 31) >> 3)) * (size_t)(D / 16) + (d >> 4), bits, word);
+    }
+}
+
+template <bool FUSE>
 __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
 {
     extern __shared__ __attribute__((aligned(16))) uint8_t glds[];
@@ -692,6 +773,7 @@ __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
     const int ywidth = proj == 0 ? p.n1 : proj == 1 ? p.n2 - p.n1 : p.N - p.n2;
     const int ycol = cpair - (proj == 0 ? 0 : proj == 1 ? p.n1 : p.n2);
     (void)rn0;
+    const bool code_tile = FUSE && n0 >= p.n1;  // K and V tiles (tiles never straddle Q/K/V here)
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi) {
         __syncthreads();  // the previous slice's reads (or the last stage's) are done
@@ -701,6 +783,10 @@ __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
             for (int e = 0; e < 16; ++e)
                 xo[(8 * (e >> 2) + 4 * fk + (e & 3)) * 128 + 32 * ni + fr] = acc[mi][ni][e];
         __syncthreads();
+        if (code_tile) {
+            fused_code_slices(p, glds, m0, n0, mi, tid);
+            continue;
+        }
         const int mrow0 = m0 + wm * 128 + 32 * mi;
         for (int r = 0; r < 32; ++r) {
             const int m = mrow0 + r;
@@ -742,7 +828,10 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
         ProjParams q = p;
         q.nxcd = gemm_xcds();
         const int per = (tiles + q.nxcd - 1) / q.nxcd;
-        hipLaunchKernelGGL(proj_gemm_kernel, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
+        if (q.fuse)
+            hipLaunchKernelGGL(proj_gemm_kernel<true>, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
+        else
+            hipLaunchKernelGGL(proj_gemm_kernel<false>, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
     } else {
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + kBM - 1) / kBM);
         hipLaunchKernelGGL(proj_big_kernel, grid, dim3(kThreads), 0, stream, p);

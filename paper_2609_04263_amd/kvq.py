@@ -59,6 +59,7 @@ def _load() -> C.CDLL:
     L.kvq_project_workspace_bytes.argtypes = [I, I, C.POINTER(S)]
     L.kvq_project_qkv.argtypes = [P, I, I, P, I, I, P, P, I, C.c_float, P, P, P, P, S, P]
     L.kvq_merge_adapter.argtypes = [P, I, I, I, P, P, I, C.c_float, P, P]
+    L.kvq_project_append.argtypes = [P, I, I, P, I, I, P, P, I, C.c_float, P, P, I, P, S, P]
     L.kvq_append.argtypes = [P, P, P, I, Fp, P]
     L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
@@ -73,7 +74,7 @@ def _load() -> C.CDLL:
 _lib = _load()
 EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
             "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
-            "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_merge_adapter", "kvq_append",
+            "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
             "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_prefill_attn")
 
 
@@ -217,6 +218,18 @@ def project_qkv(H, W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, 
                               _ptr(Q), _ptr(K), _ptr(V), _ptr(workspace), nbytes, _stream(stream))
     if st:
         _check(st, "project_qkv")
+
+
+def project_append(H, W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, Q, cache: "Cache",
+                   n_new: int, workspace, stream=None) -> None:
+    """Q (bf16) as project_qkv; K and V coded straight into `cache` (n_new
+    tokens of each sequence, rows of H sequence-major)."""
+    M, d_in = H.shape[0], H.shape[-1]
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _lib.kvq_project_append(_ptr(H), M, d_in, _ptr(W), d_q, d_kv, _ptr(A), _ptr(Bm), rank, lora_scale,
+                                 _ptr(Q), cache.handle, n_new, _ptr(workspace), nbytes, _stream(stream))
+    if st:
+        _check(st, "project_append")
 
 
 def merge_adapter(W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, Wout, stream=None) -> None:

@@ -140,6 +140,30 @@ def test_prefill_argument_checks(kvq):
     assert e.value.status == kvq.ERR_ARG
 
 
+def test_project_append_argument_checks(kvq):
+    f = configs.make_format()
+    B, H, D, T = 2, 4, 64, 512
+    c = kvq.Cache(f, B, H, D, T, storage=FakeStorage(kvq.cache_bytes(f, B, H, D, T)))
+    t = FakeStorage(0, FAKE)
+    args = dict(d_in=256, d_q=512, d_kv=256, rank=0, n_new=128)
+
+    def call(cache=c, M=None, **kw):
+        a = dict(args, **kw)
+        M = B * a["n_new"] if M is None else M
+        return kvq.lib().kvq_project_append(FAKE, M, a["d_in"], FAKE, a["d_q"], a["d_kv"], FAKE, FAKE, a["rank"],
+                                            2.0, FAKE, cache.handle, a["n_new"], FAKE, 1 << 20, None)
+    assert call(n_new=100) == kvq.ERR_ARG              # tokens not a multiple of 32
+    assert call(n_new=64) == kvq.ERR_ARG               # M = 128 < 256
+    assert call(M=2 * 128 + 32) == kvq.ERR_ARG          # M != B n_new
+    assert call(d_q=384) == kvq.ERR_ARG                 # d_q not a multiple of 256
+    assert call(d_kv=512) == kvq.ERR_ARG                # d_kv != H D
+    assert call(n_new=544) == kvq.ERR_CAPACITY          # 544 > T (checked after the shapes)
+    for bad in (configs.WORKLOADS["llama8b_kivi"].fmt, configs.make_format(rotate=64), configs.make_format(sink=32)):
+        cb = kvq.Cache(bad, B, H, D, T, storage=FakeStorage(kvq.cache_bytes(bad, B, H, D, T)))
+        assert call(cache=cb) == kvq.ERR_FORMAT
+    assert c.length() == (0, 0)
+
+
 def test_rewind_only_without_window(kvq):
     f = configs.WORKLOADS["llama8b_kivi"].fmt
     c = kvq.Cache(f, 1, 1, 128, 64, storage=FakeStorage(kvq.cache_bytes(f, 1, 1, 128, 64)))
