@@ -21,6 +21,7 @@ the CPU oracle (single thread) on a bounded sample of decode steps.
   python bench.py --phase merge [--workload llama8b_had]    (dense adapter merge, HBM roofline)
   python bench.py --phase prefill_attn [--workload gqa12b_b8] (chunked prefill attention, MFMA roofline)
   python bench.py --phase append [--workload gqa12b_b8]     (one prefill chunk appended, HBM roofline)
+  python bench.py --phase project_append [--workload gqa12b_b8] (projection fused with the append, MFMA roofline)
 """
 from __future__ import annotations
 
@@ -47,7 +48,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's decode steps)")
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn", "append"], default="decode")
+    ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn", "append", "project_append"],
+                    default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--meta-fp16", action="store_true",
                     help="store scales and offsets as fp16 (the paper's storage) instead of the workload's fp32")
@@ -138,6 +140,8 @@ def main():
         return bench_merge(args, wl, W, A, Bm, kvq, torch)
     if args.phase == "append":
         return bench_append(args, wl, dev, synth, kvq, configs, torch)
+    if args.phase == "project_append":
+        return bench_project_append(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch)
 
     # ---------------------------------------------------------------- setup
     T_max = wl.context + wl.decode_steps
@@ -316,6 +320,54 @@ def bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torc
         "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": wl.name, "M": M, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
+        "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tflops / BF16_PEAK_TFLOPS, "traffic": None},
+    }))
+
+
+def bench_project_append(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch):
+    """One prefill chunk projected and appended, fused (kvq_project_append)
+    against the two calls it replaces (project_qkv, then append of its bf16
+    K and V): MFMA roofline on the projection's flops."""
+    B, n = wl.B, wl.chunk
+    M = B * n
+    Q, K, V, ws = alloc_proj(M)
+    H = synth.normal_bf16_device(wl.seed, "prefill-bench", (M, wl.d_in), device=dev)
+    cache = kvq.Cache(wl.fmt, B, wl.H_kv, wl.D, n, device=dev)
+    steps = args.steps or 20
+
+    def fused():
+        cache.reset()
+        kvq.project_append(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Q, cache, n, ws)
+
+    def unfused():
+        cache.reset()
+        kvq.project_qkv(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Q, K, V, ws)
+        cache.append(K.view(B, n, wl.H_kv, wl.D), V.view(B, n, wl.H_kv, wl.D))
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(steps):
+            fn()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / steps
+
+    ms_unfused = timed(unfused)
+    ms = timed(fused)
+    flops = configs.projection_flops(M, wl.d_in, wl.d_q, wl.d_kv, wl.rank)
+    tflops = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "fused projection + append (prefill chunk) TFLOP/s", "value": tflops, "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "M": M, "d_in": wl.d_in, "d_qkv": wl.d_qkv, "rank": wl.rank},
+        "unfused_ms_per_step": ms_unfused,
         "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tflops / BF16_PEAK_TFLOPS, "traffic": None},
     }))
