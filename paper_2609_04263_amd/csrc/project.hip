@@ -490,20 +490,24 @@ __device__ __forceinline__ int gemm_swz(int row)
 // row halves, rows m0 + 128 h + 32 mi .. + 31, 256 columns, fp32 in the four
 // waves' LDS regions): the outputs are rounded to bf16 as the unfused path
 // stores them and coded as the append kernel codes them (per-token groups:
-// statistics reduced over the group's lanes, one piece per thread); key
-// pieces and metadata go straight to the cache, value codes through LDS to
-// be packed along tokens.  A slice is 32 tokens of one sequence starting on
-// a cache block.
+// statistics reduced over the group's lanes, one piece per thread).  A
+// slice is 32 tokens of one sequence starting on a cache block, so each
+// (row half, KV head) pair is one whole cache block: its pieces and
+// metadata are assembled in LDS and written with contiguous 16-byte stores
+// (value codes pass through LDS as bytes to be packed along tokens).
 __device__ void fused_code_slices(const ProjParams& p, uint8_t* glds, int m0, int n0, int mi, int tid)
 {
     const bool isv = n0 >= p.n2;
     const int col0 = n0 - (isv ? p.n2 : p.n1);
-    const int D = p.cD, NB = p.cT / 32;
+    const int D = p.cD, NB = p.cT / 32, hpt = 256 / D;  // KV heads per tile
     const int bits = isv ? p.v_bits : p.k_bits, mode = isv ? p.v_mode : p.k_mode;
     const int g = isv ? p.v_group : p.k_group, lanes = g / 8, ng = D / g;
-    float* sdst = isv ? p.vs : p.ks;
-    float* zdst = isv ? p.vz : p.kz;
-    uint8_t* vcode = glds + 4 * 32 * 128 * sizeof(float);  // [2][32][256] value codes
+    const int msz = p.meta16 ? 2 : 4;
+    const int cbytes = 4 * D * bits, mcount = ng * 32;          // a block's code bytes, metadata elements
+    uint8_t* vcode = glds + 4 * 32 * 128 * sizeof(float);       // [2][32][256] value codes
+    uint8_t* stg = vcode + 2 * 32 * 256;                         // [2 hpt] blocks of pieces
+    float* mss = (float*)(stg + 2 * 256 * 32 * bits / 8 * 1);    // [2 hpt][mcount] scales (fp32 or fp16)
+    float* mzs = mss + 2 * 256;                                  // offsets
     for (int step = 0; step < 8; ++step) {
         const int idx = tid + kThreads * step;
         const int hh = idx >> 10, i = (idx >> 5) & 31, P = idx & 31;
@@ -515,17 +519,12 @@ __device__ void fused_code_slices(const ProjParams& p, uint8_t* glds, int m0, in
         float s, z;
         piece_group_stats(x, lanes, mode, bits, &s, &z);
         round_meta(p.meta16, &s, &z);
-        const int m = m0 + 128 * hh + 32 * mi + i;
-        if (m >= p.M)
-            continue;
-        const int t = p.cn0 + m % p.cn_new, tau = t & 31;
-        const int kvc = col0 + 8 * P, h = kvc / D, Ph = (kvc % D) / 8;
-        const size_t blk = ((size_t)(m / p.cn_new) * p.cH + h) * NB + t / 32;
+        const int hl = (8 * P) / D, Ph = ((8 * P) % D) / 8, q = hh * hpt + hl;
         if (Ph % lanes == 0) {
-            const size_t mi_ = (blk * ng + Ph / lanes) * 32 + tau;
-            store_meta(sdst, mi_, s, p.meta16);
+            const int mi_ = (Ph / lanes) * 32 + i;
+            store_meta(mss + (p.meta16 ? q * mcount / 2 : q * mcount), mi_, s, p.meta16);
             if (mode == KVQ_AFFINE)
-                store_meta(zdst, mi_, z, p.meta16);
+                store_meta(mzs + (p.meta16 ? q * mcount / 2 : q * mcount), mi_, z, p.meta16);
         }
         const float r = __builtin_amdgcn_rcpf(s);
         uint32_t c[8];
@@ -537,31 +536,49 @@ __device__ void fused_code_slices(const ProjParams& p, uint8_t* glds, int m0, in
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 word |= (uint64_t)c[e] << (bits * e);
-            const int row = 4 * (tau >> 3) + (tau & 3), half = (tau >> 2) & 1;
-            store_piece(p.kc, ((blk * 2 + half) * 64 + row + 16 * (Ph & 3)) * (size_t)(D / 32) + (Ph >> 2), bits,
-                        word);
+            const int row = 4 * (i >> 3) + (i & 3), half = (i >> 2) & 1;
+            store_piece(stg + q * cbytes, (half * 64 + row + 16 * (Ph & 3)) * (D / 32) + (Ph >> 2), bits, word);
         } else {
             *(uint2*)(vcode + (hh * 32 + i) * 256 + 8 * P) =
                 make_uint2(c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24), c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
         }
     }
-    if (!isv)
-        return;
     __syncthreads();
-    // value pieces (octet o, column c): eight tokens of one channel
-    for (int step = 0; step < 8; ++step) {
-        const int idx = tid + kThreads * step;
-        const int hh = idx >> 10, o = (idx >> 8) & 3, cc = idx & 255;
-        const int m = m0 + 128 * hh + 32 * mi + 8 * o;
+    if (isv) {
+        // value pieces (octet o, column cc): eight tokens of one channel
+        for (int step = 0; step < 8; ++step) {
+            const int idx = tid + kThreads * step;
+            const int hh = idx >> 10, o = (idx >> 8) & 3, cc = idx & 255;
+            uint64_t word = 0;
+            for (int e = 0; e < 8; ++e)
+                word |= (uint64_t)vcode[(hh * 32 + 8 * o + e) * 256 + cc] << (bits * e);
+            const int hl = cc / D, d = cc % D, q = hh * hpt + hl;
+            store_piece(stg + q * cbytes, ((d & 15) + 16 * o) * (D / 16) + (d >> 4), bits, word);
+        }
+        __syncthreads();
+    }
+    // whole blocks to the cache: codes, scales, offsets
+    uint8_t* cdst = (uint8_t*)(isv ? (void*)p.vc : (void*)p.kc);
+    uint8_t* sdst = (uint8_t*)(isv ? p.vs : p.ks);
+    uint8_t* zdst = (uint8_t*)(isv ? p.vz : p.kz);
+    for (int q = 0; q < 2 * hpt; ++q) {
+        const int hh = q / hpt, hl = q % hpt;
+        const int m = m0 + 128 * hh + 32 * mi;
         if (m >= p.M)
             continue;
-        uint64_t word = 0;
-        for (int e = 0; e < 8; ++e)
-            word |= (uint64_t)vcode[(hh * 32 + 8 * o + e) * 256 + cc] << (bits * e);
         const int t = p.cn0 + m % p.cn_new;
-        const int kvc = col0 + cc, h = kvc / D, d = kvc % D;
+        const int h = (col0 + D * hl) / D;
         const size_t blk = ((size_t)(m / p.cn_new) * p.cH + h) * NB + t / 32;
-        store_piece(p.vc, (blk * 64 + (d & 15) + 16 * ((t & 31) >> 3)) * (size_t)(D / 16) + (d >> 4), bits, word);
+        for (int off = 16 * tid; off < cbytes; off += 16 * kThreads)
+            *(u32x4*)(cdst + blk * cbytes + off) = *(const u32x4*)(stg + q * cbytes + off);
+        const int mbytes = mcount * msz;
+        const uint8_t* ms_ = (const uint8_t*)mss + q * mbytes;
+        const uint8_t* mz_ = (const uint8_t*)mzs + q * mbytes;
+        for (int off = 16 * tid; off < mbytes; off += 16 * kThreads) {
+            *(u32x4*)(sdst + blk * mbytes + off) = *(const u32x4*)(ms_ + off);
+            if (mode == KVQ_AFFINE)
+                *(u32x4*)(zdst + blk * mbytes + off) = *(const u32x4*)(mz_ + off);
+        }
     }
 }
 
