@@ -9,14 +9,27 @@ The cache is first filled to the workload's context with the same kernels
 (prefill projection in chunks, then append).  Inputs are synthetic, seeded
 and resident in HBM before the timed region.
 
-Output: one JSON line.  ``value`` is decoded tokens per second (B tokens per
-step).  ``roofline`` reports the decode-attention kernel: algorithmic bytes
-per launch (packed codes + fp32 metadata + fp16 window + bf16 q + fp32 o)
-over its mean duration, measured with HIP events around each launch inside
-the timed region, against MI355X's 8 TB/s HBM peak.  ``cpu_baseline`` times
-the CPU oracle (single thread) on a bounded sample of decode steps.
+Timing (HIP events on the launch stream):
+  cold   the K timed steps run one after another, each preceded -- outside
+         its own events -- by a 1 GiB write that evicts the 256 MB
+         Infinity Cache (MALL) and the L2s, so every step streams its
+         weights and cache from HBM.  ``value`` is B K / (sum of the K step
+         durations) and ``roofline`` uses the attention launches of these
+         steps;
+  warm   the same K steps back to back from the same starting cache, with
+         nothing in between (the serving loop as it runs): ``warm``.
+The K steps are bracketed by a device synchronize on both sides.
 
-  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+Output: one JSON line.  ``value`` is decoded tokens per second (B tokens per
+step).  ``roofline`` reports the decode-attention launch (split + merge
+kernels): algorithmic bytes per launch (packed codes + fp32 metadata + fp16
+window + bf16 q + fp32 o) over its mean cold duration, against MI355X's
+8 TB/s HBM peak, with the measured device-to-device copy bandwidth beside
+it.  ``per_config`` repeats the measurement (fewer steps) on the other
+workloads.  ``cpu_baseline`` times the CPU oracle on a bounded sample of
+decode steps, on all host cores and on one.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline] [--no-per-config]
   python bench.py --phase prefill [--workload gqa12b_b8]   (projection GEMM, MFMA roofline)
   python bench.py --phase merge [--workload llama8b_had]    (dense adapter merge, HBM roofline)
   python bench.py --phase prefill_attn [--workload gqa12b_b8] (chunked prefill attention, MFMA roofline)
@@ -39,7 +52,9 @@ sys.path.insert(0, ROOT)
 METRIC = "packed-cache decode attn tokens/s + achieved HBM GB/s (% peak) per config"
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-DEFAULT_WORKLOAD = "tiny_b16"
+DEFAULT_WORKLOAD = "llama8b_kivi"
+FLUSH_BYTES = 1 << 30       # > 4x the 256 MB MALL
+PER_CONFIG_STEPS = 24
 
 
 def parse():
@@ -51,13 +66,17 @@ def parse():
     ap.add_argument("--phase", choices=["decode", "prefill", "merge", "prefill_attn", "append", "project_append"],
                     default="decode")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the shorter cold/warm measurement of the other workloads")
+    ap.add_argument("--no-warm", action="store_true", help="skip the back-to-back (warm) loop")
     ap.add_argument("--meta-fp16", action="store_true",
                     help="store scales and offsets as fp16 (the paper's storage) instead of the workload's fp32")
     ap.add_argument("--bits8", action="store_true",
                     help="8-bit key and value codes (the 8-bit ablation) in the workload's groups and modes")
     ap.add_argument("--sink", type=int, default=0,
                     help="keep the first SINK tokens as fp16 rows (KVarN's sink tokens; a multiple of 32)")
-    ap.add_argument("--cpu-sample-steps", type=int, default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time of the all-core oracle sample (the one-thread sample is one step)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="before the timed region, copy a buffer of this many MiB once (a kernel of known "
                          "bytes for calibrating rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
@@ -93,6 +112,17 @@ def measured_traffic(workload: str):
     return float(val.group(1))
 
 
+def with_variants(wl, args):
+    import dataclasses
+    if args.meta_fp16:
+        wl = dataclasses.replace(wl, name=wl.name + "+meta16", fmt=dict(wl.fmt, meta_fp16=1))
+    if args.bits8:
+        wl = dataclasses.replace(wl, name=wl.name + "+k8v8", fmt=dict(wl.fmt, k_bits=8, v_bits=8))
+    if args.sink:
+        wl = dataclasses.replace(wl, name=wl.name + "+sink%d" % args.sink, fmt=dict(wl.fmt, sink=args.sink))
+    return wl
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -111,43 +141,130 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
-    wl = configs.WORKLOADS[args.workload]
-    if args.meta_fp16:
-        import dataclasses
-        wl = dataclasses.replace(wl, name=wl.name + "+meta16", fmt=dict(wl.fmt, meta_fp16=1))
-    if args.bits8:
-        import dataclasses
-        wl = dataclasses.replace(wl, name=wl.name + "+k8v8", fmt=dict(wl.fmt, k_bits=8, v_bits=8))
-    if args.sink:
-        import dataclasses
-        wl = dataclasses.replace(wl, name=wl.name + "+sink%d" % args.sink, fmt=dict(wl.fmt, sink=args.sink))
-    B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
+    wl = with_variants(configs.WORKLOADS[args.workload], args)
 
     def bf16(bits):
         return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
 
-    W, A, Bm = (bf16(x) for x in synth.layer_weights(wl))
-
-    def alloc_proj(M):
+    def alloc_proj(wl, M):
         return (torch.empty((M, wl.d_q), dtype=torch.bfloat16, device=dev),
                 torch.empty((M, wl.d_kv), dtype=torch.bfloat16, device=dev),
                 torch.empty((M, wl.d_kv), dtype=torch.bfloat16, device=dev),
                 torch.empty(max(16, kvq.project_workspace_bytes(M, wl.rank)), dtype=torch.uint8, device=dev))
 
-    if args.phase == "prefill":
-        return bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch)
-    if args.phase == "merge":
-        return bench_merge(args, wl, W, A, Bm, kvq, torch)
-    if args.phase == "append":
-        return bench_append(args, wl, dev, synth, kvq, configs, torch)
-    if args.phase == "project_append":
-        return bench_project_append(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch)
+    if args.phase != "decode":
+        W, A, Bm = (bf16(x) for x in synth.layer_weights(wl))
+        ap = lambda M: alloc_proj(wl, M)
+        if args.phase == "prefill":
+            return bench_prefill(args, wl, W, A, Bm, ap, dev, synth, kvq, configs, torch)
+        if args.phase == "merge":
+            return bench_merge(args, wl, W, A, Bm, kvq, torch)
+        if args.phase == "append":
+            return bench_append(args, wl, dev, synth, kvq, configs, torch)
+        if args.phase == "project_append":
+            return bench_project_append(args, wl, W, A, Bm, ap, dev, synth, kvq, configs, torch)
+        if args.phase == "prefill_attn":
+            cache = fill_cache(wl, W, A, Bm, alloc_proj, dev, synth, kvq, torch, wl.context)
+            return bench_prefill_attn(args, wl, cache, 1.0 / float(np.sqrt(wl.D)), dev, synth, torch)
 
-    # ---------------------------------------------------------------- setup
-    T_max = wl.context + wl.decode_steps
+    flush_buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    copy_gbs = measure_copy(flush_buf, torch)
+    steps = args.steps if args.steps is not None else wl.decode_steps
+    res, state = decode_run(wl, steps, args.warmup, not args.no_warm, flush_buf, args, dev, alloc_proj, bf16,
+                            np, torch, configs, kvq, synth)
+    att = res["attention"]
+    print(f"bench: {wl.name} done: {res['tokens_per_s']:.0f} tokens/s, attention {att['us']:.1f} us "
+          f"({att['gbs']:.0f} GB/s)", file=sys.stderr, flush=True)
+    traffic = measured_traffic(wl.name)
+    result = {
+        "metric": METRIC,
+        "value": res["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u%d/f16" % wl.fmt["k_bits"],
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "H_q": wl.H_q, "H_kv": wl.H_kv, "head_dim": wl.D,
+                   "d_in": wl.d_in, "rank": wl.rank, "context": wl.context, "decode_steps": wl.decode_steps,
+                   "format": wl.fmt, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "kernel": "decode attention (split + merge), cold",
+                     "achieved": att["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": att["gbs"] / HBM_PEAK_GBS, "traffic": traffic,
+                     "bytes_per_launch": att["bytes_per_launch"], "us_per_launch": att["us"],
+                     "copy_gbs": copy_gbs, "frac_of_copy": att["gbs"] / copy_gbs},
+        "attention_us_per_step": att["us"],
+        "projection": res["projection"],
+        "warm": res.get("warm"),
+    }
+    image = None
+    if not args.no_cpu_baseline:
+        image = state["snapshot"].cpu().numpy()
+    del state
+    torch.cuda.empty_cache()
+    if not args.no_per_config:
+        per = {wl.name: summary(res)}
+        for name in configs.WORKLOAD_ORDER:
+            if name == args.workload:
+                continue
+            w2 = with_variants(configs.WORKLOADS[name], args)
+            r2, st2 = decode_run(w2, min(PER_CONFIG_STEPS, w2.decode_steps), 3, not args.no_warm, flush_buf, args,
+                                 dev, alloc_proj, bf16, np, torch, configs, kvq, synth)
+            per[w2.name] = summary(r2)
+            print(f"bench: {w2.name} done: attention {r2['attention']['us']:.1f} us "
+                  f"({r2['attention']['gbs']:.0f} GB/s)", file=sys.stderr, flush=True)
+            del st2
+            torch.cuda.empty_cache()
+        result["per_config"] = per
+    if image is not None:
+        result["cpu_baseline"] = cpu_baseline(wl, image, args, np, synth)
+        print(f"bench: cpu baseline done", file=sys.stderr, flush=True)
+    print(json.dumps(result))
+
+
+def summary(res):
+    a, p = res["attention"], res["projection"]
+    out = {"tokens_per_s": res["tokens_per_s"], "ms_per_step": res["ms_per_step"],
+           "attention_us": a["us"], "attention_gbs": a["gbs"], "attention_frac": a["gbs"] / HBM_PEAK_GBS,
+           "attention_bytes": a["bytes_per_launch"],
+           "projection_us": p["us"], "projection_gbs": p["gbs"], "projection_frac": p["gbs"] / HBM_PEAK_GBS}
+    if res.get("warm"):
+        w = res["warm"]
+        out.update({"warm_tokens_per_s": w["tokens_per_s"], "warm_attention_us": w["attention_us"],
+                    "warm_attention_gbs": w["attention_gbs"]})
+    return out
+
+
+def measure_copy(buf, torch):
+    """Device-to-device copy bandwidth (read + write bytes over time) of one
+    half of the flush buffer into the other: the K8 reference for what a
+    streaming kernel reaches on this device."""
+    half = buf.numel() // 2
+    src, dst = buf[:half], buf[half:]
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    reps = 10
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    return 2.0 * half * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+
+def fill_cache(wl, W, A, Bm, alloc_proj, dev, synth, kvq, torch, T_max):
+    """Cache filled to the workload's context by the prefill path (projection
+    of each chunk, then its append)."""
+    B, Hkv, D = wl.B, wl.H_kv, wl.D
     cache = kvq.Cache(wl.fmt, B, Hkv, D, T_max, device=dev)
     chunk = min(wl.chunk, wl.context)
-    Qp, Kp, Vp, wsp = alloc_proj(B * chunk)
+    Qp, Kp, Vp, wsp = alloc_proj(wl, B * chunk)
     done = 0
     while done < wl.context:
         c = min(chunk, wl.context - done)
@@ -156,25 +273,52 @@ def main():
                         Qp[:B * c], Kp[:B * c], Vp[:B * c], wsp)
         cache.append(Kp[:B * c].view(B, c, Hkv, D), Vp[:B * c].view(B, c, Hkv, D))
         done += c
-    del Qp, Kp, Vp, wsp
-    snapshot = cache.storage.clone() if wl.fmt["flush"] else None
+    torch.cuda.synchronize()
+    return cache
+
+
+def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, bf16, np, torch, configs, kvq,
+               synth):
+    """Fill the cache, then time `steps` decode steps cold (a MALL flush
+    before each, outside its events) and, with `with_warm`, the same steps
+    back to back.  Returns (results, objects to keep alive)."""
+    B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
+    W, A, Bm = (bf16(x) for x in synth.layer_weights(wl))
+    cache = fill_cache(wl, W, A, Bm, alloc_proj, dev, synth, kvq, torch, wl.context + wl.decode_steps)
+    snapshot = cache.storage.clone()
     Hdec = synth.normal_bf16_device(wl.seed, "decode", (wl.decode_steps, B, wl.d_in), device=dev)
-    Qd, Kd, Vd, wsd = alloc_proj(B)
+    Qd, Kd, Vd, wsd = alloc_proj(wl, B)
     O = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
     wsa = cache.decode_workspace(Hq, device=dev)
     sm = 1.0 / float(np.sqrt(D))
-    torch.cuda.synchronize()
-    if args.phase == "prefill_attn":
-        return bench_prefill_attn(args, wl, cache, sm, dev, synth, torch)
+    Kv, Vv, Qv = Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D), Qd.view(B, Hq, D)
+    Hsteps = [Hdec[i] for i in range(wl.decode_steps)]
+    flush_val = [0]
 
-    def restart(timed=False):
-        if snapshot is None:
-            cache.rewind(wl.context)          # host-only: no GPU work
-        elif timed:
-            raise RuntimeError("windowed formats restart only outside the timed region")
-        else:
-            cache.storage.copy_(snapshot)
-            cache.restore(wl.context)
+    def flush():
+        flush_val[0] = (flush_val[0] + 1) & 0xFF
+        flush_buf.fill_(flush_val[0])
+
+    def restart():
+        # outside any timed region: the storage as it was at the context length
+        cache.storage.copy_(snapshot)
+        cache.restore(wl.context)
+
+    def new_events(k):
+        return [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+
+    def step(i, ev=None):
+        if ev is not None:
+            ev[0].record()
+        kvq.project_qkv(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
+        if ev is not None:
+            ev[1].record()
+        cache.append(Kv, Vv)
+        if ev is not None:
+            ev[2].record()
+        cache.decode_attn(Qv, Hq, sm, O, wsa)
+        if ev is not None:
+            ev[3].record()
 
     if args.copy_probe_mb:
         # one elementwise kernel that reads and writes exactly this many bytes
@@ -183,92 +327,84 @@ def main():
         torch.add(src, 1, out=dst)
         torch.cuda.synchronize()
         del src, dst
-    Kv, Vv, Qv = Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D), Qd.view(B, Hq, D)
-    Hsteps = [Hdec[i] for i in range(wl.decode_steps)]
 
-    def step(i, ev=None):
-        kvq.project_qkv(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
-        cache.append(Kv, Vv)
-        if ev is not None:
-            ev[0].record()
-        cache.decode_attn(Qv, Hq, sm, O, wsa)
-        if ev is not None:
-            ev[1].record()
-
-    steps = args.steps if args.steps is not None else wl.decode_steps
-    if snapshot is not None and steps > wl.decode_steps:
-        steps = wl.decode_steps  # the fp16 window cannot be rewound in place
-    for i in range(args.warmup):
-        if i % wl.decode_steps == 0 and i:
+    # warmup: flushed like the cold steps
+    for i in range(warmup):
+        if i % wl.decode_steps == 0:
             restart()
+        flush()
         step(i % wl.decode_steps)
     torch.cuda.synchronize()
-    if snapshot is not None:
-        cache.storage.copy_(snapshot)
-        cache.restore(wl.context)
-    else:
-        cache.rewind(wl.context)
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+
+    # cold: a flush before every step, outside the step's events
+    restart()
+    evs = [new_events(4) for _ in range(steps)]
     n_at = []
     torch.cuda.synchronize()
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record()
     for i in range(steps):
         j = i % wl.decode_steps
         if j == 0 and i:
-            restart(timed=True)
+            restart()
+        flush()
         n_at.append(wl.context + j + 1)
-        step(j, events[i])
-    t1.record()
+        step(j, evs[i])
     torch.cuda.synchronize()
-    total_ms = t0.elapsed_time(t1)
-    attn_ms = np.array([a.elapsed_time(b) for a, b in events])
+    step_ms = np.array([e[0].elapsed_time(e[3]) for e in evs])
+    proj_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    attn_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
     bytes_launch = np.array([configs.attention_bytes(wl, n) for n in n_at], dtype=np.float64)
-    achieved = bytes_launch.mean() / (attn_ms.mean() * 1e-3) / 1e9
-    traffic = measured_traffic(wl.name)
-
-    result = {
-        "metric": METRIC,
-        "value": B * steps / (total_ms * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": steps,
-        "warmup": args.warmup,
-        "ms_per_step": total_ms / steps,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "u%d/f16" % wl.fmt["k_bits"],
-        "data": "synthetic",
-        "config": {"workload": wl.name, "B": B, "H_q": Hq, "H_kv": Hkv, "head_dim": D, "d_in": wl.d_in,
-                   "rank": wl.rank, "context": wl.context, "decode_steps": wl.decode_steps,
-                   "format": wl.fmt, "parallelism": "single-gpu"},
-        "roofline": {"bound": "hbm", "kernel": "decode attention", "achieved": achieved,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "bytes_per_launch": float(bytes_launch.mean()),
-                     "us_per_launch": float(attn_ms.mean() * 1e3)},
-        "attention_us_per_step": float(attn_ms.mean() * 1e3),
+    proj_bytes = configs.projection_weight_bytes(wl.d_in, wl.d_q, wl.d_kv, wl.rank) + 2 * B * (wl.d_in + wl.d_qkv)
+    res = {
+        "tokens_per_s": B * steps / (step_ms.sum() * 1e-3),
+        "ms_per_step": float(step_ms.mean()),
+        "attention": {"us": float(attn_ms.mean() * 1e3), "bytes_per_launch": float(bytes_launch.mean()),
+                      "gbs": float(bytes_launch.mean() / (attn_ms.mean() * 1e-3) / 1e9)},
+        "projection": {"us": float(proj_ms.mean() * 1e3), "bytes_per_call": int(proj_bytes),
+                       "gbs": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9),
+                       "frac": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9 / HBM_PEAK_GBS)},
     }
-    if not args.no_cpu_baseline:
-        if snapshot is None:
-            cache.rewind(wl.context)
-            torch.cuda.synchronize()
-            image = cache.storage.cpu().numpy()
-        else:
-            image = snapshot.cpu().numpy()
-        result["cpu_baseline"] = cpu_baseline(wl, image, args, np, synth)
-    print(json.dumps(result))
+    if with_warm:
+        # the same steps back to back (at most one pass over the decode
+        # inputs: the fp16 window cannot be restored inside the loop)
+        done = min(steps, wl.decode_steps)
+        restart()
+        wev = [new_events(4) for _ in range(done)]
+        torch.cuda.synchronize()
+        t0, t1 = new_events(2)
+        t0.record()
+        for i in range(done):
+            step(i, wev[i])
+        t1.record()
+        torch.cuda.synchronize()
+        warm_ms = t0.elapsed_time(t1) / done
+        wa = np.array([e[2].elapsed_time(e[3]) for e in wev])
+        res["warm"] = {"tokens_per_s": B / (warm_ms * 1e-3), "ms_per_step": warm_ms, "steps": done,
+                       "attention_us": float(wa.mean() * 1e3),
+                       "attention_gbs": float(bytes_launch[:done].mean() / (wa.mean() * 1e-3) / 1e9)}
+    restart()
+    torch.cuda.synchronize()
+    state = {"cache": cache, "snapshot": snapshot, "weights": (W, A, Bm), "inputs": Hdec, "workspace": wsa}
+    return res, state
 
 
 def cpu_baseline(wl, image, args, np, synth):
-    """The oracle (single-threaded C) on a bounded sample of the same
-    workload: starting from the GPU-filled cache image at the context length,
-    it runs S decode steps (projection of the B new tokens, append, attention
-    over all cached tokens), timed end to end.  S is chosen from a first
-    timed step so the sample takes about 15 s."""
+    """The oracle (C, OpenMP over independent units) on a bounded sample of
+    the same workload: starting from the GPU-filled cache image at the
+    context length, decode steps (projection of the B new tokens, append,
+    fp64 attention over all cached tokens), timed end to end on every core
+    this process may use, then one step on one thread."""
     import oracle
 
+    cores = len(os.sched_getaffinity(0))
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     W, A, Bm = synth.layer_weights(wl)
     ref = oracle.Cache(wl.fmt, wl.B, wl.H_kv, wl.D, wl.T_max)
     ref.image[:] = image
@@ -283,17 +419,28 @@ def cpu_baseline(wl, image, args, np, synth):
         ref.append(k, v)
         ref.decode_attn(q, 1.0 / np.sqrt(wl.D))
 
-    t = time.perf_counter()
-    one(0)
-    first = time.perf_counter() - t
-    S = args.cpu_sample_steps or int(min(max(15.0 / max(first, 1e-3), 2), wl.decode_steps))
-    t = time.perf_counter()
-    for i in range(1, S + 1):
-        one(i)
-    el = time.perf_counter() - t
-    return {"value": wl.B * S / el, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{S} decode steps of {wl.name} (B={wl.B}, from context {wl.context}): oracle projection, "
-                      f"append and fp64 attention, single thread, {el:.1f} s"}
+    before = oracle.get_threads()
+    try:
+        oracle.set_threads(cores)
+        t = time.perf_counter()
+        one(0)
+        first = time.perf_counter() - t
+        S = int(min(max(args.cpu_seconds / max(first, 1e-3), 2), wl.decode_steps - 2))
+        t = time.perf_counter()
+        for i in range(1, S + 1):
+            one(i)
+        el = time.perf_counter() - t
+        oracle.set_threads(1)
+        t = time.perf_counter()
+        one(S + 1)
+        el1 = time.perf_counter() - t
+    finally:
+        oracle.set_threads(before)
+    return {"value": wl.B * S / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu_model": model, "value_1thread": wl.B / el1,
+            "sample": f"{S} decode steps of {wl.name} (B={wl.B}, from context {wl.context}) on {cores} threads "
+                      f"({el:.1f} s), then 1 step on 1 thread ({el1:.1f} s): oracle projection (fp64), append "
+                      f"and fp64 attention over all cached tokens"}
 
 
 def bench_prefill(args, wl, W, A, Bm, alloc_proj, dev, synth, kvq, configs, torch):

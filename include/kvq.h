@@ -125,8 +125,14 @@ typedef struct kvq_cache kvq_cache;
 kvq_status kvq_cache_bytes(const kvq_format* fmt, int B, int H_kv, int D, int T_max, size_t* bytes);
 
 /* Create a handle over caller storage (at least kvq_cache_bytes bytes,
- * 256-byte aligned, ZERO-FILLED by the caller).  Host-only: enqueues nothing.
- * The cache starts empty (n = 0). */
+ * 256-byte aligned).  Host-only: enqueues nothing.  The cache starts empty
+ * (n = 0).  No result depends on what the storage holds at init: appends
+ * write every byte of a token's codes and metadata (clearing the code bits
+ * of later tokens in pieces they share), and attention masks every slot at
+ * or past the cached length, whatever it contains.  Only the bytes of dead
+ * slots do: storage zero-filled before init gives an image that is a
+ * function of the appended tokens alone (what byte-for-byte comparisons
+ * with a reference need). */
 kvq_status kvq_cache_init(const kvq_format* fmt, int B, int H_kv, int D, int T_max, void* storage,
                           size_t bytes, kvq_cache** out);
 
@@ -246,6 +252,9 @@ kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float
  * exactly as kvq_decode_attn (same head grouping, rotation and softmax).
  *   Q  bf16 [B][C][H_q][D]
  *   O  fp32 [B][C][H_q][D], normalized
+ * Reconstructed keys and values (after rotation, for a rotating format)
+ * enter the products as binary16 MFMA operands, so their magnitudes must
+ * stay below 65504 (binary16's largest finite value).
  * H_q a multiple of H_kv.  No workspace.  Pointers 16-byte aligned device
  * memory owned by the caller; invalid arguments return KVQ_ERR_ARG before
  * any launch. */

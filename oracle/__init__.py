@@ -57,7 +57,7 @@ def build(force: bool = True) -> str:
     """Compile the oracle with gcc into ``oracle/libkvq_oracle.so``."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
-        subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math",
+        subprocess.run(["gcc", "-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
                         "-Wall", "-Wextra", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"],
                        check=True)
         os.replace(tmp, _LIB)
@@ -102,6 +102,9 @@ def lib() -> C.CDLL:
         L.orc_project.argtypes = [P, C.c_int, C.c_int, P, C.c_int, C.c_int, P, P, C.c_int,
                                   C.c_double, P, P]
         L.orc_merge_adapter.argtypes = [P, C.c_int, C.c_int, C.c_int, P, P, C.c_int, C.c_double, P, P]
+        L.orc_set_threads.argtypes = [C.c_int]
+        L.orc_set_threads.restype = None
+        L.orc_get_threads.restype = C.c_int
         _lib = L
     return _lib
 
@@ -113,6 +116,18 @@ def _ptr(a: np.ndarray):
 
 def _fmt(fmt) -> _Format:
     return _Format(*[int(fmt.get(name, 0)) for name in FORMAT_FIELDS])
+
+
+# ---------------------------------------------------------------- threads
+
+def set_threads(n: int) -> None:
+    """OpenMP threads for the loops over independent units (results are the
+    same for any count)."""
+    lib().orc_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().orc_get_threads())
 
 
 # ---------------------------------------------------------------- scalars

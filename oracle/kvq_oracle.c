@@ -32,6 +32,12 @@
  * is compiled with -O2 -ffp-contract=off and no fast-math.  Projection,
  * reconstruction and attention accumulate in binary64.
  *
+ * Threads: the loops over independent units -- (sequence, KV head) pairs
+ * for append, reconstruction and attention, rows for the projection and
+ * the merge -- are shared among OpenMP threads.  Each unit is still
+ * computed by one thread in the serial order written below, so every
+ * result is the same for any thread count (orc_set_threads).
+ *
  * Storage image (the byte layout the GPU library must reproduce exactly):
  * sections Kc, Ks, Kz, Vc, Vs, Vz, Kr, Vr, Kq, Vq, each starting at a
  * multiple of 256 bytes.
@@ -81,6 +87,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <omp.h>
+
 enum {
     ORC_OK = 0,
     ORC_ERR_ARG = 1,
@@ -100,6 +108,18 @@ typedef struct {
     int meta_fp16;        /* 0: fp32 scales and offsets; 1: fp16 (the paper's storage) */
     int sink;             /* 0, or S (a multiple of 32): the first S tokens kept as fp16 */
 } orc_format;
+
+/* Threads used by the unit loops (n >= 1), and the current setting. */
+void orc_set_threads(int n)
+{
+    if (n >= 1)
+        omp_set_num_threads(n);
+}
+
+int orc_get_threads(void)
+{
+    return omp_get_max_threads();
+}
 
 /* ------------------------------------------------------------------ */
 /* Scalar number formats                                               */
@@ -672,17 +692,23 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
     const int S = f->sink, n0t = n0 - S, n1t = n1 - S;
     const int q0 = orc_num_coded(f, n0), q1 = orc_num_coded(f, n1);
     const int kb = f->k_bits, vb = f->v_bits;
+    const int m16 = f->meta_fp16;
+    int nomem = 0;
+
+    /* (b, h) units are independent: each writes only its own pieces,
+     * metadata and rows. */
+#pragma omp parallel reduction(| : nomem)
+    {
     float* x = (float*)malloc(sizeof(float) * (size_t)D * 32);
     uint8_t* codes = (uint8_t*)malloc((size_t)D * 32);
-    if (!x || !codes) {
-        free(x);
-        free(codes);
-        return ORC_ERR_NOMEM;
-    }
-    const int m16 = f->meta_fp16;
-
-    for (int b = 0; b < B; ++b) {
-        for (int h = 0; h < H; ++h) {
+    if (!x || !codes)
+        nomem = 1;
+#pragma omp for schedule(dynamic, 1)
+    for (int u = 0; u < B * H; ++u) {
+        if (!x || !codes)
+            continue;
+        const int b = u / H, h = u % H;
+        {
             /* K, groups along head_dim: each coded token on its own. */
             if (f->k_axis == 0) {
                 for (int t = q0; t < q1; ++t) {
@@ -775,6 +801,9 @@ int orc_append(const orc_format* f, int B, int H, int D, int T_max, uint8_t* ima
     }
     free(x);
     free(codes);
+    }
+    if (nomem)
+        return ORC_ERR_NOMEM;
     *n_io = n1;
     return ORC_OK;
 }
@@ -835,11 +864,11 @@ int orc_dequant(const orc_format* f, int B, int H, int D, int T_max, const uint8
         return st;
     if (n < 0 || n > T_max)
         return ORC_ERR_ARG;
-    for (int b = 0; b < B; ++b)
-        for (int h = 0; h < H; ++h) {
-            size_t o = ((size_t)b * H + h) * (size_t)n * D;
-            reconstruct_bh(&v, b, h, n, Khat + o, Vhat + o);
-        }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int u = 0; u < B * H; ++u) {
+        size_t o = (size_t)u * (size_t)n * D;
+        reconstruct_bh(&v, u / H, u % H, n, Khat + o, Vhat + o);
+    }
     return ORC_OK;
 }
 
@@ -860,20 +889,24 @@ int orc_decode_attn(const orc_format* f, int B, int H, int D, int T_max, const u
     if (n < 1 || n > T_max || H_q < H || H_q % H != 0 || !Q || !O)
         return ORC_ERR_ARG;
     const int G = H_q / H;
+    int nomem = 0;
+    /* (b, KV head) units are independent; each thread has its own buffers. */
+#pragma omp parallel reduction(| : nomem)
+    {
     double* khat = (double*)malloc(sizeof(double) * (size_t)n * D);
     double* vhat = (double*)malloc(sizeof(double) * (size_t)n * D);
     double* logit = (double*)malloc(sizeof(double) * (size_t)n);
     double* q = (double*)malloc(sizeof(double) * (size_t)D * 2);
-    if (!khat || !vhat || !logit || !q) {
-        free(khat);
-        free(vhat);
-        free(logit);
-        free(q);
-        return ORC_ERR_NOMEM;
-    }
-    double* o = q + D;
-    for (int b = 0; b < B; ++b) {
-        for (int h = 0; h < H; ++h) {
+    const int ok = khat && vhat && logit && q;
+    if (!ok)
+        nomem = 1;
+    double* o = ok ? q + D : NULL;
+#pragma omp for schedule(dynamic, 1)
+    for (int u = 0; u < B * H; ++u) {
+        if (!ok)
+            continue;
+        const int b = u / H, h = u % H;
+        {
             reconstruct_bh(&v, b, h, n, khat, vhat);
             for (int hq = h * G; hq < (h + 1) * G; ++hq) {
                 const uint16_t* qs = Q + ((size_t)b * H_q + hq) * D;
@@ -916,7 +949,8 @@ int orc_decode_attn(const orc_format* f, int B, int H, int D, int T_max, const u
     free(vhat);
     free(logit);
     free(q);
-    return ORC_OK;
+    }
+    return nomem ? ORC_ERR_NOMEM : ORC_OK;
 }
 
 /* Chunked prefill attention (Sec. 3.1: evaluation consumes chunks; the
@@ -938,20 +972,24 @@ int orc_prefill_attn(const orc_format* f, int B, int H, int D, int T_max, const 
     if (n < 1 || n > T_max || C < 1 || C > n || H_q < H || H_q % H != 0 || !Q || !O)
         return ORC_ERR_ARG;
     const int G = H_q / H;
+    int nomem = 0;
+    /* (b, KV head) units are independent; each thread has its own buffers. */
+#pragma omp parallel reduction(| : nomem)
+    {
     double* khat = (double*)malloc(sizeof(double) * (size_t)n * D);
     double* vhat = (double*)malloc(sizeof(double) * (size_t)n * D);
     double* logit = (double*)malloc(sizeof(double) * (size_t)n);
     double* q = (double*)malloc(sizeof(double) * (size_t)D * 2);
-    if (!khat || !vhat || !logit || !q) {
-        free(khat);
-        free(vhat);
-        free(logit);
-        free(q);
-        return ORC_ERR_NOMEM;
-    }
-    double* o = q + D;
-    for (int b = 0; b < B; ++b) {
-        for (int h = 0; h < H; ++h) {
+    const int ok = khat && vhat && logit && q;
+    if (!ok)
+        nomem = 1;
+    double* o = ok ? q + D : NULL;
+#pragma omp for schedule(dynamic, 1)
+    for (int u = 0; u < B * H; ++u) {
+        if (!ok)
+            continue;
+        const int b = u / H, h = u % H;
+        {
             reconstruct_bh(&v, b, h, n, khat, vhat);
             for (int i = 0; i < C; ++i) {
                 const int last = n - C + i;  /* newest token this query sees */
@@ -997,7 +1035,8 @@ int orc_prefill_attn(const orc_format* f, int B, int H, int D, int T_max, const 
     free(vhat);
     free(logit);
     free(q);
-    return ORC_OK;
+    }
+    return nomem ? ORC_ERR_NOMEM : ORC_OK;
 }
 
 /* ------------------------------------------------------------------ */
@@ -1018,14 +1057,18 @@ int orc_project(const uint16_t* Hm, int M, int d_in, const uint16_t* W, int d_q,
     if (rank > 0 && (!A || !Bm))
         return ORC_ERR_ARG;
     const int N = d_q + 2 * d_kv;
+    int nomem = 0;
+    /* rows are independent; each thread has its own buffers */
+#pragma omp parallel reduction(| : nomem)
+    {
     double* h = (double*)malloc(sizeof(double) * (size_t)d_in);
     double* t = (double*)malloc(sizeof(double) * (size_t)(3 * rank + 1));
-    if (!h || !t) {
-        free(h);
-        free(t);
-        return ORC_ERR_NOMEM;
-    }
+    if (!h || !t)
+        nomem = 1;
+#pragma omp for schedule(dynamic, 4)
     for (int m = 0; m < M; ++m) {
+        if (!h || !t)
+            continue;
         for (int i = 0; i < d_in; ++i)
             h[i] = bf16_to_f32(Hm[(size_t)m * d_in + i]);
         for (int k = 0; k < 3 * rank; ++k) {
@@ -1052,7 +1095,8 @@ int orc_project(const uint16_t* Hm, int M, int d_in, const uint16_t* W, int d_q,
     }
     free(h);
     free(t);
-    return ORC_OK;
+    }
+    return nomem ? ORC_ERR_NOMEM : ORC_OK;
 }
 
 /* ------------------------------------------------------------------ */
@@ -1073,6 +1117,7 @@ int orc_merge_adapter(const uint16_t* W, int d_in, int d_q, int d_kv, const uint
     if (rank > 0 && (!A || !Bm))
         return ORC_ERR_ARG;
     const int N = d_q + 2 * d_kv;
+#pragma omp parallel for schedule(dynamic, 16)
     for (int n = 0; n < N; ++n) {
         const int p = n < d_q ? 0 : (n < d_q + d_kv ? 1 : 2);
         for (int i = 0; i < d_in; ++i) {

@@ -479,10 +479,12 @@ struct Split {
         softmax(l);  // l now holds p (<= 2^kTau), 0 for masked tokens
 
         // ---------------------------------------------------- values
-        // Masked tokens have p = 0 and finite metadata (the storage starts
-        // zero-filled and is only ever written with finite values), so their
-        // terms vanish without a select.  With one column set per group the
-        // B operand built in the first pass holds every group.
+        // Masked tokens have p = 0.  The slots past the cached length may hold
+        // anything (storage that was never written, or left by an earlier
+        // window), so in a partial block their scales and offsets are replaced
+        // by zeros before they meet p; full blocks need no select.  With one
+        // column set per group the B operand built in the first pass holds
+        // every group.
         half8 ph, pl;
 #pragma unroll
         for (int pass = 0; pass < NVG; ++pass) {
@@ -490,8 +492,16 @@ struct Split {
                 const int g = rep ? vg : pass;
                 const float4 s0 = vs[8 * g + 2 * qg], s1 = vs[8 * g + 2 * qg + 1];
                 const float4 z0 = vz[8 * g + 2 * qg], z1 = vz[8 * g + 2 * qg + 1];
-                const float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-                const float zn[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+                float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+                float zn[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+                if (valid < 32) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const bool live = 8 * qg + k < valid;
+                        sn[k] = live ? sn[k] : 0.0f;
+                        zn[k] = live ? zn[k] : 0.0f;
+                    }
+                }
                 float pv[8];
                 float zs = 0.0f;
 #pragma unroll

@@ -82,3 +82,125 @@ def test_workspace_too_small_is_rejected():
     with pytest.raises(kvq.KvqError) as e:
         gc.decode_attn(Q, 8, 0.125, O, ws)
     assert e.value.status == kvq.ERR_WORKSPACE
+
+
+# ---------------------------------------------------------------------------
+# Workload unit counts.  The planner gives every (sequence, KV head) unit
+# about (resident workgroups) / (units) splits, and each wave of a split
+# walks every fourth 32-token block, so with many units a wave codes several
+# blocks in a row: both register sets of the load pipeline alternate, and
+# the online softmax rescales accumulators that already hold earlier blocks.
+# These cases use the workloads' unit counts (B * H_kv = 64 or 256), with
+# ragged last blocks and last splits.
+
+def run_ramped(name, B, H, G, n, seed, span):
+    """Keys get a component +-r_t on every channel (sign pattern u) and the
+    queries point along u, so each logit carries r_t sqrt(D) at the default
+    softmax scale.  r_t runs linearly over the context so that the logits
+    climb by |span| (natural-log units) from the first token to the last
+    (span > 0) or fall by it (span < 0).  With a climbing ramp every later
+    block raises the running maximum of its wave after earlier blocks were
+    accumulated (40 log2 units in all: about ten rescales past the lazy
+    threshold); with a falling one the first block holds the maximum."""
+    from paper_2609_04263_amd import kvq
+    fmt, D = CASES[name]
+    outlier = ("student_t", 3.0) if fmt["rotate"] else ("scale", 4, 20.0)
+    K, V = synth.kv_tokens(seed, B, n, H, D, outlier=outlier)
+    u = np.where(np.arange(D) % 2 == 0, 1.0, -1.0).astype(np.float32)
+    t = np.arange(n, dtype=np.float32) / np.float32(max(n - 1, 1))
+    r = (abs(span) / np.sqrt(D)) * (t if span > 0 else 1.0 - t)
+    K = synth.to_bf16_bits(synth.bf16_bits_to_f32(K) + (r[:, None] * u[None, :])[None, :, None, :])
+    T = n + 8
+    ref = oracle.Cache(fmt, B, H, D, T)
+    ref.append(K, V)
+    gc = kvq.Cache(fmt, B, H, D, T)
+    gc.append(dev_bf16(K), dev_bf16(V))
+    H_q = H * G
+    Q = synth.to_bf16_bits(synth.bf16_bits_to_f32(synth.queries(seed, B, H_q, D)) * np.float32(0.25) + u)
+    sm = 1.0 / np.sqrt(D)
+    O = torch.empty((B, H_q, D), dtype=torch.float32, device="cuda")
+    gc.decode_attn(dev_bf16(Q), H_q, sm, O, gc.decode_workspace(H_q))
+    torch.cuda.synchronize()
+    return assert_close(O.cpu().numpy(), ref.decode_attn(Q, sm), what=f"{name} logit ramp {span} n={n}")
+
+
+def test_multi_block_waves_tiny_b16_units():
+    # tiny_b16's 64 units at its first decode length: 3 blocks per wave
+    run("tiny_b16", B=16, H=4, G=8, n=4097, seed=90)
+
+
+def test_multi_block_waves_kivi_units():
+    # llama8b_kivi's 256 units (two coded splits per unit plus the fp16
+    # split): 7-8 blocks per wave
+    run("kivi", B=32, H=8, G=4, n=2000, seed=91)
+
+
+def test_multi_block_waves_gqa12b_units():
+    # gqa12b_b8's 64 units at D = 256 (one workgroup per CU): 6 blocks per wave
+    run("gqa12b", B=8, H=8, G=2, n=3001, seed=92)
+
+
+def test_multi_block_waves_hadamard_units():
+    # llama8b_had's 32 units (rotated K4V2): 5 blocks per wave
+    run("hadamard", B=4, H=8, G=4, n=9000 + 5, seed=93)
+
+
+@pytest.mark.parametrize("name", ["tiny_b16", "kivi", "gqa12b", "hadamard", "tiny_meta16", "affine8"])
+@pytest.mark.parametrize("span", [28.0, -28.0])
+def test_multi_block_waves_running_max(name, span):
+    """A climbing logit ramp (the running maximum rises in every block,
+    far past the lazy-rescale threshold) and a falling one (the first block
+    holds the maximum), at unit counts that give several blocks per wave."""
+    B, H, G, n = {"tiny_b16": (16, 4, 8, 4097), "kivi": (32, 8, 4, 1700), "gqa12b": (8, 8, 2, 3001),
+                  "hadamard": (4, 8, 4, 6001), "tiny_meta16": (16, 4, 8, 2500),
+                  "affine8": (16, 4, 4, 2100)}[name]
+    run_ramped(name, B, H, G, n, seed=95 + int(span > 0), span=span)
+
+
+def test_peaked_softmax_many_blocks_per_wave():
+    run("tiny_b16", B=16, H=4, G=8, n=3333, seed=97, sm=4.0)
+    run("kivi", B=32, H=8, G=4, n=1500, seed=98, sm=2.0)
+
+
+@pytest.mark.parametrize("name", ["tiny_b16", "kivi", "hadamard", "kvarn_sink", "sink32_window", "affine8"])
+def test_storage_contents_at_init_do_not_matter(name):
+    """A cache whose storage starts as all-ones bytes (NaN in every fp32 and
+    fp16 field) instead of zeros: after appends of ragged lengths, decode and
+    prefill attention must still match the oracle, since dead slots are
+    masked and appends write every live byte."""
+    from paper_2609_04263_amd import kvq
+    fmt, D = CASES[name]
+    B, H, G = 2, 2, 4
+    outlier = ("student_t", 3.0) if fmt["rotate"] else ("scale", 4, 20.0)
+    n = 333
+    K, V = synth.kv_tokens(99, B, n, H, D, outlier=outlier)
+    T = n + 40
+    nbytes = kvq.cache_bytes(fmt, B, H, D, T)
+    storage = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+    gc = kvq.Cache(fmt, B, H, D, T, storage=storage)
+    ref = oracle.Cache(fmt, B, H, D, T)
+    Kd, Vd = dev_bf16(K), dev_bf16(V)
+    H_q = H * G
+    sm = 1.0 / np.sqrt(D)
+    O = torch.empty((B, H_q, D), dtype=torch.float32, device="cuda")
+    ws = gc.decode_workspace(H_q)
+    for a, b in ((0, 1), (1, 45), (45, 200), (200, 201), (201, n)):
+        gc.append(Kd[:, a:b].contiguous(), Vd[:, a:b].contiguous())
+        ref.append(K[:, a:b], V[:, a:b])
+        Q = synth.queries(100 + b, B, H_q, D)
+        gc.decode_attn(dev_bf16(Q), H_q, sm, O, ws)
+        torch.cuda.synchronize()
+        assert_close(O.cpu().numpy(), ref.decode_attn(Q, sm), what=f"{name} NaN-filled storage n={b}")
+    # the live bytes decode to the oracle's reconstruction
+    probe = oracle.Cache(fmt, B, H, D, T)
+    probe.image[:] = image(gc)
+    probe.n = n
+    kh, vh = probe.dequant()
+    kr, vr = ref.dequant()
+    assert np.array_equal(kh, kr) and np.array_equal(vh, vr)
+    C = 45
+    Qc = synth.normal_bf16(101, "qc", (B, C, H_q, D))
+    Oc = torch.empty((B, C, H_q, D), dtype=torch.float32, device="cuda")
+    gc.prefill_attn(dev_bf16(Qc), C, H_q, sm, Oc)
+    torch.cuda.synchronize()
+    assert_close(Oc.cpu().numpy(), ref.prefill_attn(Qc, sm), what=f"{name} NaN-filled storage prefill")

@@ -31,18 +31,47 @@ CASES = {
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_fused_projection_append_matches_oracle(name):
-    from paper_2609_04263_amd import kvq
     fmt, D, rank = CASES[name]
-    B, n_new, calls = 2, 128, 2
-    d_in, d_kv = 256, 256
-    H = d_kv // D
-    d_q = 512
+    check_fused(name, fmt, D, H=256 // D, rank=rank, B=2, n_new=128, calls=2, d_in=256, d_q=512,
+                seed=140 + D + rank)
+
+
+# Shapes with several K and V column tiles per projection (so the KV-head
+# offset of a tile is not 0), row counts that are not a multiple of the
+# 256-row tile (slices past M skipped, sequences crossing row tiles), and
+# more than one row tile under the XCD-grouped tile order.
+SHAPES = {
+    "d128_h4_B3_n96": (configs.make_format(4, 4, k_group=64, v_group=64), 128, 4, 16, 3, 96, 512, 256),
+    "d256_h4_B5_n160": (configs.make_format(2, 2, k_group=128, v_group=64), 256, 4, 8, 5, 160, 1024, 512),
+    "d128_h8_B4_n224_sym": (configs.make_format(4, 2, k_mode=1, v_mode=1, k_group=128, v_group=32), 128, 8, 32,
+                            4, 224, 1024, 384),
+    "d64_h16_B6_n64_meta16": (configs.make_format(4, 4, k_group=32, v_group=64, meta_fp16=1), 64, 16, 0, 6, 64,
+                              768, 128),
+}
+
+
+@pytest.mark.parametrize("name", list(SHAPES))
+def test_fused_multi_tile_and_ragged_rows(name):
+    fmt, D, H, rank, B, n_new, d_q, d_in = SHAPES[name]
+    check_fused(name, fmt, D, H=H, rank=rank, B=B, n_new=n_new, calls=2, d_in=d_in, d_q=d_q, seed=170 + B)
+
+
+def test_fused_benchmark_shape():
+    """gqa12b_b8's prefill chunk as the benchmark runs it: M = 8 x 2048 rows,
+    d_in 3840, d_q 4096, d_kv 2048 (eight KV heads of 256), rank 32."""
+    wl = configs.WORKLOADS["gqa12b_b8"]
+    check_fused("gqa12b_b8", wl.fmt, wl.D, H=wl.H_kv, rank=wl.rank, B=wl.B, n_new=wl.chunk, calls=1,
+                d_in=wl.d_in, d_q=wl.d_q, seed=wl.seed, lora_scale=wl.lora_scale)
+
+
+def check_fused(name, fmt, D, H, rank, B, n_new, calls, d_in, d_q, seed, lora_scale=2.0):
+    from paper_2609_04263_amd import kvq
+    d_kv = H * D
     N = d_q + 2 * d_kv
-    seed = 140 + D + rank
-    W = dev_bf16(synth.normal_bf16(seed, "W", (N, d_in), std=1.0 / 16))
-    A = dev_bf16(synth.normal_bf16(seed, "A", (3 * max(rank, 1), d_in), std=1.0 / 16))
+    W = dev_bf16(synth.normal_bf16(seed, "W", (N, d_in), std=1.0 / np.sqrt(d_in)))
+    A = dev_bf16(synth.normal_bf16(seed, "A", (3 * max(rank, 1), d_in), std=1.0 / np.sqrt(d_in)))
     Bm = dev_bf16(synth.normal_bf16(seed, "B", (N, max(rank, 1)), std=0.14))
-    scale = 2.0
+    scale = lora_scale
     T = n_new * calls
     ref = oracle.Cache(fmt, B, H, D, T)
     gc = kvq.Cache(fmt, B, H, D, T)

@@ -69,14 +69,43 @@ def test_projection_odd_scale_and_rank():
 
 
 @pytest.mark.parametrize("name", configs.WORKLOAD_ORDER)
-@pytest.mark.parametrize("mode", ["decode", "prefill"])
-def test_workload_shapes_sampled_rows(name, mode):
+def test_workload_shapes_decode_rows(name):
     wl = configs.WORKLOADS[name]
     W, A, Bm = synth.layer_weights(wl)
-    M = wl.B if mode == "decode" else min(wl.B * wl.chunk, 4096)
-    H = synth.hidden(wl, ("test", mode), M)
+    H = synth.hidden(wl, ("test", "decode"), wl.B)
     y = run_gpu(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv)
-    rows = np.unique(np.random.default_rng(1).choice(M, size=min(M, 6), replace=False))
+    ref, _ = oracle.project(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv)
+    assert_close(y, ref, what=f"{name} decode")
+
+
+TILE_ROWS = 256  # row tile of the large-M kernel
+
+
+@pytest.mark.parametrize("name", configs.WORKLOAD_ORDER)
+def test_workload_prefill_chunk_every_tile(name):
+    """The projection of one whole prefill chunk (M = B * chunk rows, the
+    shape the benchmark runs), with the launch the benchmark uses.  One
+    row at a random offset inside every 256-row tile is compared across all
+    d_q + 2 d_kv columns, so every output tile of the XCD-ordered grid is
+    checked (M = 16384 at gqa12b_b8: 64 row tiles x 32 column tiles)."""
+    from paper_2609_04263_amd import kvq
+    wl = configs.WORKLOADS[name]
+    M = wl.B * min(wl.chunk, wl.context)
+    W, A, Bm = synth.layer_weights(wl)
+    Hd = synth.normal_bf16_device(wl.seed, ("test", "prefill-tiles"), (M, wl.d_in))
+    Q = torch.empty((M, wl.d_q), dtype=torch.bfloat16, device="cuda")
+    K = torch.empty((M, wl.d_kv), dtype=torch.bfloat16, device="cuda")
+    V = torch.empty((M, wl.d_kv), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(1, kvq.project_workspace_bytes(M, wl.rank)), dtype=torch.uint8, device="cuda")
+    kvq.project_qkv(Hd, dev_bf16(W), dev_bf16(A), dev_bf16(Bm), wl.rank, wl.lora_scale, wl.d_q, wl.d_kv,
+                    Q, K, V, ws)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(M)
+    tiles = np.arange((M + TILE_ROWS - 1) // TILE_ROWS)
+    rows = np.minimum(tiles * TILE_ROWS + g.integers(0, TILE_ROWS, size=tiles.size), M - 1)
     rows = np.union1d(rows, [0, M - 1])
-    ref, _ = oracle.project(H[rows], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv)
-    assert_close(y[rows], ref, what=f"{name} {mode}")
+    idx = torch.from_numpy(rows).to("cuda")
+    H = host_bits(Hd[idx])
+    y = synth.bf16_bits_to_f32(np.concatenate([host_bits(Q[idx]), host_bits(K[idx]), host_bits(V[idx])], axis=1))
+    ref, _ = oracle.project(H, W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv)
+    assert_close(y, ref, what=f"{name} prefill chunk M={M}, {rows.size} rows")
