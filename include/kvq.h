@@ -37,7 +37,8 @@ typedef enum {
     KVQ_ERR_FORMAT = 2,    /* unsupported format, or format differs from the cache's */
     KVQ_ERR_CAPACITY = 3,  /* append would exceed T_max tokens */
     KVQ_ERR_WORKSPACE = 4, /* workspace smaller than the *_workspace_bytes query */
-    KVQ_ERR_DEVICE = 5     /* HIP runtime/launch error */
+    KVQ_ERR_DEVICE = 5,    /* HIP runtime/launch error */
+    KVQ_ERR_SCRATCH = 6    /* kvq_decode_attn_noalloc: partials exceed KVQ_SCRATCH_BYTES */
 } kvq_status;
 
 enum { KVQ_AFFINE = 0, KVQ_SYMMETRIC = 1 };
@@ -243,6 +244,29 @@ kvq_status kvq_decode_workspace_bytes(const kvq_cache* cache, int H_q, size_t* b
  * An empty cache (n == 0) returns KVQ_ERR_ARG. */
 kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
                            void* workspace, size_t ws_bytes, void* stream);
+
+/* Bytes of the library's static split-partial scratch: one array per GPU,
+ * held from the first kvq_decode_attn_noalloc call on that GPU until the
+ * process ends. */
+#define KVQ_SCRATCH_BYTES (4u << 20)
+
+/* kvq_decode_attn for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops that forbid allocation): the same
+ * attention, with the split-K partials in the library's static scratch
+ * instead of a caller workspace.  Nothing is allocated or freed and no
+ * memory is cleared (every split writes its own partials before the merge
+ * reads them).  The split plan is kvq_decode_attn's, with the split count
+ * capped so that the partials, B * H_q * (D + 2) floats per split, fit in
+ * KVQ_SCRATCH_BYTES (then the outputs can differ from kvq_decode_attn's by
+ * summation order, within the same bound).  A call that would need two
+ * splits and cannot fit even that (a cache with an fp16 window or sink and
+ * B * H_q * (D + 2) * 8 > KVQ_SCRATCH_BYTES - 256) returns KVQ_ERR_SCRATCH
+ * before any launch.  Every call on one GPU shares that GPU's scratch:
+ * calls that overlap on one GPU (different streams, or threads) race and
+ * must be ordered by the caller.  Arguments, results and other errors as
+ * kvq_decode_attn. */
+kvq_status kvq_decode_attn_noalloc(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
+                                   void* stream);
 
 /* Chunked prefill attention (Sec. 3.1: evaluation consumes chunks; the
  * chunk's states are coded and appended first, then the reconstruction of

@@ -6,6 +6,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "kvq_internal.h"
 
 namespace {
@@ -157,6 +159,8 @@ const char* kvq_strerror(kvq_status s)
         return "workspace too small";
     case KVQ_ERR_DEVICE:
         return "HIP device error";
+    case KVQ_ERR_SCRATCH:
+        return "call needs more split-partial memory than the static scratch (KVQ_SCRATCH_BYTES)";
     }
     return "unknown status";
 }
@@ -501,22 +505,25 @@ kvq_status kvq_decode_workspace_bytes(const kvq_cache* c, int H_q, size_t* bytes
     return KVQ_OK;
 }
 
-kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_scale, void* O, void* workspace,
-                           size_t ws_bytes, void* stream)
+}  // extern "C"
+
+namespace {
+
+// Everything of a decode-attention call except its partial-result buffers
+// and split plan: argument checks, then the cache sections, dimensions and
+// format of the kernel parameters.
+kvq_status decode_setup(const kvq_cache* c, const void* Q, int H_q, float sm_scale, void* O, kvq::AttnParams* pp)
 {
-    if (!c || !Q || !O || !workspace || !aligned16(Q) || !aligned16(O) || !aligned16(workspace))
+    if (!c || !Q || !O || !aligned16(Q) || !aligned16(O))
         return KVQ_ERR_ARG;
     if (H_q < c->H || H_q % c->H != 0 || H_q / c->H > 16 || !isfinite(sm_scale))
         return KVQ_ERR_ARG;
     if (c->n < 1)
         return KVQ_ERR_ARG;
     const kvq_format& f = c->fmt;
-    kvq::AttnParams p = {};
+    kvq::AttnParams& p = *pp;
+    p = kvq::AttnParams{};
     p.nq = kvq::num_coded(f, c->n);
-    size_t off_ml;
-    const size_t need = decode_workspace_layout(c, H_q, &off_ml);
-    if (ws_bytes < need)
-        return KVQ_ERR_WORKSPACE;
     p.kc = at<uint32_t>(c, 0);
     p.ks = at<float>(c, 1);
     p.kz = at<float>(c, 2);
@@ -528,8 +535,6 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.kq = at<uint16_t>(c, 8);
     p.vq = at<uint16_t>(c, 9);
     p.q = (const uint16_t*)Q;
-    p.part_o = (float*)workspace;
-    p.part_ml = (float*)((uint8_t*)workspace + off_ml);
     p.out = (float*)O;
     p.B = c->B;
     p.H = c->H;
@@ -552,19 +557,116 @@ kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_
     p.rot_c = rotation_constant(c->D);
     p.meta16 = f.meta_fp16;
     p.lds_bytes = kvq::decode_lds_bytes(c->D, f, p.G);
-    // With many splits per unit, the fp16 split (sink and window) of every
-    // unit takes a slot of the one resident round that the coded splits are
-    // planned to fill (one split fewer costs little; workgroups left for a
-    // second round cost a whole split).  With few splits per unit, a split
-    // fewer would lengthen every split, and the short fp16 splits free their
-    // slots early instead.
-    const bool fp16_split = f.flush || f.sink;
+    return KVQ_OK;
+}
+
+// Target workgroups of the split kernel for this call.  With many splits per
+// unit, the fp16 split (sink and window) of every unit takes a slot of the
+// one resident round that the coded splits are planned to fill (one split
+// fewer costs little; workgroups left for a second round cost a whole
+// split).  With few splits per unit, a split fewer would lengthen every
+// split, and the short fp16 splits free their slots early instead.
+int decode_groups(const kvq_cache* c, const kvq::AttnParams& p)
+{
     const int units = c->B * c->H;
     int groups = kvq::decode_target_groups(p, c->D);
-    if (fp16_split && groups >= 4 * units)
+    if ((c->fmt.flush || c->fmt.sink) && groups >= 4 * units)
         groups -= units;
-    kvq::decode_plan(c->B, c->H, groups, p.nq, &p.S_q, &p.bps);
-    p.S_tot = p.S_q + (fp16_split ? 1 : 0);
+    return groups;
+}
+
+void decode_finish_plan(const kvq_cache* c, int groups, kvq::AttnParams* p)
+{
+    kvq::decode_plan(c->B, c->H, groups, p->nq, &p->S_q, &p->bps);
+    p->S_tot = p->S_q + (c->fmt.flush || c->fmt.sink ? 1 : 0);
+}
+
+// ------------------------------------------------ static decode scratch
+// Split partials of kvq_decode_attn_noalloc live in this array: one copy per
+// GPU, held until the process ends.  Host code never passes the array's name
+// to a kernel (on the host it is only a stand-in for the symbol); it uses the
+// device address hipGetSymbolAddress returns, looked up once per device with
+// that device current.
+static __device__ __align__(256) uint8_t scratch[KVQ_SCRATCH_BYTES];
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices];
+
+// Device address of `scratch` on the current device, or null on error.
+void* scratch_address()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices)
+        return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+kvq_status kvq_decode_attn(const kvq_cache* c, const void* Q, int H_q, float sm_scale, void* O, void* workspace,
+                           size_t ws_bytes, void* stream)
+{
+    if (!workspace || !aligned16(workspace))
+        return KVQ_ERR_ARG;
+    kvq::AttnParams p;
+    const kvq_status st = decode_setup(c, Q, H_q, sm_scale, O, &p);
+    if (st != KVQ_OK)
+        return st;
+    size_t off_ml;
+    const size_t need = decode_workspace_layout(c, H_q, &off_ml);
+    if (ws_bytes < need)
+        return KVQ_ERR_WORKSPACE;
+    p.part_o = (float*)workspace;
+    p.part_ml = (float*)((uint8_t*)workspace + off_ml);
+    decode_finish_plan(c, decode_groups(c, p), &p);
+    return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+}
+
+kvq_status kvq_decode_attn_noalloc(const kvq_cache* c, const void* Q, int H_q, float sm_scale, void* O, void* stream)
+{
+    kvq::AttnParams p;
+    const kvq_status st = decode_setup(c, Q, H_q, sm_scale, O, &p);
+    if (st != KVQ_OK)
+        return st;
+    // The plan of kvq_decode_attn, with the split count capped so that the
+    // partials (D + 2 floats per row and split, the (max, sum) pairs
+    // starting at a 256-byte boundary) fit the scratch.
+    const size_t rows = (size_t)c->B * H_q;
+    const int fp16_split = c->fmt.flush || c->fmt.sink ? 1 : 0;
+    const size_t per_split = rows * ((size_t)c->D + 2) * sizeof(float);
+    const long cap = (long)((KVQ_SCRATCH_BYTES - 256) / per_split) - fp16_split;
+    int groups = decode_groups(c, p);
+    const int units = c->B * c->H;
+    if (cap < 1) {
+        // one coded split writes the outputs itself and needs no partials;
+        // an fp16 split always makes two
+        if (fp16_split)
+            return KVQ_ERR_SCRATCH;
+        groups = units;
+    } else if ((long)groups > cap * units) {
+        groups = (int)(cap * units);
+    }
+    decode_finish_plan(c, groups, &p);
+    if (p.S_tot > 1) {
+        uint8_t* base = (uint8_t*)scratch_address();
+        if (!base)
+            return KVQ_ERR_DEVICE;
+        const size_t off_ml = round_up(rows * p.S_tot * c->D * sizeof(float), 256);
+        if (off_ml + rows * p.S_tot * 2 * sizeof(float) > KVQ_SCRATCH_BYTES)
+            return KVQ_ERR_SCRATCH;  // not reached: the cap above keeps the plan inside
+        p.part_o = (float*)base;
+        p.part_ml = (float*)(base + off_ml);
+    }
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 

@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libkvq.so")
 FORMAT_FIELDS = ("k_bits", "v_bits", "k_mode", "v_mode", "k_axis", "v_axis",
                  "k_group", "v_group", "residual", "flush", "rotate", "meta_fp16", "sink")
 
-OK, ERR_ARG, ERR_FORMAT, ERR_CAPACITY, ERR_WORKSPACE, ERR_DEVICE = range(6)
+OK, ERR_ARG, ERR_FORMAT, ERR_CAPACITY, ERR_WORKSPACE, ERR_DEVICE, ERR_SCRATCH = range(7)
+SCRATCH_BYTES = 4 << 20  # KVQ_SCRATCH_BYTES
 
 
 class KvqError(RuntimeError):
@@ -63,10 +64,12 @@ def _load() -> C.CDLL:
     L.kvq_append.argtypes = [P, P, P, I, Fp, P]
     L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
+    L.kvq_decode_attn_noalloc.argtypes = [P, P, I, C.c_float, P, P]
     L.kvq_prefill_attn.argtypes = [P, P, I, I, C.c_float, P, P]
     for name in ("kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section", "kvq_cache_reset",
                  "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_project_workspace_bytes",
-                 "kvq_project_qkv", "kvq_append", "kvq_decode_workspace_bytes", "kvq_decode_attn"):
+                 "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
+                 "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn"):
         getattr(L, name).restype = I
     return L
 
@@ -75,7 +78,7 @@ _lib = _load()
 EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
             "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
             "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
-            "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_prefill_attn")
+            "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn")
 
 
 def lib() -> C.CDLL:
@@ -191,6 +194,13 @@ class Cache:
                                   nbytes, _stream(stream))
         if st:
             _check(st, "decode_attn")
+
+    def decode_attn_noalloc(self, Q, H_q: int, sm_scale: float, O, stream=None) -> None:
+        """As decode_attn, with the split partials in the library's static
+        scratch (no workspace, nothing allocated)."""
+        st = _lib.kvq_decode_attn_noalloc(self.handle, Q.data_ptr(), H_q, sm_scale, O.data_ptr(), _stream(stream))
+        if st:
+            _check(st, "decode_attn_noalloc")
 
     def prefill_attn(self, Q, C_len: int, H_q: int, sm_scale: float, O, stream=None) -> None:
         """O[B, C, H_q, D] (fp32) <- causal attention of the newest C_len tokens'
