@@ -38,7 +38,7 @@ typedef enum {
     KVQ_ERR_CAPACITY = 3,  /* append would exceed T_max tokens */
     KVQ_ERR_WORKSPACE = 4, /* workspace smaller than the *_workspace_bytes query */
     KVQ_ERR_DEVICE = 5,    /* HIP runtime/launch error */
-    KVQ_ERR_SCRATCH = 6    /* kvq_decode_attn_noalloc: partials exceed KVQ_SCRATCH_BYTES */
+    KVQ_ERR_SCRATCH = 6    /* kvq_decode_attn_noalloc: partials cannot fit KVQ_SCRATCH_BYTES (reserved) */
 } kvq_status;
 
 enum { KVQ_AFFINE = 0, KVQ_SYMMETRIC = 1 };
@@ -257,14 +257,14 @@ kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float
  * memory is cleared (every split writes its own partials before the merge
  * reads them).  The split plan is kvq_decode_attn's, with the split count
  * capped so that the partials, B * H_q * (D + 2) floats per split, fit in
- * KVQ_SCRATCH_BYTES (then the outputs can differ from kvq_decode_attn's by
- * summation order, within the same bound).  A call that would need two
- * splits and cannot fit even that (a cache with an fp16 window or sink and
- * B * H_q * (D + 2) * 8 > KVQ_SCRATCH_BYTES - 256) returns KVQ_ERR_SCRATCH
- * before any launch.  Every call on one GPU shares that GPU's scratch:
- * calls that overlap on one GPU (different streams, or threads) race and
- * must be ordered by the caller.  Arguments, results and other errors as
- * kvq_decode_attn. */
+ * KVQ_SCRATCH_BYTES; when not even two splits fit, one split per (sequence,
+ * KV head) computes the outputs directly and the scratch is not used.  A
+ * capped plan sums in another order than kvq_decode_attn, within the same
+ * bound.  KVQ_ERR_SCRATCH is reserved for a plan that cannot fit (the
+ * planner above always finds one).  Every call on one GPU shares that GPU's
+ * scratch: calls that overlap on one GPU (different streams, or threads)
+ * race and must be ordered by the caller.  Arguments, results and other
+ * errors as kvq_decode_attn. */
 kvq_status kvq_decode_attn_noalloc(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
                                    void* stream);
 

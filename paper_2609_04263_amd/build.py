@@ -28,13 +28,18 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libkvq.so")
 ROOT = os.path.dirname(HERE)
 
-SOURCES = ["kvq_api.cpp", "append.hip", "attn.hip", "attn_d64.hip", "attn_d128.hip", "attn_d256.hip",
-           "project.hip", "merge.hip", "prefill.hip"]
 # MFMA accumulators in VGPRs: the attention loop rescales them with VALU
 # instructions, and AGPR accumulators cost a copy each way per block.
 _VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
-PER_FILE = {"append.hip": ["-ffp-contract=off"], "attn_d64.hip": _VGPR_MFMA, "attn_d128.hip": _VGPR_MFMA,
-            "attn_d256.hip": _VGPR_MFMA}
+# (source, object name, extra flags).  The decode split kernels are built
+# from one source, once per (head size, metadata width, key axis) family.
+UNITS = [("kvq_api.cpp", "kvq_api", []), ("append.hip", "append", ["-ffp-contract=off"]),
+         ("attn.hip", "attn", _VGPR_MFMA), ("project.hip", "project", []), ("merge.hip", "merge", []),
+         ("prefill.hip", "prefill", [])]
+UNITS += [("attn_part.hip", f"attn_{d}_{m}_{pc}",
+           _VGPR_MFMA + [f"-DKVQ_PART_D={d}", f"-DKVQ_PART_M16={m}", f"-DKVQ_PART_PC={pc}"])
+          for d in (64, 128, 256) for m in (0, 1) for pc in (0, 1)]
+SOURCES = sorted({u[0] for u in UNITS})
 
 
 def hipcc() -> str:
@@ -52,21 +57,24 @@ def common_flags() -> list[str]:
             "-I", os.path.join(ROOT, "include")]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *common_flags(), *PER_FILE.get(src, []), "-x", "hip", "-c",
-           os.path.join(CSRC, src), "-o", obj]
+def _compile(unit) -> str:
+    src, name, extra = unit
+    obj = os.path.join(BUILD, name + ".o")
+    cmd = [hipcc(), *common_flags(), *extra, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed for {src}:\n{res.stdout}\n{res.stderr}")
+        raise RuntimeError(f"hipcc failed for {name} ({src}):\n{res.stdout}\n{res.stderr}")
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libkvq.so; returns its path."""
+def build(verbose: bool = False, units=None) -> str:
+    """Compile every unit (or the named objects) and link libkvq.so; returns its path."""
     os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+    todo = UNITS if units is None else [u for u in UNITS if u[1] in units]
+    workers = max(1, min(len(todo), os.cpu_count() or 1))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(_compile, todo))
+    objs = [os.path.join(BUILD, u[1] + ".o") for u in UNITS]
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -1,17 +1,45 @@
-// Decode attention: split planning and dispatch by head dimension.  The
-// kernels live in attn_impl.h and are instantiated in one translation unit
-// per head dimension (attn_d64.hip, attn_d128.hip, attn_d256.hip).
+// Decode attention: split planning, dispatch to the split-kernel families
+// (attn_part.hip, one object per head size x metadata width x key axis) and
+// the merge kernels.
 
 #include "attn_impl.h"
 
 namespace kvq {
 
-hipError_t launch_decode_64(const AttnParams& p, hipStream_t stream);
-hipError_t launch_decode_128(const AttnParams& p, hipStream_t stream);
-hipError_t launch_decode_256(const AttnParams& p, hipStream_t stream);
-int decode_resident_64(const AttnParams& p);
-int decode_resident_128(const AttnParams& p);
-int decode_resident_256(const AttnParams& p);
+#define KVQ_FAMILY(D, M, P)                                                     \
+    hipError_t launch_split_##D##_##M##_##P(const AttnParams& p, hipStream_t s); \
+    int resident_split_##D##_##M##_##P(const AttnParams& p);
+#define KVQ_FAMILIES(D) KVQ_FAMILY(D, 0, 0) KVQ_FAMILY(D, 0, 1) KVQ_FAMILY(D, 1, 0) KVQ_FAMILY(D, 1, 1)
+KVQ_FAMILIES(64)
+KVQ_FAMILIES(128)
+KVQ_FAMILIES(256)
+#undef KVQ_FAMILIES
+#undef KVQ_FAMILY
+
+namespace {
+
+typedef hipError_t (*SplitLaunch)(const AttnParams&, hipStream_t);
+typedef int (*SplitResident)(const AttnParams&);
+
+// family index: (D slot) * 4 + meta16 * 2 + per-channel keys
+const SplitLaunch kLaunch[12] = {
+    launch_split_64_0_0,  launch_split_64_0_1,  launch_split_64_1_0,  launch_split_64_1_1,
+    launch_split_128_0_0, launch_split_128_0_1, launch_split_128_1_0, launch_split_128_1_1,
+    launch_split_256_0_0, launch_split_256_0_1, launch_split_256_1_0, launch_split_256_1_1};
+const SplitResident kResident[12] = {
+    resident_split_64_0_0,  resident_split_64_0_1,  resident_split_64_1_0,  resident_split_64_1_1,
+    resident_split_128_0_0, resident_split_128_0_1, resident_split_128_1_0, resident_split_128_1_1,
+    resident_split_256_0_0, resident_split_256_0_1, resident_split_256_1_0, resident_split_256_1_1};
+
+int family(const AttnParams& p, int D)
+{
+    const int slot = D == 64 ? 0 : D == 128 ? 1 : D == 256 ? 2 : -1;
+    if (slot < 0)
+        return -1;
+    return slot * 4 + (p.meta16 ? 2 : 0) + (p.k_axis == KVQ_PER_CHANNEL ? 1 : 0);
+}
+
+}  // namespace
 
 // Split planning.  Each wave streams every fourth block of its split with
 // the next block's loads in flight, so a split may be long; splits exist to
@@ -48,30 +76,18 @@ static int compute_units()
 
 int decode_target_groups(const AttnParams& p, int D)
 {
-    const int cus = compute_units();
-    int per = 1;
-    switch (D) {
-    case 64:
-        per = decode_resident_64(p);
-        break;
-    case 128:
-        per = decode_resident_128(p);
-        break;
-    case 256:
-        per = decode_resident_256(p);
-        break;
-    default:
-        break;
-    }
-    return per * cus;
+    const int f = family(p, D);
+    const int per = f < 0 ? 1 : kResident[f](p);
+    return per * compute_units();
 }
 
-void decode_plan(int B, int H, int groups, int nq, int* S_q, int* bps)
+void decode_plan(int B, int H, int D, int groups, int nq, int* S_q, int* bps)
 {
     const int nblk = (nq + 31) / 32;
-    const int sb = attn::kWaves;
+    const int sb = attn::waves_for(D);
     if (nblk == 0) {
-        *S_q = 0;
+        // no coded tokens: one split walks the fp16 tokens
+        *S_q = 1;
         *bps = sb;
         return;
     }
@@ -93,30 +109,29 @@ int decode_split_bound(int B, int H)
 
 size_t decode_lds_bytes(int D, const kvq_format& f, int G)
 {
-    // Per-wave metadata buffers; the query rows and the final merge reuse
-    // the same memory.
-    const int nvg = D / f.v_group;
-    size_t need = (size_t)attn::kWaves * 2048 * attn::meta_pairs(D, nvg);
-    const size_t q = 16 * (size_t)D * sizeof(float);
-    const size_t merge = (2 * attn::kWaves * 16 + (size_t)attn::kWaves * G * D) * sizeof(float);
-    if (q > need)
-        need = q;
-    if (merge > need)
-        need = merge;
-    return need;
+    // the layout is described in attn_impl.h
+    const int nvg = D / f.v_group, W = attn::waves_for(D), np = attn::meta_pairs(D, nvg);
+    const bool perch = f.k_axis == KVQ_PER_CHANNEL, fp16 = f.flush || f.sink;
+    const size_t need = attn::lds_waves(D, perch, G) + (size_t)W * attn::lds_per_wave(D, np, perch, G, fp16);
+    const size_t merge = (2 * (size_t)W * 16 + (size_t)W * G * D) * sizeof(float);
+    return merge > need ? merge : need;
 }
 
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream)
 {
+    const int f = family(p, D);
+    if (f < 0)
+        return hipErrorInvalidValue;
+    const hipError_t e = kLaunch[f](p, stream);
+    if (e != hipSuccess || p.S_tot == 1)
+        return e;
     switch (D) {
     case 64:
-        return launch_decode_64(p, stream);
+        return attn::launch_merge<64>(p, stream);
     case 128:
-        return launch_decode_128(p, stream);
-    case 256:
-        return launch_decode_256(p, stream);
+        return attn::launch_merge<128>(p, stream);
     default:
-        return hipErrorInvalidValue;
+        return attn::launch_merge<256>(p, stream);
     }
 }
 

@@ -1,7 +1,8 @@
 // Split-K decode attention over the packed cache with in-kernel
 // reconstruction (Sec. 3.1-3.2 of the paper: attention sees the stored
 // reconstruction; here it is computed from the codes without materializing
-// it).  Included by one translation unit per head dimension.
+// it).  The split kernels are instantiated by attn_part.hip, once per (head
+// size, metadata width, key axis) family; the merge kernels by attn.hip.
 //
 // Work decomposition.  A workgroup of 4 waves handles one (split, sequence,
 // KV head).  The MFMA v_mfma_f32_16x16x32_f16 has 16 columns; the G <= 16
@@ -56,8 +57,6 @@
 namespace kvq {
 namespace attn {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
 constexpr float kNegInf = -__builtin_inff();
 constexpr float kTau = 4.0f;        // lazy rescale threshold, log2 units
 constexpr float kPScale = 0.0625f;  // 2^-kTau: keeps p s below the group scale
@@ -71,9 +70,19 @@ __host__ __device__ constexpr int meta_pairs(int D, int nvg)
     return ((D + 32 * nvg) / 4 + 63) / 64;
 }
 
+// Waves per split workgroup.  Two waves of the head_dim 128 kernel fit a
+// SIMD, so a workgroup of eight fills a compute unit: with as many (sequence,
+// KV head) units as compute units, one split per unit covers the device and
+// no merge is needed.  The other head sizes use four.
+__host__ __device__ constexpr int waves_for(int D)
+{
+    return D == 128 ? 8 : 4;
+}
+
 // Compile-time shape of one kernel instance.
 template <int D_, int KBITS_, int VBITS_, bool PERCH_, int VGS_, bool M16_ = false>
 struct Cfg {
+    static constexpr int WAVES = waves_for(D_), THREADS = 64 * WAVES;
     static constexpr int D = D_, KBITS = KBITS_, VBITS = VBITS_, VGS = VGS_;
     static constexpr bool PERCH = PERCH_;
     static constexpr bool M16 = M16_;           // fp16 scales and offsets
@@ -85,8 +94,75 @@ struct Cfg {
     static constexpr int NVG = D / VG;          // value groups per token
     static constexpr int MBPG = VG / 16;        // value M-blocks per group
     static constexpr int NPAIR = meta_pairs(D, NVG);
+    // Register sets of the block pipeline: a wave computes one block while
+    // the loads of the next NBUF - 1 are in flight.  Wider heads run fewer
+    // waves per SIMD, so each wave keeps more bytes in flight.
+    static constexpr int NBUF = KBITS == 8 ? 2 : D == 64 ? 2 : 3;
     static_assert(NVG >= 1, "value group larger than head_dim");
 };
+
+// Per-channel keys (KIVI): the score operand q_hd s_d changes with every
+// 32-token block.  Its G D products are formed once per block, eight per
+// (head, channel octet) item spread over the wave's lanes, and exchanged
+// through the wave's LDS slots into the MFMA operand layout.
+struct PerchCtx {
+    const float* qw;  // LDS [G][D] fp32 queries (rotated when the format rotates)
+    uint8_t* slots;   // this wave's LDS slots: item i = (head i / (D/8), octet i % (D/8)) at 32 i, hi then lo
+    int items;        // G D / 8
+    int rbase;        // byte offset of this lane's operand slot at K-block 0 (+128 per K-block)
+    int zsrc, zj;     // lane (x4) and writer iteration holding this column's key offset term
+    int hn;           // head of this lane's column (below G)
+};
+
+// Split kernel LDS, in bytes from its start: the rotated query rows
+// ([16][D] fp32, rotating formats); for per-channel keys the fp32 query rows
+// [G][D]; then one region per wave.  During the coded blocks a wave's region
+// holds its metadata buffer (npair 2 KiB) and, for per-channel keys, its
+// operand slots (G D 4 bytes); the fp16 blocks come after the coded ones and
+// reuse it for a transposed value block ([D][kVtPitch] halves).  The final
+// merge of the waves reuses everything from the start.
+constexpr int kVtPitch = 40;  // halves per channel row of a transposed fp16 value block
+
+__host__ __device__ constexpr size_t lds_qw(int D)
+{
+    return (size_t)16 * D * 4;
+}
+
+__host__ __device__ constexpr size_t lds_waves(int D, bool perch, int G)
+{
+    return lds_qw(D) + (perch ? (size_t)G * D * 4 : 0);
+}
+
+__host__ __device__ constexpr size_t lds_per_wave(int D, int npair, bool perch, int G, bool fp16)
+{
+    const size_t coded = (size_t)npair * 2048 + (perch ? (size_t)G * D * 4 : 0);
+    const size_t vt = fp16 ? (size_t)D * kVtPitch * 2 : 0;
+    return ((coded > vt ? coded : vt) + 15) / 16 * 16;
+}
+
+// Sum over aligned groups of NL lanes (NL = 8, 16 or 32), every lane of a
+// group receiving the group's sum (DPP quad xors, half-row and row mirrors,
+// then a swap of adjacent rows).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+template <int NL>
+__device__ __forceinline__ float group_sum(float v)
+{
+    v += dpp_f32<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+    v += dpp_f32<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+    v += dpp_f32<0x141>(v);  // row_half_mirror
+    if constexpr (NL >= 16)
+        v += dpp_f32<0x140>(v);  // row_mirror
+    if constexpr (NL >= 32) {
+        auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+    }
+    return v;
+}
 
 __device__ __forceinline__ float max_rows(float v)
 {
@@ -241,31 +317,57 @@ struct BlockRegs {
     u32x4 ms[C::NPAIR], mz[C::NPAIR];  // metadata chunk pairs lane + 64 u
 };
 
-// Issue every load of block `ub` (unit * NB + block) of a lane.  Every lane
-// issues the same loads whatever the format (surplus lanes re-read the last
-// chunk pair), so the number of loads in flight is fixed.
+// A lane's load addresses for block 0 of its (sequence, KV head) unit; block
+// b is at a fixed stride from them.  The metadata chunk a lane loads (a key
+// or a value chunk, fixed per lane) is selected once, so the loads of a block
+// need no per-block selects or branches.
 template <class C>
-__device__ __forceinline__ void load_block(BlockRegs<C>& r, const AttnParams& p, const MetaMap& mm, size_t ub,
-                                           int lane)
+struct LoadMap {
+    const uint32_t* kc;              // key code words of this lane
+    const uint32_t* vc;              // value code words of this lane
+    const uint8_t* ms[C::NPAIR];     // scale chunk of pair u
+    long dz[C::NPAIR];               // offset chunk - scale chunk (bytes)
+    uint32_t mstride[C::NPAIR];      // metadata bytes per block of the chunk's section
+};
+
+template <class C>
+__device__ __forceinline__ LoadMap<C> load_map(const AttnParams& p, const MetaMap& mm, size_t ub0, int lane)
 {
-    const uint32_t* kc = p.kc + ub * (2 * 64 * C::KW) + lane * C::KW;
-    gload_words<C::KW>(kc, r.k[0]);
-    gload_words<C::KW>(kc + 64 * C::KW, r.k[1]);
-    gload_words<C::VW>(p.vc + ub * (64 * C::VW) + lane * C::VW, r.v);
+    LoadMap<C> L;
+    L.kc = p.kc + ub0 * (2 * 64 * C::KW) + lane * C::KW;
+    L.vc = p.vc + ub0 * (64 * C::VW) + lane * C::VW;
 #pragma unroll
     for (int u = 0; u < C::NPAIR; ++u) {
+        // every lane issues the same loads whatever the format: surplus
+        // lanes re-read the last chunk pair, so the loads in flight are fixed
         const int c = min(lane + 64 * u, mm.np - 1);
         const bool key = c < mm.kp;
-        // one base pointer and selected offsets keep the loads global ones
-        const long s_off = (key ? (long)ub * mm.nk + 4 * c : (long)ub * mm.nv + 4 * (c - mm.kp)) * mm.esz +
-                           (key ? 0 : mm.dvs);
-        const long z_off = s_off + (key ? mm.dkz : mm.dvz - mm.dvs);
+        const long off = key ? ((long)ub0 * mm.nk + 4 * c) * mm.esz
+                             : mm.dvs + ((long)ub0 * mm.nv + 4 * (c - mm.kp)) * mm.esz;
+        L.ms[u] = mm.ks + off;
+        L.dz[u] = key ? mm.dkz : mm.dvz - mm.dvs;
+        L.mstride[u] = (uint32_t)((key ? mm.nk : mm.nv) * mm.esz);
+    }
+    return L;
+}
+
+// Issue every load of block `blk` (within the unit) of a lane.
+template <class C>
+__device__ __forceinline__ void load_block(BlockRegs<C>& r, const LoadMap<C>& L, int blk)
+{
+    const uint32_t* kc = L.kc + (size_t)blk * (2 * 64 * C::KW);
+    gload_words<C::KW>(kc, r.k[0]);
+    gload_words<C::KW>(kc + 64 * C::KW, r.k[1]);
+    gload_words<C::VW>(L.vc + (size_t)blk * (64 * C::VW), r.v);
+#pragma unroll
+    for (int u = 0; u < C::NPAIR; ++u) {
+        const uint8_t* ms = L.ms[u] + (size_t)blk * L.mstride[u];
         if constexpr (!C::M16) {
-            r.ms[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + s_off));
-            r.mz[u] = __builtin_nontemporal_load((const u32x4*)(mm.ks + z_off));
+            r.ms[u] = __builtin_nontemporal_load((const u32x4*)ms);
+            r.mz[u] = __builtin_nontemporal_load((const u32x4*)(ms + L.dz[u]));
         } else {  // four fp16 values, widened when staged
-            const u32x2 s2 = __builtin_nontemporal_load((const u32x2*)(mm.ks + s_off));
-            const u32x2 z2 = __builtin_nontemporal_load((const u32x2*)(mm.ks + z_off));
+            const u32x2 s2 = __builtin_nontemporal_load((const u32x2*)ms);
+            const u32x2 z2 = __builtin_nontemporal_load((const u32x2*)(ms + L.dz[u]));
             r.ms[u] = u32x4{s2.x, s2.y, 0u, 0u};
             r.mz[u] = u32x4{z2.x, z2.y, 0u, 0u};
         }
@@ -279,7 +381,6 @@ struct Split {
     static constexpr int NKB = C::NKB, NMB = C::NMB, NVG = C::NVG;
     half8 qhi[C::PERCH ? 1 : NKB], qlo[C::PERCH ? 1 : NKB];  // query B operands (per-token keys)
     float qsum[C::PERCH ? 1 : NKB];                          // sum of the 32 query channels of K-block kb
-    float qf[C::PERCH ? NKB : 1][8];                         // fp32 query, operand order (per-channel keys)
     float m, lsum;                                           // running max (log2 units), lane partial sum
     float zl[NVG];                                           // lane partials of sum_t p_t z'_tg
     floatx4 oacc[NMB];
@@ -372,7 +473,7 @@ struct Split {
     // group of this lane's column when every group has its own columns.
     __device__ __forceinline__ void coded_block(const BlockRegs<C>& r, float4* wl, const MetaMap& mm, int lane,
                                                 int lgk, bool qlo_on, bool rep, int vg, const CodeBits& kcb,
-                                                const CodeBits& vcb, int valid)
+                                                const CodeBits& vcb, int valid, const PerchCtx& pc)
     {
         const int qg = lane >> 4;
         // Stage the block's metadata: key scales and z' times sm_scale log2(e),
@@ -439,36 +540,69 @@ struct Split {
                 break;
             }
         } else {
-            // Per-channel keys: B = q * s_d (hi + lo), and sum_d q_d z'_d per head.
-            half8 bh[NKB], bl[NKB];
+            // Per-channel keys: B = q s_d (hi + lo), and sum_d q_d z'_d per head.
+            // Writer: item it = lane + 64 j forms the eight products of its
+            // (head, octet) in operand order and the octet's offset partial;
+            // lanes past the last item repeat it without storing.
+            constexpr int NO = C::D / 8, JMAX = (16 * NO + 63) / 64;
+            float zsum[JMAX];
+#pragma unroll
+            for (int jj = 0; jj < JMAX; ++jj) {
+                zsum[jj] = 0.0f;
+                if (64 * jj < pc.items) {
+                    const int it = lane + 64 * jj;
+                    const int ic = min(it, pc.items - 1);
+                    const int h = ic / NO, o = ic % NO;
+                    const float4 qa = *(const float4*)(pc.qw + h * C::D + 8 * o);
+                    const float4 qb = *(const float4*)(pc.qw + h * C::D + 8 * o + 4);
+                    const float4 s0 = ks[2 * o], s1 = ks[2 * o + 1];
+                    const float4 z0 = kz[2 * o], z1 = kz[2 * o + 1];
+                    const float qn[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+                    const float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+                    const float zn[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+                    float v[8];
+                    float zp = 0.0f;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        v[e] = qn[perm4(e)] * sn[perm4(e)];
+                        zp += qn[e] * zn[e];
+                    }
+                    half8 hi, lo;
+                    split_pairs(v, &hi, &lo);
+                    if (it < pc.items) {
+                        *(half8*)(pc.slots + 32 * it) = hi;
+                        *(half8*)(pc.slots + 32 * it + 16) = lo;
+                    }
+                    zsum[jj] = group_sum<NO>(zp);
+                }
+            }
+            // Reader: this column's offset term from the first lane of its
+            // head's items, then the operand slots (written by this wave
+            // above; a wave's LDS accesses are performed in order).
             float zq = 0.0f;
 #pragma unroll
-            for (int kb = 0; kb < NKB; ++kb) {
-                const float4 s0 = ks[8 * kb + 2 * qg], s1 = ks[8 * kb + 2 * qg + 1];
-                const float4 z0 = kz[8 * kb + 2 * qg], z1 = kz[8 * kb + 2 * qg + 1];
-                const float sn[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-                const float zn[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-                float v[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    v[e] = qf[kb][e] * sn[perm4(e)];
-                    zq += qf[kb][e] * zn[perm4(e)];
+            for (int jj = 0; jj < JMAX; ++jj) {
+                if (64 * jj < pc.items) {
+                    const float t = __int_as_float(__builtin_amdgcn_ds_bpermute(pc.zsrc, __float_as_int(zsum[jj])));
+                    zq = jj == pc.zj ? t : zq;
                 }
-                split_pairs(v, &bh[kb], &bl[kb]);
             }
-            zq = sum_rows(zq);
+            floatx4 acc0 = {zq, zq, zq, zq}, acc1 = acc0;
 #pragma unroll
-            for (int h2 = 0; h2 < 2; ++h2) {
-                floatx4 acc = {zq, zq, zq, zq};
+            for (int kb = 0; kb < NKB; ++kb) {
+                const half8 bh = *(const half8*)(pc.slots + pc.rbase + 128 * kb);
+                const half8 bl = *(const half8*)(pc.slots + pc.rbase + 128 * kb + 16);
+                const half8 a0 = biased_codes<C::KBITS>(r.k[0], kb, kcb);
+                const half8 a1 = biased_codes<C::KBITS>(r.k[1], kb, kcb);
+                acc0 = mfma16(a0, bh, acc0);
+                acc0 = mfma16(a0, bl, acc0);
+                acc1 = mfma16(a1, bh, acc1);
+                acc1 = mfma16(a1, bl, acc1);
+            }
 #pragma unroll
-                for (int kb = 0; kb < NKB; ++kb) {
-                    const half8 a = biased_codes<C::KBITS>(r.k[h2], kb, kcb);
-                    acc = mfma16(a, bh[kb], acc);
-                    acc = mfma16(a, bl[kb], acc);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    l[4 * h2 + i] = acc[i];
+            for (int i = 0; i < 4; ++i) {
+                l[i] = acc0[i];
+                l[4 + i] = acc1[i];
             }
         }
         if (valid < 32) {
@@ -523,15 +657,36 @@ struct Split {
         }
     }
 
-    // One block of fp16 tokens (t0 .. t0 + 31, those >= n masked) read
-    // straight from rows [unit][rows][D] at slot t mod rows: the window ring
-    // (rows = R + F) or the sink (rows = sink, slot t).
+    // One block of fp16 tokens (t0 .. t0 + 31, those >= n masked) read from
+    // rows [unit][rows][D] at slot t mod rows: the window ring (rows = R + F)
+    // or the sink (rows = sink, slot t).  Key rows feed the score operands
+    // directly (a lane's eight channels are contiguous); the value operands
+    // need eight tokens of one channel per lane, so the value rows are read
+    // in 16-byte pieces and written transposed into the wave's LDS buffer
+    // vt ([D][kVtPitch] halves, the tokens of each octet in operand order).
     __device__ __forceinline__ void fp16_block(const AttnParams& p, const uint16_t* kr, const uint16_t* vr, int ring,
-                                               int n, int unit, int t0, int lane, bool qlo_on)
+                                               int n, int unit, int t0, int lane, bool qlo_on, const PerchCtx& pc,
+                                               uint16_t* vt)
     {
         constexpr int D = C::D;
         const int hh = lane & 15, qg = lane >> 4;
         const size_t rbase = (size_t)unit * ring;
+        // value rows -> vt (every piece of the block, masked tokens as zeros)
+#pragma unroll 2
+        for (int i = 0; i < D / 16; ++i) {
+            const int idx = lane + 64 * i;
+            const int r = idx / (D / 8), c8 = 8 * (idx % (D / 8));
+            const int t = t0 + r;
+            u32x4 w = {0u, 0u, 0u, 0u};
+            if (t < n)
+                w = *(const u32x4*)(vr + (rbase + (size_t)(t % ring)) * D + c8);
+            const int e = r & 7;
+            const int pos = (r & ~7) + (e < 4 ? 2 * e : 2 * (e - 4) + 1);  // operand slot of token r
+            const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                vt[(c8 + k) * kVtPitch + pos] = (uint16_t)(ww[k >> 1] >> (16 * (k & 1)));
+        }
         float l[8];
 #pragma unroll
         for (int h2 = 0; h2 < 2; ++h2) {
@@ -552,8 +707,15 @@ struct Split {
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) {
                 if constexpr (C::PERCH) {
+                    const float* qr = pc.qw + pc.hn * D + 32 * kb + 8 * qg;
+                    const float4 qa = *(const float4*)qr, qb = *(const float4*)(qr + 4);
+                    const float qn[8] = {qa.x, qa.y, qa.z, qa.w, qb.x, qb.y, qb.z, qb.w};
+                    float v[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        v[e] = qn[perm4(e)];
                     half8 bh, bl;
-                    split_pairs(qf[kb], &bh, &bl);
+                    split_pairs(v, &bh, &bl);
                     acc = mfma16(a[kb], bh, acc);
                     acc = mfma16(a[kb], bl, acc);
                 } else {
@@ -566,47 +728,33 @@ struct Split {
             for (int i = 0; i < 4; ++i)
                 l[4 * h2 + i] = acc[i] * p.sm_log2;
         }
-        int slot[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int t = t0 + 8 * qg + k;
-            slot[k] = t < n ? t % ring : -1;
-            l[k] = t < n ? l[k] : kNegInf;
-        }
-        softmax(l);
+        for (int k = 0; k < 8; ++k)
+            l[k] = t0 + 8 * qg + k < n ? l[k] : kNegInf;
+        softmax(l);  // masked tokens get p = 0 (their value rows are zeros too)
         float pv[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            pv[e] = slot[perm4(e)] >= 0 ? l[perm4(e)] * kPScale : 0.0f;
+            pv[e] = l[perm4(e)] * kPScale;
         half8 ph, pl;
         split_pairs(pv, &ph, &pl);
-        half8 va[NMB];
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb) {
-            const int d = 16 * mb + hh;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int sl = slot[perm4(e)];
-                const uint16_t raw = sl >= 0 ? vr[(rbase + (size_t)sl) * D + d] : (uint16_t)0;
-                va[mb][e] = __builtin_bit_cast(_Float16, raw);
-            }
-        }
-#pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) {
-            oacc[mb] = mfma16(va[mb], ph, oacc[mb]);
-            oacc[mb] = mfma16(va[mb], pl, oacc[mb]);
+            const half8 va = *(const half8*)(vt + (16 * mb + hh) * kVtPitch + 8 * qg);
+            oacc[mb] = mfma16(va, ph, oacc[mb]);
+            oacc[mb] = mfma16(va, pl, oacc[mb]);
         }
     }
 };
 
 // Inverse rotation (the normalized transform is its own inverse) of G rows
 // of D outputs staged in LDS, then the store to O.
-template <int D>
+template <int D, int NT>
 __device__ __forceinline__ void finish_rows(const AttnParams& p, float* xo, size_t row0, int G)
 {
     if (p.rotate) {
         for (int h = 1; h < D; h <<= 1) {
-            for (int idx = threadIdx.x; idx < G * (D / 2); idx += kThreads) {
+            for (int idx = threadIdx.x; idx < G * (D / 2); idx += NT) {
                 const int r = idx / (D / 2), k = idx % (D / 2);
                 const int jj = (k / h) * 2 * h + (k % h);
                 const float a = xo[r * D + jj], c = xo[r * D + jj + h];
@@ -617,20 +765,19 @@ __device__ __forceinline__ void finish_rows(const AttnParams& p, float* xo, size
         }
     }
     const float post = p.rotate ? p.rot_c : 1.0f;
-    for (int idx = threadIdx.x; idx < G * D; idx += kThreads)
+    for (int idx = threadIdx.x; idx < G * D; idx += NT)
         p.out[row0 * D + idx] = xo[idx] * post;
 }
 
 template <class C>
 __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
 {
-    constexpr int D = C::D, NKB = C::NKB, NMB = C::NMB;
+    constexpr int D = C::D, NKB = C::NKB, NMB = C::NMB, W = C::WAVES, NT = C::THREADS;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
     const int hh = lane & 15, qg = lane >> 4;
     const int split = blockIdx.x, unit = blockIdx.y;
     const int b = unit / p.H, j = unit % p.H, G = p.G;
-    const bool ring_split = (p.ring || p.sink) && split == p.S_q;  // the fp16 split: sink and window
     const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
     const bool qlo_on = p.rotate != 0;
     const int NB = p.T >> 5;
@@ -667,9 +814,10 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
 
     // ---- block range of this split
     const int nblk = (p.nq + 31) >> 5;
-    const int blk_begin = ring_split ? 0 : split * p.bps;
-    const int blk_end = ring_split ? 0 : min(nblk, blk_begin + p.bps);
+    const int blk_begin = min(nblk, split * p.bps);
+    const int blk_end = min(nblk, blk_begin + p.bps);
     const size_t ub0 = (size_t)unit * NB;
+    const LoadMap<C> ldm = load_map<C>(p, mm, ub0, lane);
 
     // ---- queries.  Without rotation each lane reads its own operand
     // pieces (head `head`, channels 32 kb + 8 qg .. + 7) straight from
@@ -681,14 +829,20 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
         for (int kb = 0; kb < NKB; ++kb)
             qpc[kb] = active ? *(const u32x4*)(p.q + (qrow + head) * D + 32 * kb + 8 * qg) : u32x4{0u, 0u, 0u, 0u};
     }
-    BlockRegs<C> ra, rb;
+    BlockRegs<C> rbuf[C::NBUF];
     int blk = blk_begin + wave;
-    if (blk_end > blk_begin)
-        load_block<C>(ra, p, mm, ub0 + min(blk, blk_end - 1), lane);
+    const int last = blk_end - 1;
+    // the first NBUF - 1 blocks of this wave go in flight before the query
+    // setup (past the end they re-read the last block)
+    if (blk_end > blk_begin) {
+#pragma unroll
+        for (int u = 0; u + 1 < C::NBUF; ++u)
+            load_block<C>(rbuf[u], ldm, min(blk + W * u, last));
+    }
     float* lq = (float*)lds;
     if (p.rotate) {
         constexpr int QPIECES = 16 * D / 8;
-        for (int pc = threadIdx.x; pc < QPIECES; pc += kThreads) {
+        for (int pc = threadIdx.x; pc < QPIECES; pc += NT) {
             const int row = pc / (D / 8);
             u32x4 raw = {0u, 0u, 0u, 0u};
             if (row < G)
@@ -703,7 +857,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
         }
         __syncthreads();
         for (int h = 1; h < D; h <<= 1) {
-            for (int idx = threadIdx.x; idx < 16 * (D / 2); idx += kThreads) {
+            for (int idx = threadIdx.x; idx < 16 * (D / 2); idx += NT) {
                 const int row = idx / (D / 2), k = idx % (D / 2);
                 const int jj = (k / h) * 2 * h + (k % h);
                 const float a = lq[row * D + jj], c = lq[row * D + jj + h];
@@ -712,7 +866,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
             }
             __syncthreads();
         }
-        for (int idx = threadIdx.x; idx < 16 * D; idx += kThreads)
+        for (int idx = threadIdx.x; idx < 16 * D; idx += NT)
             lq[idx] *= p.rot_c;
         __syncthreads();
     }
@@ -733,55 +887,75 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
             }
             part += v[k];
         }
-        if constexpr (C::PERCH) {
-#pragma unroll
-            for (int k = 0; k < 8; ++k)
-                S.qf[kb][k] = v[k];
-        } else {
+        if constexpr (!C::PERCH) {
             split_pairs(v, &S.qhi[kb], &S.qlo[kb]);
             S.qsum[kb] = sum_rows(part);
         }
     }
-    if (p.rotate)
-        __syncthreads();  // the metadata buffers overwrite the query rows
+    // This wave's LDS region, and for per-channel keys the G query rows as
+    // fp32 (after the rotated rows) and this lane's slot addresses.
+    const bool fp16_tokens = p.ring || p.sink;
+    uint8_t* region = lds + lds_waves(D, C::PERCH, G) + (size_t)wave * lds_per_wave(D, C::NPAIR, C::PERCH, G, fp16_tokens);
+    PerchCtx pc = {};
+    if constexpr (C::PERCH) {
+        constexpr int NO = D / 8;
+        float* qw = (float*)(lds + lds_qw(D));
+        for (int idx = threadIdx.x; idx < G * D; idx += NT)
+            qw[idx] = p.rotate ? lq[idx] : bf16_to_f32(p.q[qrow * D + idx]);
+        pc.qw = qw;
+        pc.slots = region + C::NPAIR * 2048;
+        pc.items = G * NO;
+        pc.hn = head < G ? head : 0;
+        pc.rbase = (pc.hn * NO + qg) * 32;
+        const int first = pc.hn * NO;  // the head's first item
+        pc.zj = first >> 6;
+        pc.zsrc = (first & 63) * 4;
+        __syncthreads();
+    }
 
     const CodeBits kcb = code_bits<C::KBITS>(), vcb = code_bits<C::VBITS>();
-    if (!ring_split) {
-        float4* wl = (float4*)lds + wave * (128 * C::NPAIR);
-        // Two register sets alternate: the next block's loads fly while
-        // this one is computed (past the end they re-read the last block).
-        const int last = blk_end - 1;
-        while (blk < blk_end) {
-            load_block<C>(rb, p, mm, ub0 + min(blk + kWaves, last), lane);
-            S.coded_block(ra, wl, mm, lane, lgk, qlo_on, rep, vg, kcb, vcb, min(32, p.nq - 32 * blk));
-            blk += kWaves;
-            if (blk >= blk_end)
-                break;
-            load_block<C>(ra, p, mm, ub0 + min(blk + kWaves, last), lane);
-            S.coded_block(rb, wl, mm, lane, lgk, qlo_on, rep, vg, kcb, vcb, min(32, p.nq - 32 * blk));
-            blk += kWaves;
+    {
+        float4* wl = (float4*)region;
+        // NBUF register sets rotate: while block blk is computed, the loads
+        // of the next NBUF - 1 blocks of this wave are in flight.
+        // Whole rounds of NBUF blocks, the compute of blocks past the end
+        // skipped: the loop has one exit, at the top of a round, so the
+        // compiler's wait counts see the same loads in flight on every path.
+        for (int left = (blk_end - blk + W - 1) / W; left > 0; left -= C::NBUF) {
+#pragma unroll
+            for (int u = 0; u < C::NBUF; ++u) {
+                load_block<C>(rbuf[(u + C::NBUF - 1) % C::NBUF], ldm, min(blk + W * (C::NBUF - 1), last));
+                if (blk < blk_end)
+                    S.coded_block(rbuf[u], wl, mm, lane, lgk, qlo_on, rep, vg, kcb, vcb, min(32, p.nq - 32 * blk),
+                                  pc);
+                blk += W;
+            }
         }
-    } else {
+    }
+    // fp16 blocks (sink blocks, then window blocks): block f of the unit's
+    // fp16 tokens goes to split f % S and wave (f / S) % W, round robin.
+    if (fp16_tokens) {
         const int nsb = (p.n_sink + 31) >> 5, nrb = (p.n - p.nq + 31) >> 5;
-        for (int rb = wave; rb < nsb + nrb; rb += kWaves) {
-            if (rb < nsb)
-                S.fp16_block(p, p.kq, p.vq, p.sink, p.n_sink, unit, 32 * rb, lane, qlo_on);
+        uint16_t* vt = (uint16_t*)region;  // the coded blocks are done with it
+        for (int f = split + p.S_tot * wave; f < nsb + nrb; f += p.S_tot * W) {
+            if (f < nsb)
+                S.fp16_block(p, p.kq, p.vq, p.sink, p.n_sink, unit, 32 * f, lane, qlo_on, pc, vt);
             else
-                S.fp16_block(p, p.kr, p.vr, p.ring, p.n, unit, p.nq + 32 * (rb - nsb), lane, qlo_on);
+                S.fp16_block(p, p.kr, p.vr, p.ring, p.n, unit, p.nq + 32 * (f - nsb), lane, qlo_on, pc, vt);
         }
     }
 
-    // ---- merge the four waves of this split in LDS
+    // ---- merge the W waves of this split in LDS
     const float lsum = sum_rows(S.lsum);
     float zl[C::NVG];
 #pragma unroll
     for (int g = 0; g < C::NVG; ++g)
         zl[g] = sum_rows(S.zl[g]);
     __syncthreads();
-    float* lm = (float*)lds;           // [4][16] running max per wave and head
-    float* ll = lm + kWaves * 16;      // [4][16] softmax sums
-    float* lo = lm + 2 * kWaves * 16;  // [4][G][D] unnormalized outputs
-    float* xo = lo;  // [G][D] result: element idx is written after its own four reads
+    float* lm = (float*)lds;      // [W][16] running max per wave and head
+    float* ll = lm + W * 16;      // [W][16] softmax sums
+    float* lo = lm + 2 * W * 16;  // [W][G][D] unnormalized outputs
+    float* xo = lo;  // [G][D] result: element idx is written after its own W reads
     if (qg == 0 && vg == 0 && active) {
         lm[wave * 16 + head] = S.m;
         ll[wave * 16 + head] = lsum;
@@ -792,7 +966,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
             const int g = mb / C::MBPG;
             // with one column set per group, a column holds its own group's channels
             if (!rep || g == vg) {
-                const float z = ring_split ? 0.0f : zl[rep ? 0 : g];
+                const float z = zl[rep ? 0 : g];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
                     lo[((size_t)wave * G + head) * D + 16 * mb + 4 * qg + i] =
@@ -803,14 +977,14 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     __syncthreads();
     const bool single = p.S_tot == 1;
     const size_t row0 = (size_t)b * p.H_q + (size_t)j * G;
-    for (int idx = threadIdx.x; idx < G * D; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < G * D; idx += NT) {
         const int h = idx / D, d = idx % D;
         float M = kNegInf;
-        for (int w = 0; w < kWaves; ++w)
+        for (int w = 0; w < W; ++w)
             M = fmaxf(M, lm[w * 16 + h]);
         float acc = 0.0f, Ls = 0.0f;
         if (M != kNegInf) {
-            for (int w = 0; w < kWaves; ++w) {
+            for (int w = 0; w < W; ++w) {
                 const float sc = fast_exp2(lm[w * 16 + h] - M);
                 acc += sc * lo[((size_t)w * G + h) * D + d];
                 Ls += sc * ll[w * 16 + h];
@@ -830,7 +1004,7 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
     if (!single)
         return;  // the merge kernel finishes
     __syncthreads();
-    finish_rows<D>(p, xo, row0, G);
+    finish_rows<D, NT>(p, xo, row0, G);
 }
 
 // Waves per SIMD the register allocation is held to: 3 at head_dim 64 (the
@@ -842,48 +1016,50 @@ constexpr int split_waves_per_simd()
 }
 
 template <class C>
-__global__ __launch_bounds__(kThreads, split_waves_per_simd<C>()) void decode_split_kernel(AttnParams p)
+__global__ __launch_bounds__(C::THREADS, split_waves_per_simd<C>()) void decode_split_kernel(AttnParams p)
 {
     extern __shared__ float lds_f[];
     split_body<C>(p, (uint8_t*)lds_f);
 }
 
 // Merge the S_tot split partials: one thread per output element (row, d),
-// 256 / D rows per workgroup.  A thread reads the partials of its row in
-// chunks of kMergeChunk splits, all loads of a chunk in flight together,
-// and combines them online: O = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
+// kMergeThreads / D rows per workgroup.  A thread reads the (max, sum) pairs
+// and partial outputs of its row in chunks of up to kMergeChunk splits, all
+// loads of a chunk in flight together (no loads past the last split), and
+// combines them online: O = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
 // The rows are then rotated back when the format rotates, and stored.
-constexpr int kMergeChunk = 16;
+constexpr int kMergeChunk = 8, kMergeThreads = 256;
 
 template <int D>
-__global__ __launch_bounds__(kThreads) void decode_merge_kernel(AttnParams p)
+__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(AttnParams p)
 {
-    constexpr int R = kThreads / D;  // rows per workgroup
-    __shared__ float xo[kThreads];
+    constexpr int R = kMergeThreads / D;  // rows per workgroup
+    __shared__ float xo[kMergeThreads];
     const int t = threadIdx.x, rl = t / D, d = t % D;
     const size_t rows = (size_t)p.B * p.H_q;
     const size_t row = (size_t)blockIdx.x * R + rl;
     const int S = p.S_tot;
     float Mx = kNegInf, acc = 0.0f, Ls = 0.0f;
     if (row < rows) {
-        const float* ml = p.part_ml + row * S * 2;
+        const float2* ml = (const float2*)p.part_ml + row * S;
         const float* po = p.part_o + row * S * D + d;
         for (int s0 = 0; s0 < S; s0 += kMergeChunk) {
-            float m[kMergeChunk], l[kMergeChunk], o[kMergeChunk];
+            float2 m[kMergeChunk];
+            float o[kMergeChunk];
 #pragma unroll
             for (int k = 0; k < kMergeChunk; ++k) {
-                const bool in = s0 + k < S;
-                const int s = in ? s0 + k : s0;
-                m[k] = ml[2 * s];
-                l[k] = ml[2 * s + 1];
-                o[k] = po[(size_t)s * D];
-                if (!in)
-                    m[k] = kNegInf;
+                if (s0 + k < S) {
+                    m[k] = ml[s0 + k];
+                    o[k] = po[(size_t)(s0 + k) * D];
+                } else {
+                    m[k] = float2{kNegInf, 0.0f};
+                    o[k] = 0.0f;
+                }
             }
             float cm = kNegInf;
 #pragma unroll
             for (int k = 0; k < kMergeChunk; ++k)
-                cm = fmaxf(cm, m[k]);
+                cm = fmaxf(cm, m[k].x);
             const float nm = fmaxf(Mx, cm);
             if (nm != kNegInf) {
                 const float sc = Mx == kNegInf ? 0.0f : fast_exp2(Mx - nm);
@@ -891,9 +1067,9 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(AttnParams p)
                 Ls *= sc;
 #pragma unroll
                 for (int k = 0; k < kMergeChunk; ++k) {
-                    const float w = m[k] == kNegInf ? 0.0f : fast_exp2(m[k] - nm);
+                    const float w = m[k].x == kNegInf ? 0.0f : fast_exp2(m[k].x - nm);
                     acc += w * o[k];
-                    Ls += w * l[k];
+                    Ls += w * m[k].y;
                 }
                 Mx = nm;
             }
@@ -935,7 +1111,7 @@ int resident_per_cu(const AttnParams& p)
     if (hit != 0 && (hit >> 32) == lds)
         return (int)(hit & 0xFFFFFFFFu);
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_split_kernel<C>, kThreads, p.lds_bytes) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_split_kernel<C>, C::THREADS, p.lds_bytes) != hipSuccess)
         n = 1;
     if (n < 1)
         n = 1;
@@ -946,7 +1122,7 @@ int resident_per_cu(const AttnParams& p)
 template <class C>
 hipError_t launch_split(const AttnParams& p, hipStream_t stream)
 {
-    hipLaunchKernelGGL(decode_split_kernel<C>, dim3(p.S_tot, p.B * p.H), dim3(kThreads), p.lds_bytes, stream, p);
+    hipLaunchKernelGGL(decode_split_kernel<C>, dim3(p.S_tot, p.B * p.H), dim3(C::THREADS), p.lds_bytes, stream, p);
     return hipGetLastError();
 }
 
@@ -963,25 +1139,18 @@ auto by_groups(const AttnParams& p, A... args)
     }
 }
 
-template <template <class> class F, int D, bool M16, class... A>
+template <template <class> class F, int D, bool M16, bool PC, class... A>
 auto by_bits(const AttnParams& p, A... args)
 {
-    const bool pc = p.k_axis == KVQ_PER_CHANNEL;
     if (p.k_bits == 8)  // 8-bit codes come as K and V both 8-bit
-        return pc ? by_groups<F, D, 8, 8, true, M16>(p, args...) : by_groups<F, D, 8, 8, false, M16>(p, args...);
+        return by_groups<F, D, 8, 8, PC, M16>(p, args...);
     if (p.k_bits == 4 && p.v_bits == 4)
-        return pc ? by_groups<F, D, 4, 4, true, M16>(p, args...) : by_groups<F, D, 4, 4, false, M16>(p, args...);
+        return by_groups<F, D, 4, 4, PC, M16>(p, args...);
     if (p.k_bits == 4 && p.v_bits == 2)
-        return pc ? by_groups<F, D, 4, 2, true, M16>(p, args...) : by_groups<F, D, 4, 2, false, M16>(p, args...);
+        return by_groups<F, D, 4, 2, PC, M16>(p, args...);
     if (p.k_bits == 2 && p.v_bits == 4)
-        return pc ? by_groups<F, D, 2, 4, true, M16>(p, args...) : by_groups<F, D, 2, 4, false, M16>(p, args...);
-    return pc ? by_groups<F, D, 2, 2, true, M16>(p, args...) : by_groups<F, D, 2, 2, false, M16>(p, args...);
-}
-
-template <template <class> class F, int D, class... A>
-auto by_format(const AttnParams& p, A... args)
-{
-    return p.meta16 ? by_bits<F, D, true>(p, args...) : by_bits<F, D, false>(p, args...);
+        return by_groups<F, D, 2, 4, PC, M16>(p, args...);
+    return by_groups<F, D, 2, 2, PC, M16>(p, args...);
 }
 
 template <class C>
@@ -994,20 +1163,25 @@ struct Resident {
     static int run(const AttnParams& p) { return resident_per_cu<C>(p); }
 };
 
-template <int D>
-int resident_d(const AttnParams& p)
+// The split kernels of one (head size, metadata width, key axis) family:
+// one translation unit each (attn_part.hip, built once per family).
+template <int D, bool M16, bool PC>
+hipError_t launch_split_family(const AttnParams& p, hipStream_t stream)
 {
-    return by_format<Resident, D>(p);
+    return by_bits<LaunchSplit, D, M16, PC>(p, stream);
+}
+
+template <int D, bool M16, bool PC>
+int resident_family(const AttnParams& p)
+{
+    return by_bits<Resident, D, M16, PC>(p);
 }
 
 template <int D>
-hipError_t launch_decode_d(const AttnParams& p, hipStream_t stream)
+hipError_t launch_merge(const AttnParams& p, hipStream_t stream)
 {
-    const hipError_t e = by_format<LaunchSplit, D>(p, stream);
-    if (e != hipSuccess || p.S_tot == 1)
-        return e;
-    const int rows = p.B * p.H_q, per = kThreads / D;
-    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3((rows + per - 1) / per), dim3(kThreads), 0, stream, p);
+    const int rows = p.B * p.H_q, per = kMergeThreads / D;
+    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3((rows + per - 1) / per), dim3(kMergeThreads), 0, stream, p);
     return hipGetLastError();
 }
 

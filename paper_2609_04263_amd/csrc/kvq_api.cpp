@@ -108,7 +108,7 @@ float rotation_constant(int D)
 // cache can need (the split count of a call never exceeds it).
 size_t decode_workspace_layout(const kvq_cache* c, int H_q, size_t* off_ml)
 {
-    int S_max = kvq::decode_split_bound(c->B, c->H) + (c->fmt.flush || c->fmt.sink ? 1 : 0);
+    int S_max = kvq::decode_split_bound(c->B, c->H);
     size_t rows = (size_t)c->B * H_q;
     size_t o_ml = round_up(rows * S_max * c->D * sizeof(float), 256);
     if (off_ml)
@@ -560,25 +560,16 @@ kvq_status decode_setup(const kvq_cache* c, const void* Q, int H_q, float sm_sca
     return KVQ_OK;
 }
 
-// Target workgroups of the split kernel for this call.  With many splits per
-// unit, the fp16 split (sink and window) of every unit takes a slot of the
-// one resident round that the coded splits are planned to fill (one split
-// fewer costs little; workgroups left for a second round cost a whole
-// split).  With few splits per unit, a split fewer would lengthen every
-// split, and the short fp16 splits free their slots early instead.
+// Target workgroups of the split kernel for this call: one resident round.
 int decode_groups(const kvq_cache* c, const kvq::AttnParams& p)
 {
-    const int units = c->B * c->H;
-    int groups = kvq::decode_target_groups(p, c->D);
-    if ((c->fmt.flush || c->fmt.sink) && groups >= 4 * units)
-        groups -= units;
-    return groups;
+    return kvq::decode_target_groups(p, c->D);
 }
 
 void decode_finish_plan(const kvq_cache* c, int groups, kvq::AttnParams* p)
 {
-    kvq::decode_plan(c->B, c->H, groups, p->nq, &p->S_q, &p->bps);
-    p->S_tot = p->S_q + (c->fmt.flush || c->fmt.sink ? 1 : 0);
+    kvq::decode_plan(c->B, c->H, c->D, groups, p->nq, &p->S_q, &p->bps);
+    p->S_tot = p->S_q;
 }
 
 // ------------------------------------------------ static decode scratch
@@ -640,22 +631,17 @@ kvq_status kvq_decode_attn_noalloc(const kvq_cache* c, const void* Q, int H_q, f
         return st;
     // The plan of kvq_decode_attn, with the split count capped so that the
     // partials (D + 2 floats per row and split, the (max, sum) pairs
-    // starting at a 256-byte boundary) fit the scratch.
+    // starting at a 256-byte boundary) fit the scratch; a single split
+    // writes the outputs itself and needs none.
     const size_t rows = (size_t)c->B * H_q;
-    const int fp16_split = c->fmt.flush || c->fmt.sink ? 1 : 0;
     const size_t per_split = rows * ((size_t)c->D + 2) * sizeof(float);
-    const long cap = (long)((KVQ_SCRATCH_BYTES - 256) / per_split) - fp16_split;
+    const long cap = (long)((KVQ_SCRATCH_BYTES - 256) / per_split);
     int groups = decode_groups(c, p);
     const int units = c->B * c->H;
-    if (cap < 1) {
-        // one coded split writes the outputs itself and needs no partials;
-        // an fp16 split always makes two
-        if (fp16_split)
-            return KVQ_ERR_SCRATCH;
+    if (cap < 2)
         groups = units;
-    } else if ((long)groups > cap * units) {
+    else if ((long)groups > cap * units)
         groups = (int)(cap * units);
-    }
     decode_finish_plan(c, groups, &p);
     if (p.S_tot > 1) {
         uint8_t* base = (uint8_t*)scratch_address();

@@ -116,8 +116,8 @@ struct AttnParams {
     int n, nq;            // tail tokens (past the sink; prefill: n - sink, negative inside the sink), coded tokens
     int ring;
     int sink, n_sink;     // sink rows per (b, h), and those holding tokens (min(length, sink))
-    int S_q;              // splits over coded tokens
-    int S_tot;            // S_q (+1 when a window or a sink exists: the fp16 split)
+    int S_q;              // splits over coded tokens (fp16 sink and window blocks are spread over them)
+    int S_tot;            // splits in the grid (= S_q)
     int bps;              // 32-token blocks per split
     int k_bits, v_bits, k_mode, v_mode, k_axis, k_group, v_group;
     int rotate;
@@ -130,9 +130,9 @@ struct AttnParams {
 // Workgroups of the split kernel that fit the device at once (all fields of p
 // that select the kernel instance and its LDS must be set).
 int decode_target_groups(const AttnParams& p, int D);
-// Split count and 32-token blocks per split over nq coded tokens for a
-// target number of workgroups.
-void decode_plan(int B, int H, int groups, int nq, int* S_q, int* bps);
+// Split count (at least 1) and 32-token blocks per split over nq coded
+// tokens for a target number of workgroups of the head size D kernel.
+void decode_plan(int B, int H, int D, int groups, int nq, int* S_q, int* bps);
 // Upper bound of S_q for any coded-token count and target.
 int decode_split_bound(int B, int H);
 // Dynamic LDS of the split kernel.

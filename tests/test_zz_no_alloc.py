@@ -4,9 +4,9 @@ against kvq_decode_attn (partials in a caller workspace), through the C ABI.
 Two calls in a row on one GPU, the second on a smaller cache, so the second
 reuses scratch the first left dirty; with the uncapped plan both entry
 points run the same kernels on the same plan and must agree bit for bit.
-A cache whose partials would not fit is planned with fewer splits (checked
-against the workspace entry point at the float bar), and one that cannot
-fit even two splits is rejected before any launch.
+A cache whose partials would not fit is planned with fewer splits, down to
+a single split that needs no partials (checked against the workspace entry
+point at the float bar).
 """
 import numpy as np
 import pytest
@@ -65,17 +65,13 @@ def test_noalloc_caps_splits_to_the_scratch():
     assert_close(na, ws, what="noalloc (capped splits) vs workspace")
 
 
-def test_noalloc_rejects_what_cannot_fit():
+def test_noalloc_single_split_when_two_do_not_fit():
     from paper_2609_04263_amd import kvq
     kivi = configs.WORKLOADS["llama8b_kivi"].fmt
-    # 4096 rows of D = 128 with an fp16 split: two splits need 4.26 MB
+    # 4096 rows of D = 128: two splits would need 4.26 MB of partials, more
+    # than the 4 MiB scratch, so one split per unit writes the outputs
     B, H, H_q, D = 32, 8, 128, 128
-    gc = filled_cache(kivi, B=B, H=H, D=D, n=200, seed=506)
     assert B * H_q * (D + 2) * 4 * 2 > kvq.SCRATCH_BYTES - 256
-    Q = dev_bf16(synth.queries(507, B, H_q, D))
-    O = torch.zeros((B, H_q, D), dtype=torch.float32, device="cuda")
-    with pytest.raises(kvq.KvqError) as e:
-        gc.decode_attn_noalloc(Q, H_q, 0.125, O)
-    assert e.value.status == kvq.ERR_SCRATCH
-    torch.cuda.synchronize()
-    assert not O.any().item(), "a rejected call must launch nothing"
+    gc = filled_cache(kivi, B=B, H=H, D=D, n=1200, seed=506)
+    na, ws = both(gc, H_q=H_q, seed=507)
+    assert_close(na, ws, what="noalloc (single split) vs workspace")
