@@ -81,10 +81,10 @@ int decode_target_groups(const AttnParams& p, int D)
     return per * compute_units();
 }
 
-void decode_plan(int B, int H, int D, int groups, int nq, int* S_q, int* bps)
+void decode_plan(int B, int H, int waves, int groups, int nq, int* S_q, int* bps)
 {
     const int nblk = (nq + 31) / 32;
-    const int sb = attn::waves_for(D);
+    const int sb = waves;
     if (nblk == 0) {
         // no coded tokens: one split walks the fp16 tokens
         *S_q = 1;
@@ -107,11 +107,17 @@ int decode_split_bound(int B, int H)
     return s < 1 ? 1 : s;
 }
 
+int decode_waves(int D, const kvq_format& f)
+{
+    return attn::waves_for(D, f.k_axis == KVQ_PER_CHANNEL, f.k_bits, f.v_bits);
+}
+
 size_t decode_lds_bytes(int D, const kvq_format& f, int G)
 {
     // the layout is described in attn_impl.h
-    const int nvg = D / f.v_group, W = attn::waves_for(D), np = attn::meta_pairs(D, nvg);
+    const int nvg = D / f.v_group, np = attn::meta_pairs(D, nvg);
     const bool perch = f.k_axis == KVQ_PER_CHANNEL, fp16 = f.flush || f.sink;
+    const int W = decode_waves(D, f);
     const size_t need = attn::lds_waves(D, perch, G) + (size_t)W * attn::lds_per_wave(D, np, perch, G, fp16);
     const size_t merge = (2 * (size_t)W * 16 + (size_t)W * G * D) * sizeof(float);
     return merge > need ? merge : need;

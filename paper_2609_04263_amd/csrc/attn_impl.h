@@ -4,14 +4,17 @@
 // it).  The split kernels are instantiated by attn_part.hip, once per (head
 // size, metadata width, key axis) family; the merge kernels by attn.hip.
 //
-// Work decomposition.  A workgroup of 4 waves handles one (split, sequence,
-// KV head).  The MFMA v_mfma_f32_16x16x32_f16 has 16 columns; the G <= 16
+// Work decomposition.  A workgroup of W waves (waves_for: 4, or at
+// head_dim 128 a whole compute unit of 8 or 12) handles one (split,
+// sequence, KV head).  The MFMA v_mfma_f32_16x16x32_f16 has 16 columns; the G <= 16
 // query heads of the KV head take G of them, so every code is read from HBM
 // once per KV head.  When the value groups of a token times G fit in the 16
 // columns, each value group gets its own copy of the G head columns
 // (column r G + h: head h, value group r) and one pass of the value-side
 // arithmetic serves every group; otherwise groups are taken one per pass.
-// Each wave walks every fourth 32-token block of the split:
+// The split's 32-token blocks are dealt to the waves round robin, in whole
+// rounds of W blocks (a wave whose block lies past the end skips its
+// arithmetic but keeps the loop shape, so the prefetch wait stays exact):
 //
 //   loads     the cache stores each block's code pieces in the order of
 //             this kernel's MFMA operands, so a lane reads its key and value
@@ -41,12 +44,15 @@
 //             sum_t p_t z'_tg accumulated per lane in fp32.
 //
 // Every MFMA product is exact (fp16 x fp16 in fp32) and accumulation is
-// fp32.  Tokens of an fp16 window are handled by one extra split per KV head
-// that feeds the fp16 values to the same MFMAs.  Each split writes an
-// unnormalized partial (m, l, o) and a second kernel merges them (a kernel
-// boundary instead of an in-kernel cross-workgroup handoff, whose
-// agent-scope fences write back and invalidate the L2 on gfx950).  With a
-// single split the first kernel writes the outputs itself.
+// fp32.  Tokens of an fp16 window (a sink prefix, or the unflushed tail) are
+// 32-token blocks too: after its coded blocks every split takes a share of
+// them, round robin over splits and waves, reads the fp16 keys as MFMA
+// operands directly and the values through a transposed copy in the wave's
+// LDS region.  The waves of a workgroup then merge their states in LDS.
+// Each split writes an unnormalized partial (m, l, o) and a second kernel
+// merges them (a kernel boundary instead of an in-kernel cross-workgroup
+// handoff, whose agent-scope fences write back and invalidate the L2 on
+// gfx950).  With a single split the first kernel writes the outputs itself.
 #pragma once
 
 #include <atomic>
@@ -70,19 +76,21 @@ __host__ __device__ constexpr int meta_pairs(int D, int nvg)
     return ((D + 32 * nvg) / 4 + 63) / 64;
 }
 
-// Waves per split workgroup.  Two waves of the head_dim 128 kernel fit a
-// SIMD, so a workgroup of eight fills a compute unit: with as many (sequence,
-// KV head) units as compute units, one split per unit covers the device and
-// no merge is needed.  The other head sizes use four.
-__host__ __device__ constexpr int waves_for(int D)
+// Waves per split workgroup.  At head_dim 128 one workgroup fills a compute
+// unit: eight waves (two per SIMD), or twelve (three per SIMD) for 2-bit
+// per-channel keys with 2-bit values, whose state fits 168 registers.  With
+// as many (sequence, KV head) units as compute units, one split per unit
+// then covers the device and no merge is needed.  The other head sizes use
+// four.
+__host__ __device__ constexpr int waves_for(int D, bool perch, int kbits, int vbits)
 {
-    return D == 128 ? 8 : 4;
+    return D != 128 ? 4 : (perch && kbits == 2 && vbits == 2) ? 12 : 8;
 }
 
 // Compile-time shape of one kernel instance.
 template <int D_, int KBITS_, int VBITS_, bool PERCH_, int VGS_, bool M16_ = false>
 struct Cfg {
-    static constexpr int WAVES = waves_for(D_), THREADS = 64 * WAVES;
+    static constexpr int WAVES = waves_for(D_, PERCH_, KBITS_, VBITS_), THREADS = 64 * WAVES;
     static constexpr int D = D_, KBITS = KBITS_, VBITS = VBITS_, VGS = VGS_;
     static constexpr bool PERCH = PERCH_;
     static constexpr bool M16 = M16_;           // fp16 scales and offsets
@@ -1008,11 +1016,12 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
 }
 
 // Waves per SIMD the register allocation is held to: 3 at head_dim 64 (the
-// block state fits without spills), fewer for wider heads.
+// block state fits without spills), a workgroup's share of a compute unit at
+// head_dim 128, 1 at head_dim 256.
 template <class C>
 constexpr int split_waves_per_simd()
 {
-    return C::D == 64 ? 3 : C::D == 128 ? 2 : 1;
+    return C::D == 64 ? 3 : C::D == 128 ? C::WAVES / 4 : 1;
 }
 
 template <class C>

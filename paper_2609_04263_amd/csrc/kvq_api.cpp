@@ -568,7 +568,7 @@ int decode_groups(const kvq_cache* c, const kvq::AttnParams& p)
 
 void decode_finish_plan(const kvq_cache* c, int groups, kvq::AttnParams* p)
 {
-    kvq::decode_plan(c->B, c->H, c->D, groups, p->nq, &p->S_q, &p->bps);
+    kvq::decode_plan(c->B, c->H, kvq::decode_waves(c->D, c->fmt), groups, p->nq, &p->S_q, &p->bps);
     p->S_tot = p->S_q;
 }
 

@@ -130,9 +130,11 @@ struct AttnParams {
 // Workgroups of the split kernel that fit the device at once (all fields of p
 // that select the kernel instance and its LDS must be set).
 int decode_target_groups(const AttnParams& p, int D);
-// Split count (at least 1) and 32-token blocks per split over nq coded
-// tokens for a target number of workgroups of the head size D kernel.
-void decode_plan(int B, int H, int D, int groups, int nq, int* S_q, int* bps);
+// Waves per workgroup of the split kernel for head size D and format f.
+int decode_waves(int D, const kvq_format& f);
+// Split count (at least 1) and 32-token blocks per split (a multiple of
+// `waves`) over nq coded tokens for a target number of workgroups.
+void decode_plan(int B, int H, int waves, int groups, int nq, int* S_q, int* bps);
 // Upper bound of S_q for any coded-token count and target.
 int decode_split_bound(int B, int H);
 // Dynamic LDS of the split kernel.
