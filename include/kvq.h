@@ -162,8 +162,9 @@ kvq_status kvq_cache_restore(kvq_cache* cache, int n);
 /* Free the host handle (not the storage). */
 void kvq_cache_destroy(kvq_cache* cache);
 
-/* Workspace bytes kvq_project_qkv needs for M rows and adapter rank r
- * (the fp32 adapter activations (alpha/r) A h, M x 3r). */
+/* Workspace bytes kvq_project_qkv and kvq_project_append need for M rows and
+ * adapter rank r: the fp32 adapter activations A h, M x 3r, times 16 for
+ * M <= 32 (partial sums over up to 16 slices of d_in).  0 when r is 0. */
 kvq_status kvq_project_workspace_bytes(int M, int rank, size_t* bytes);
 
 /* Adapted Q/K/V projection, Eq. (1)-(2) with the explicit adapter branch of

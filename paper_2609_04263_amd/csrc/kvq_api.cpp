@@ -255,7 +255,7 @@ kvq_status kvq_project_workspace_bytes(int M, int rank, size_t* bytes)
 {
     if (!bytes || M < 0 || rank < 0 || rank > 64)
         return KVQ_ERR_ARG;
-    *bytes = (size_t)M * 3 * rank * sizeof(float);
+    *bytes = kvq::project_workspace_bytes(M, rank);
     return KVQ_OK;
 }
 
@@ -275,18 +275,19 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
     if (rank > 0) {
         if (!A || !Bm || !aligned16(A) || !aligned16(Bm) || !workspace || !aligned16(workspace))
             return KVQ_ERR_ARG;
-        if (ws_bytes < (size_t)M * 3 * rank * sizeof(float))
+        if (ws_bytes < kvq::project_workspace_bytes(M, rank))
             return KVQ_ERR_WORKSPACE;
     }
     hipStream_t s = (hipStream_t)stream;
     const int N = d_q + 2 * d_kv;
-    if (M <= 32 && rank <= 16) {
-        // decode, small rank: one fused kernel computes the adapter activations itself
+    if (M <= 32) {
+        // decode: partial adapter activations over K slices, then the weight stream
         kvq::ProjParams p = {};
         p.x = (const uint16_t*)H;
         p.w = (const uint16_t*)W;
         p.a = (const uint16_t*)A;
         p.bm = (const uint16_t*)Bm;
+        p.t = (const float*)workspace;
         p.y0 = (uint16_t*)Q;
         p.y1 = (uint16_t*)K;
         p.y2 = (uint16_t*)V;
@@ -351,7 +352,7 @@ kvq_status kvq_project_append(const void* H, int M, int d_in, const void* W, int
     if (rank > 0) {
         if (!A || !Bm || !aligned16(A) || !aligned16(Bm) || !workspace || !aligned16(workspace))
             return KVQ_ERR_ARG;
-        if (ws_bytes < (size_t)M * 3 * rank * sizeof(float))
+        if (ws_bytes < kvq::project_workspace_bytes(M, rank))
             return KVQ_ERR_WORKSPACE;
     }
     if ((long long)c->n + n_new > c->T_max)

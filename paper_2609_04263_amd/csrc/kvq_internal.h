@@ -58,7 +58,8 @@ struct ProjParams {
     const uint16_t* x;    // bf16 [M][K]  (hidden states)
     const uint16_t* w;    // bf16 [N][K]  (weight rows)
     const uint16_t* bm;   // bf16 [N][rank] adapter up-projection rows (rank > 0)
-    const float* t;       // fp32 [M][3 rank] scaled adapter activations (rank > 0, two-pass path)
+    const float* t;       // rank > 0: fp32 [M][3 rank] scaled adapter activations (M > 32), or for
+                          // M <= 32 the workspace of [ks][M][3 rank] unscaled partial sums over K slices
     const uint16_t* a;    // bf16 [3 rank][K] adapter down-projections (rank > 0, fused decode path)
     uint16_t* y0;         // bf16 outputs: columns [0, n1) -> y0, [n1, n2) -> y1, [n2, N) -> y2
     uint16_t* y1;
@@ -69,6 +70,7 @@ struct ProjParams {
     int rank;
     float scale;          // multiplies the fp32 output (activation pass); the adapter scale (fused path)
     int nxcd;             // XCDs the large-M tile order spreads over (set at launch)
+    int tslices;          // K slices of the partial adapter activations (M <= 32, set at launch)
     // Fused append (large-M path only): with fuse set, the K and V tiles are
     // coded into the cache instead of stored.  Rows are (sequence, token)
     // pairs, cn_new tokens per sequence starting at cache position cn0 (a
@@ -84,6 +86,13 @@ struct ProjParams {
     int k_bits, v_bits, k_mode, v_mode, k_group, v_group, meta16;
 };
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
+// Upper bound on the K slices of the decode path's partial adapter activations.
+constexpr int kProjTSlices = 16;
+// Workspace bytes of the projection for M rows and adapter rank r.
+inline size_t project_workspace_bytes(int M, int rank)
+{
+    return (size_t)(M <= 32 ? kProjTSlices : 1) * M * 3 * rank * sizeof(float);
+}
 
 // ---------------------------------------------------------------- merge
 struct MergeParams {

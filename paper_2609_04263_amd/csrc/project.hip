@@ -7,14 +7,10 @@
 //      of the same accumulators: t_p (split into bf16 hi + lo parts) times
 //      B_p^T, then one rounding to bf16 and routing of the columns to Q/K/V.
 //
-// M <= 32 (decode: one token per sequence) runs as one fused kernel that
-// streams the weights from HBM: a workgroup owns 16 weight rows and its
-// eight waves split the reduction dimension, each issuing its 16-byte loads
-// of W, H and the adapter rows A_p in one batch.  The same H fragments feed
-// both Y = H W^T and the adapter activations t = H A_p^T (its own copy per
-// workgroup: the adapter rows are small and stay in L2), which are reduced
-// across waves in LDS and applied as the K-extension.  Larger M (prefill)
-// uses the two passes with a 128x128 tiled GEMM staged through LDS.
+// M <= 32 (decode: one token per sequence) streams the weights from HBM
+// with whole-line loads staged through LDS; its activation pass is split
+// over K (see the decode section).  Larger M (prefill) uses a 256x256 tiled
+// GEMM staged through LDS, or a 128x128 one for small shapes.
 
 #include <atomic>
 
@@ -116,231 +112,461 @@ __device__ __forceinline__ bf16x8 lora_weight_operand(const ProjParams& p, int n
     return __builtin_bit_cast(bf16x8, a);
 }
 
-// ----------------------------------------------------------- fused decode
-// Workgroup: weight rows [n0, n0 + 16 R) x all M (<= 16 MT) tokens, 8 waves.
-// Each wave owns one eighth of the reduction dimension for all R row tiles,
-// so one H fragment (and one adapter fragment) serves R weight tiles: the
-// rows of H and A_p, which every workgroup reads, cost 1/R of the weight
-// traffic instead of as much as it.  Workgroups start their waves at
-// different eighths so that concurrent workgroups read different lines.
-// MFMA roles: Y: A = W rows (16 weight rows), B = H^T (16 tokens);
-//             t: A = H rows (16 tokens), B = A_p^T (16 adapter rows).
-// Output lane layout: token = 16 mt + (lane % 16), row n0 + 16 rt + 4 qg + i.
-constexpr int kDecWaves = 8;
+// ----------------------------------------------------------------- decode
+// M <= 32 tokens (decode: one per sequence).  The weights stream from HBM in
+// proj_stream_kernel: Y = H W^T, then the adapter branch (scale t_p) B_p^T
+// as a K-extension of the same accumulators (t split into bf16 hi + lo), one
+// rounding to bf16, routed to Q/K/V.  The adapter activations t = H A_p^T
+// come from one of two places:
+//   rank <= 16   the stream kernel computes them itself: its workgroups
+//                stage the 16 rows of A_p along with W and H (A_p stays in
+//                L2, read by every workgroup of projection p);
+//   rank > 16    proj_tpart_kernel first writes partial sums over at most
+//                kTSlices K slices (fp32 [slice][M][3r] in the workspace),
+//                one workgroup per (16 adapter rows, K slice), so that the
+//                larger A is read once; the stream kernel sums the slices.
+//
+// proj_stream_kernel: a workgroup owns RG = 8 G consecutive weight rows (G
+// chosen so that the row groups cover the compute units about once) and all
+// of K, with eight waves.  K is walked in 64-wide steps, step s going to wave
+// s % 8, so the waves read 1 KiB runs of each row together.  Every global
+// load is 16 bytes per lane over whole 128-byte lines: eight rows x 128 bytes
+// per instruction.  (An MFMA operand fragment is 16 rows x 64 bytes, half
+// lines, which the load path serves at a fraction of the rate, from L2 as
+// well as from HBM.)  A wave writes its step's rows to its own LDS region
+// (row pitch 160 bytes, which measured an order of magnitude fewer bank
+// conflicts than 128 or 144 for these line writes and fragment reads), reads them back as v_mfma_f32_16x16x32_bf16 fragments
+// (Y: A = 16 weight rows, B = 16 tokens; t: A = 16 tokens, B = 16 adapter
+// rows) and accumulates.  Three register sets keep two steps of loads in
+// flight while one is consumed.  The waves' partial sums are reduced in LDS.
+// Weight tiles: 16 rows at offsets 0 and RG - 16 of the group (RG = 24: rows
+// 8..15 are computed twice and stored once; RG = 8: the upper 8 fragment
+// rows are never written and their outputs never stored).  A group that
+// straddles a projection boundary also stages the second projection's
+// adapter rows.  No group touches three projections: d_q and d_kv are
+// multiples of 16 and a group of RG <= 32 rows starts at a multiple of RG, so
+// it cannot hold rows on both sides of a 16-row (or longer) K block.
+constexpr int kSWaves = 8;
+constexpr int kSPitch = 160;   // bytes per staged row: 128 + 32
+constexpr int kSXor = 0;       // chunk c of staged row r sits at chunk position c ^ (kSXor ? r & 7 : 0)
 
-template <int R, int MT, int NKT, bool TLOAD>
-struct DecShape {
-    static constexpr int NV = R * MT + MT * NKT;       // floatx4 partials per lane
-    static constexpr int NKK = (16 * NKT + 31) / 32;   // 32-wide rank chunks of the fused K-extension
-    static constexpr int PER_STEP = R + MT + NKT;      // 16-byte loads per K-step
-    static constexpr int U = PER_STEP <= 3 ? 8 : PER_STEP <= 6 ? 4 : 2;  // K-steps per load batch
-    static constexpr size_t LDS = sizeof(floatx4) * kDecWaves * NV * 64 + sizeof(float) * 16 * MT * 16 * NKT;
+__device__ __forceinline__ int stage_off(int row, int chunk)
+{
+    return row * kSPitch + 16 * (kSXor ? (chunk ^ (row & 7)) : chunk);
+}
+constexpr int kTSlices = kProjTSlices;
+constexpr int kTWaves = 4;
+
+template <int G, int GH, bool FA>
+struct StreamShape {
+    static constexpr int RG = 8 * G;                   // weight rows per workgroup
+    static constexpr int NTW = G <= 2 ? 1 : 2;         // 16-row weight tiles
+    static constexpr int MT = (GH + 1) / 2;            // 16-token tiles
+    static constexpr int WR = RG < 16 ? 16 : RG;       // staged weight rows
+    static constexpr int HR = 16 * MT;                 // staged token rows
+    static constexpr int AR = FA ? 32 : 0;             // staged adapter rows (two projections)
+    static constexpr int WAVE_BYTES = (WR + HR + AR) * kSPitch;
+    static constexpr int STAGE_BYTES = kSWaves * WAVE_BYTES;
+    static constexpr int NSLOT = NTW * MT + (FA ? 2 * MT : 0);  // reduced accumulators
+    static constexpr int RED_BYTES = kSWaves * NSLOT * 64 * 16;
+    static constexpr int TL_OFFSET = STAGE_BYTES > RED_BYTES ? STAGE_BYTES : RED_BYTES;
 };
 
-template <int R, int MT, int NKT, bool TLOAD>
-__global__ __launch_bounds__(kDecWaves * 64) void proj_decode_kernel(ProjParams p)
+// LDS bytes for the scaled adapter activations: two projections x M x rank fp32.
+inline size_t stream_tl_bytes(int M, int rank)
 {
-    using S = DecShape<R, MT, NKT, TLOAD>;
-    constexpr int NV = S::NV, NKK = S::NKK, U = S::U;
-    extern __shared__ floatx4 red[];  // [kDecWaves][NV][64], then t [16 MT][16 NKT]
+    return (size_t)2 * M * rank * sizeof(float);
+}
+
+template <int G, int GH, bool FA>
+struct StreamRegs {
+    u32x4 w[G], h[GH], a[FA ? 2 : 1], a2[FA ? 2 : 1];
+};
+
+template <int G, int GH, bool FA>
+__global__ __launch_bounds__(kSWaves * 64, 1) void proj_stream_kernel(ProjParams p)
+{
+    using S = StreamShape<G, GH, FA>;
+    using Regs = StreamRegs<G, GH, FA>;
+    constexpr int RG = S::RG, NTW = S::NTW, MT = S::MT, WR = S::WR, HR = S::HR;
+    extern __shared__ __align__(16) uint8_t slds[];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, qg = lane >> 4;
-    const int n0 = blockIdx.x * 16 * R;
-    const int proj = proj_of(p, n0);  // tiles never straddle projections (see launch_project)
-    const int steps = p.K / 32;
-    const int per = (steps + kDecWaves - 1) / kDecWaves;
-    const int chunk = (wave + (int)blockIdx.x) % kDecWaves;
-    const int s_begin = chunk * per, s_end = min(steps, s_begin + per);
+    const int r0 = blockIdx.x * RG;
+    const int S64 = p.K / 64;
+    const int NI = S64 > wave ? (S64 - wave + kSWaves - 1) / kSWaves : 0;  // this wave's steps
+    // projections this group touches
+    const int rend = min(r0 + RG, p.N);
+    const int p_lo = proj_of(p, r0), p_hi = proj_of(p, rend - 1);
+    const bool dual = FA && p_hi != p_lo;
 
-    const uint16_t* wp[R];
-    bool wok[R];
+    // line-load addresses: octet o covers rows 8 o + lane / 8, 16 bytes at column 8 (lane % 8)
+    const int lrow = lane >> 3, lcol = 8 * (lane & 7);
+    const uint16_t* wrow[G];
 #pragma unroll
-    for (int rt = 0; rt < R; ++rt) {
-        wp[rt] = p.w + (size_t)min(n0 + 16 * rt + r, p.N - 1) * p.K + 8 * qg;
-        wok[rt] = n0 + 16 * rt + r < p.N;
+    for (int o = 0; o < G; ++o)
+        wrow[o] = p.w + (size_t)min(r0 + 8 * o + lrow, p.N - 1) * p.K + lcol;
+    const uint16_t* hrow[GH];
+#pragma unroll
+    for (int o = 0; o < GH; ++o)
+        hrow[o] = p.x + (size_t)min(8 * o + lrow, p.M - 1) * p.K + lcol;
+    const uint16_t *arow[2], *arow2[2];
+#pragma unroll
+    for (int o = 0; o < 2; ++o) {
+        const int j = min(8 * o + lrow, max(p.rank, 1) - 1);
+        arow[o] = FA ? p.a + (size_t)(p_lo * p.rank + j) * p.K + lcol : nullptr;
+        arow2[o] = FA ? p.a + (size_t)(p_hi * p.rank + j) * p.K + lcol : nullptr;
     }
-    const uint16_t* xp[MT];
-    bool xok[MT];
+    uint8_t* region = slds + wave * S::WAVE_BYTES;
+
+    // workgroups start their walk at different steps, so that the workgroups of
+    // an XCD do not all read the same lines of H and A at the same time
+    const int rot = NI > 0 ? (int)(blockIdx.x % (unsigned)NI) : 0;
+    auto issue = [&](Regs& b, int i) {
+        int ii = min(i, max(NI - 1, 0)) + rot;
+        ii = ii >= NI ? ii - NI : ii;
+        const int j = min(wave + kSWaves * ii, S64 - 1);
+        const size_t k = (size_t)64 * j;
+#pragma unroll
+        for (int o = 0; o < G; ++o)
+            b.w[o] = __builtin_nontemporal_load((const u32x4*)(wrow[o] + k));
+#pragma unroll
+        for (int o = 0; o < GH; ++o)
+            b.h[o] = *(const u32x4*)(hrow[o] + k);
+        if constexpr (FA) {
+#pragma unroll
+            for (int o = 0; o < 2; ++o)
+                b.a[o] = *(const u32x4*)(arow[o] + k);
+            if (dual) {
+#pragma unroll
+                for (int o = 0; o < 2; ++o)
+                    b.a2[o] = *(const u32x4*)(arow2[o] + k);
+            }
+        }
+        // keep the loads ahead of the step consumed next (the scheduler would sink them)
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    floatx4 acc[NTW][MT], tacc[MT][FA ? 2 : 1];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-        xp[mt] = p.x + (size_t)min(16 * mt + r, p.M - 1) * p.K + 8 * qg;
-        xok[mt] = 16 * mt + r < p.M;
+#pragma unroll
+        for (int tw = 0; tw < NTW; ++tw)
+            acc[tw][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int u = 0; u < (FA ? 2 : 1); ++u)
+            tacc[mt][u] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
-    const uint16_t* ap[NKT > 0 ? NKT : 1];
-    bool aok[NKT > 0 ? NKT : 1];
+    auto frag = [&](int row, int hf) {
+        return __builtin_bit_cast(bf16x8, *(const u32x4*)(region + stage_off(row, 4 * hf + qg)));
+    };
+    // line writes: octet starting at staged row r8 (a multiple of 8)
+    auto put = [&](int r8, const u32x4& v) { *(u32x4*)(region + stage_off(r8 + lrow, lane & 7)) = v; };
+    auto consume = [&](const Regs& b) {
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) {
-        ap[kt] = p.a + (size_t)(proj * p.rank + min(16 * kt + r, p.rank - 1)) * p.K + 8 * qg;
-        aok[kt] = 16 * kt + r < p.rank;
-    }
-
-    // the adapter up-projection operands of this wave's row tile (used after
-    // the reduction) are loaded now, so that their latency overlaps the loop
-    bf16x8 bop[NKK > 0 ? NKK : 1];
+        for (int o = 0; o < G; ++o)
+            put(8 * o, b.w[o]);
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk)
-        bop[kk] = wave < R ? lora_weight_operand(p, n0 + 16 * (wave < R ? wave : 0) + r, proj, kk, qg) : zero_bf16x8();
-
-    floatx4 acc[R][MT], tacc[MT][NKT > 0 ? NKT : 1];
+        for (int o = 0; o < GH; ++o)
+            put(WR + 8 * o, b.h[o]);
+        if constexpr (FA) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
+            for (int o = 0; o < 2; ++o)
+                put(WR + HR + 8 * o, b.a[o]);
+            if (dual) {
 #pragma unroll
-        for (int rt = 0; rt < R; ++rt)
-            acc[rt][mt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
-            tacc[mt][kt] = floatx4{0.f, 0.f, 0.f, 0.f};
-    }
-    for (int s = s_begin; s < s_end; s += U) {
-        bf16x8 wv[R][U], xv[MT][U], av[NKT > 0 ? NKT : 1][U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const bool in = s + u < s_end;
-#pragma unroll
-            for (int rt = 0; rt < R; ++rt)
-                wv[rt][u] = (in && wok[rt]) ? load_bf16x8(wp[rt] + 32 * (s + u)) : zero_bf16x8();
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                xv[mt][u] = (in && xok[mt]) ? load_bf16x8(xp[mt] + 32 * (s + u)) : zero_bf16x8();
-#pragma unroll
-            for (int kt = 0; kt < NKT; ++kt)
-                av[kt][u] = (in && aok[kt]) ? load_bf16x8(ap[kt] + 32 * (s + u)) : zero_bf16x8();
+                for (int o = 0; o < 2; ++o)
+                    put(WR + HR + 16 + 8 * o, b.a2[o]);
+            }
         }
 #pragma unroll
-        for (int u = 0; u < U; ++u)
+        for (int hf = 0; hf < 2; ++hf) {
+            bf16x8 wf[NTW], xf[MT];
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+            for (int tw = 0; tw < NTW; ++tw)
+                wf[tw] = frag((tw == NTW - 1 ? (RG < 16 ? 0 : RG - 16) : 16 * tw) + r, hf);
 #pragma unroll
-                for (int rt = 0; rt < R; ++rt)
-                    acc[rt][mt] = mfma16_bf16(wv[rt][u], xv[mt][u], acc[rt][mt]);
+            for (int mt = 0; mt < MT; ++mt)
+                xf[mt] = frag(WR + 16 * mt + r, hf);
 #pragma unroll
-                for (int kt = 0; kt < NKT; ++kt)
-                    tacc[mt][kt] = mfma16_bf16(xv[mt][u], av[kt][u], tacc[mt][kt]);
+            for (int tw = 0; tw < NTW; ++tw)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    acc[tw][mt] = mfma16_bf16(wf[tw], xf[mt], acc[tw][mt]);
+            if constexpr (FA) {
+                const bf16x8 af = frag(WR + HR + r, hf);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    tacc[mt][0] = mfma16_bf16(xf[mt], af, tacc[mt][0]);
+                if (dual) {
+                    const bf16x8 af2 = frag(WR + HR + 16 + r, hf);
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt)
+                        tacc[mt][1] = mfma16_bf16(xf[mt], af2, tacc[mt][1]);
+                }
             }
-    }
-    // reduce the eight waves' partials: slot v of every wave -> wave v % 8 sums it
+        }
+    };
+
+    float* tl = (float*)(slds + S::TL_OFFSET);  // scaled t: [p - p_lo][M][rank]
+    // epilogue slot of this wave (Y tile tw, token tile mt; waves below NTW MT) and
+    // the extension's weight operands B_p, loaded now so that their latency
+    // overlaps the main loop
+    const int tw = wave / MT, mt = wave % MT;
+    const int off = tw >= NTW - 1 ? (RG < 16 ? 0 : RG - 16) : 16 * tw;  // tile's first row in the group
+    const int nk = (p.rank + 31) / 32;
+    bf16x8 bop[2][2];
 #pragma unroll
-    for (int rt = 0; rt < R; ++rt)
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+            bop[u][kk] = (wave < NTW * MT && p_lo + u <= p_hi && kk < nk)
+                             ? lora_weight_operand(p, r0 + off + r, p_lo + u, kk, qg)
+                             : zero_bf16x8();
+    Regs b0, b1, b2;
+    issue(b0, 0);
+    issue(b1, 1);
+    if (!FA && p.rank > 0) {
+        // sum the partial activations of the slices
+        const int per = p.M * p.rank, n = (p_hi - p_lo + 1) * per, ld = 3 * p.rank;
+        for (int e = threadIdx.x; e < n; e += kSWaves * 64) {
+            const int pj = e / per, m = (e % per) / p.rank, k = e % p.rank;
+            const float* src = p.t + (size_t)m * ld + (p_lo + pj) * p.rank + k;
+            float v[kTSlices];
+#pragma unroll
+            for (int s = 0; s < kTSlices; ++s)
+                v[s] = src[(size_t)min(s, p.tslices - 1) * p.M * ld];
+            float sum = 0.0f;
+#pragma unroll
+            for (int s = 0; s < kTSlices; ++s)
+                sum += s < p.tslices ? v[s] : 0.0f;
+            tl[e] = sum * p.scale;
+        }
+    }
+    int i = 0;
+    for (; i + 5 <= NI; i += 3) {
+        issue(b2, i + 2);
+        consume(b0);
+        issue(b0, i + 3);
+        consume(b1);
+        issue(b1, i + 4);
+        consume(b2);
+    }
+    switch (NI - i) {
+    case 4:
+        issue(b2, i + 2);
+        consume(b0);
+        issue(b0, i + 3);
+        consume(b1);
+        consume(b2);
+        consume(b0);
+        break;
+    case 3:
+        issue(b2, i + 2);
+        consume(b0);
+        consume(b1);
+        consume(b2);
+        break;
+    case 2:
+        consume(b0);
+        consume(b1);
+        break;
+    case 1:
+        consume(b0);
+        break;
+    default:
+        break;
+    }
+
+    // reduce the waves' partials: slot v of every wave -> wave v sums it
+    // (slots: Y tiles tw MT + mt, then the activations NTW MT + 2 mt + u)
+    __syncthreads();
+    floatx4* red = (floatx4*)slds;
+    constexpr int NS = S::NSLOT;
+#pragma unroll
+    for (int tw = 0; tw < NTW; ++tw)
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
-            red[(wave * NV + rt * MT + mt) * 64 + lane] = acc[rt][mt];
+            red[(wave * NS + tw * MT + mt) * 64 + lane] = acc[tw][mt];
+    if constexpr (FA) {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
-            red[(wave * NV + R * MT + mt * NKT + kt) * 64 + lane] = tacc[mt][kt];
+            for (int u = 0; u < 2; ++u)
+                red[(wave * NS + NTW * MT + 2 * mt + u) * 64 + lane] = tacc[mt][u];
+    }
     __syncthreads();
-    for (int v = wave; v < NV; v += kDecWaves) {
+    floatx4 out = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int v = wave; v < NS; v += kSWaves) {
         floatx4 sum = red[v * 64 + lane];
 #pragma unroll
-        for (int w = 1; w < kDecWaves; ++w)
-            sum += red[(w * NV + v) * 64 + lane];
-        red[v * 64 + lane] = sum;  // wave 0's slots hold the totals
-    }
-    if constexpr (NKT > 0) {
-        __syncthreads();
-        // t[m][k] = scale * total, from the accumulator layout (lane: k = 16 kt + r,
-        // m = 16 mt + 4 qg + i) to rows of m after the partial slots
-        float* tl = (float*)(red + kDecWaves * NV * 64);
-        constexpr int TK = 16 * NKT;
-        if (wave == 0) {
+        for (int w = 1; w < kSWaves; ++w)
+            sum += red[(w * NS + v) * 64 + lane];
+        if (v < NTW * MT) {
+            out = sum;
+        } else if (FA) {
+            // activations: lane holds adapter row r (k), tokens 16 mt + 4 qg + e
+            const int mt = (v - NTW * MT) / 2, u = (v - NTW * MT) % 2;
+            if (u == 0 || dual) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-                for (int kt = 0; kt < NKT; ++kt) {
-                    const floatx4 tv = red[(R * MT + mt * NKT + kt) * 64 + lane];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        tl[(16 * mt + 4 * qg + i) * TK + 16 * kt + r] = tv[i] * p.scale;
+                for (int e = 0; e < 4; ++e) {
+                    const int m = 16 * mt + 4 * qg + e;
+                    if (m < p.M && r < p.rank)
+                        tl[((size_t)u * p.M + m) * p.rank + r] = sum[e] * p.scale;
                 }
+            }
         }
+    }
+    if constexpr (FA)
         __syncthreads();
-        if (wave >= R)
-            return;
-        // wave rt applies the K-extension to row tile rt
-        const int rt = wave;
-        floatx4 out[MT];
+    if (wave >= NTW * MT)
+        return;
+    if (p.rank > 0) {
+        const int m = 16 * mt + r;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-            out[mt] = red[(rt * MT + mt) * 64 + lane];
+        for (int u = 0; u < 2; ++u) {
+            if (p_lo + u > p_hi)
+                break;
+            const float* tp = tl + (size_t)u * p.M * p.rank + (size_t)min(m, p.M - 1) * p.rank;
 #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) {
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
+            for (int kk = 0; kk < 2; ++kk) {
+                if (kk >= nk)
+                    break;
                 float v[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const int k = 32 * kk + 8 * qg + e;
-                    v[e] = k < TK ? tl[(16 * mt + r) * TK + k] : 0.0f;
+                    v[e] = (m < p.M && k < p.rank) ? tp[k] : 0.0f;
                 }
                 bf16x8 hi, lo;
                 split_bf16x8(v, &hi, &lo);
-                out[mt] = mfma16_bf16(bop[kk], hi, out[mt]);
-                out[mt] = mfma16_bf16(bop[kk], lo, out[mt]);
+                out = mfma16_bf16(bop[u][kk], hi, out);
+                out = mfma16_bf16(bop[u][kk], lo, out);
             }
         }
+    }
+    // lane: token 16 mt + r, rows off + 4 qg .. + 3 of the group (one projection: boundaries are multiples of 16)
+    const int m = 16 * mt + r, lr = off + 4 * qg, n = r0 + lr;
+    const bool mine = lr >= 16 * tw && lr < RG;  // rows this tile stores
+    if (!mine || m >= p.M || n >= p.N)
+        return;
+    uint16_t o4[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        o4[e] = f32_to_bf16(out[e]);
+    const uint2 pk = {o4[0] | ((uint32_t)o4[1] << 16), o4[2] | ((uint32_t)o4[3] << 16)};
+    uint16_t* dst;
+    if (n < p.n1)
+        dst = p.y0 + (size_t)m * p.n1 + n;
+    else if (n < p.n2)
+        dst = p.y1 + (size_t)m * (p.n2 - p.n1) + (n - p.n1);
+    else
+        dst = p.y2 + (size_t)m * (p.N - p.n2) + (n - p.n2);
+    *(uint2*)dst = pk;
+}
+
+// Partial adapter activations: workgroup (jt, ks) computes
+// tpart[ks][m][16 jt + j] = sum over its K slice of H[m][k] A[16 jt + j][k]
+// (unscaled), four waves over the slice's 32-wide steps, reduced in LDS.
+// MFMA roles: A = H rows (16 tokens), B = A^T (16 adapter rows).
+template <int MT>
+__global__ __launch_bounds__(kTWaves * 64) void proj_tpart_kernel(ProjParams p, int slice)
+{
+    __shared__ floatx4 red[kTWaves][MT][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, qg = lane >> 4;
+    const int jt = blockIdx.x, ks = blockIdx.y;
+    const int rows = 3 * p.rank;
+    const int k0 = ks * slice, k1 = min(p.K, k0 + slice);
+    const uint16_t* ap = p.a + (size_t)min(16 * jt + r, rows - 1) * p.K + 8 * qg;
+    const uint16_t* xp[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+        xp[mt] = p.x + (size_t)min(16 * mt + r, p.M - 1) * p.K + 8 * qg;
+    floatx4 acc[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+        acc[mt] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int k = k0 + 32 * wave; k < k1; k += 32 * kTWaves) {
+        const bf16x8 av = load_bf16x8(ap + k);
+        bf16x8 xv[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                store_out(p, 16 * mt + r, n0 + 16 * rt + 4 * qg + i, out[mt][i]);
-    } else {
-        __syncthreads();
-        if (wave >= R)
-            return;
-        const int rt = wave;
-        floatx4 out[MT];
+            xv[mt] = load_bf16x8(xp[mt] + k);
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
-            out[mt] = red[(rt * MT + mt) * 64 + lane];
-        if (TLOAD && p.rank > 0) {
-            // K-extension with the activations of a separate pass (fp32 in p.t)
-            const int nk = (p.rank + 31) / 32;
-            for (int kk = 0; kk < nk; ++kk) {
-                const bf16x8 bop = lora_weight_operand(p, n0 + 16 * rt + r, proj, kk, qg);
+            acc[mt] = mfma16_bf16(xv[mt], av, acc[mt]);
+    }
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    bf16x8 hi, lo;
-                    lora_token_operand(p, 16 * mt + r, proj, kk, qg, &hi, &lo);
-                    out[mt] = mfma16_bf16(bop, hi, out[mt]);
-                    out[mt] = mfma16_bf16(bop, lo, out[mt]);
-                }
-            }
-        }
+    for (int mt = 0; mt < MT; ++mt)
+        red[wave][mt][lane] = acc[mt];
+    __syncthreads();
+    if (wave >= MT)
+        return;
+    floatx4 s = red[0][wave][lane];
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
+    for (int w = 1; w < kTWaves; ++w)
+        s += red[w][wave][lane];
+    // lane: adapter row 16 jt + r, tokens 16 mt + 4 qg + e
+    const int j = 16 * jt + r;
+    if (j >= rows)
+        return;
+    float* dst = p.yf + (size_t)ks * p.M * rows + j;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                store_out(p, 16 * mt + r, n0 + 16 * rt + 4 * qg + i, out[mt][i]);
-        }
+    for (int e = 0; e < 4; ++e) {
+        const int m = 16 * wave + 4 * qg + e;
+        if (m < p.M)
+            dst[(size_t)m * rows] = s[e];
     }
 }
 
-template <int R, int MT, int NKT, bool TLOAD>
-hipError_t launch_decode_proj(const ProjParams& p, hipStream_t stream)
+// Compute units of the current device (256 when unknown), cached per device.
+int stream_compute_units()
 {
-    constexpr size_t lds = DecShape<R, MT, NKT, TLOAD>::LDS;
-    hipLaunchKernelGGL((proj_decode_kernel<R, MT, NKT, TLOAD>), dim3((p.N + 16 * R - 1) / (16 * R)),
-                       dim3(kDecWaves * 64), lds, stream, p);
+    static std::atomic<int> cached[64];
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 256;
+    if ((cus = cached[dev].load(std::memory_order_relaxed)) > 0)
+        return cus;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        cus = 256;
+    cached[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
+template <int G, int GH, bool FA>
+hipError_t launch_stream(const ProjParams& p, hipStream_t stream)
+{
+    using S = StreamShape<G, GH, FA>;
+    const size_t lds = S::TL_OFFSET + (p.rank > 0 ? stream_tl_bytes(p.M, p.rank) : 0);
+    hipLaunchKernelGGL((proj_stream_kernel<G, GH, FA>), dim3((p.N + S::RG - 1) / S::RG), dim3(kSWaves * 64), lds,
+                       stream, p);
     return hipGetLastError();
 }
 
-// Decode-path dispatch.  Adapters of rank <= 16 are fused (each workgroup
-// computes its projection's activations: one adapter row tile per row tile
-// of weights); larger ranks read activations from a separate pass, since
-// recomputing them per workgroup would read the adapter rows more often
-// than the weights.  Workgroups take two row tiles when the output is wide
-// enough to keep all compute units busy with half as many workgroups.
-template <int MT>
-hipError_t launch_decode_proj_m(const ProjParams& p, hipStream_t stream)
+template <int G, bool FA>
+hipError_t launch_stream_g(const ProjParams& p, hipStream_t stream)
 {
-    const int dq = p.n1, dkv = p.n2 - p.n1;
-    const bool two = p.N >= 4096 && dq % 32 == 0 && dkv % 32 == 0;
-    if (p.yf || p.rank == 0)
-        return two ? launch_decode_proj<2, MT, 0, false>(p, stream) : launch_decode_proj<1, MT, 0, false>(p, stream);
-    if (p.a && p.rank <= 16)
-        return two ? launch_decode_proj<2, MT, 1, false>(p, stream) : launch_decode_proj<1, MT, 1, false>(p, stream);
-    return two ? launch_decode_proj<2, MT, 0, true>(p, stream) : launch_decode_proj<1, MT, 0, true>(p, stream);
+    if (p.M <= 8)
+        return launch_stream<G, 1, FA>(p, stream);
+    if (p.M <= 16)
+        return launch_stream<G, 2, FA>(p, stream);
+    return launch_stream<G, 4, FA>(p, stream);
+}
+
+template <bool FA>
+hipError_t launch_stream_fa(const ProjParams& p, int G, hipStream_t stream)
+{
+    switch (G) {
+    case 1:
+        return launch_stream_g<1, FA>(p, stream);
+    case 2:
+        return launch_stream_g<2, FA>(p, stream);
+    case 3:
+        return launch_stream_g<3, FA>(p, stream);
+    default:
+        return launch_stream_g<4, FA>(p, stream);
+    }
 }
 
 // --------------------------------------------------------------------- big
@@ -833,13 +1059,42 @@ int gemm_xcds()
 
 }  // namespace
 
+hipError_t launch_project_decode(const ProjParams& p, hipStream_t stream)
+{
+    if (p.M <= 0)
+        return hipSuccess;
+    if (p.M > 32 || p.K % 64 != 0)
+        return hipErrorInvalidValue;
+    ProjParams q = p;
+    q.tslices = 0;
+    const bool fused = p.rank > 0 && p.rank <= 16;
+    if (p.rank > 16) {
+        // K slices: whole 64-wide steps, at most kTSlices of them
+        const int s64 = p.K / 64, per = (s64 + kTSlices - 1) / kTSlices;
+        q.tslices = (s64 + per - 1) / per;
+        ProjParams a = p;
+        a.yf = (float*)p.t;
+        dim3 grid((3 * p.rank + 15) / 16, q.tslices);
+        if (p.M <= 16)
+            hipLaunchKernelGGL(proj_tpart_kernel<1>, grid, dim3(kTWaves * 64), 0, stream, a, 64 * per);
+        else
+            hipLaunchKernelGGL(proj_tpart_kernel<2>, grid, dim3(kTWaves * 64), 0, stream, a, 64 * per);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
+    // row groups of 8 G rows: the smallest G whose groups fit the compute units once (at most 4)
+    const int octets = (p.N + 7) / 8, cus = stream_compute_units();
+    const int G = min(4, max(1, (octets + cus - 1) / cus));
+    return fused ? launch_stream_fa<true>(q, G, stream) : launch_stream_fa<false>(q, G, stream);
+}
+
 hipError_t launch_project(const ProjParams& p, hipStream_t stream)
 {
     if (p.M <= 0)
         return hipSuccess;
-    if (p.M <= 32) {
-        // fused path: W, H and (rank > 0) the adapter rows p.a in one kernel
-        return p.M <= 16 ? launch_decode_proj_m<1>(p, stream) : launch_decode_proj_m<2>(p, stream);
+    if (p.M <= 32 && !p.yf) {
+        return launch_project_decode(p, stream);
     } else if (p.M >= kGM && p.N >= kGN && !p.yf && p.K % kGK == 0) {
         const int tiles = ((p.M + kGM - 1) / kGM) * ((p.N + kGN - 1) / kGN);
         ProjParams q = p;

@@ -196,7 +196,8 @@ def test_projection_argument_checks(kvq):
     with pytest.raises(kvq.KvqError) as e:
         kvq.project_qkv(_Shape(4, 128), p, p, p, 8, 2.0, 64, 64, p, p, p, ws_small, stream=0)
     assert e.value.status == kvq.ERR_WORKSPACE
-    assert kvq.project_workspace_bytes(4, 8) == 4 * 24 * 4
+    assert kvq.project_workspace_bytes(4, 8) == 16 * 4 * 24 * 4
+    assert kvq.project_workspace_bytes(64, 8) == 64 * 24 * 4
 
 
 def test_merge_argument_checks(kvq):
