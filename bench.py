@@ -2,7 +2,9 @@
 
 One step = one decode token per sequence through the whole hot path:
   1. adapted Q/K/V projection of the B new hidden states (Eq. (1)-(2)),
-  2. quantize-and-pack append of the new K/V into the packed cache,
+  2. quantize-and-pack append of the new K/V into the packed cache (for
+     window formats such as KIVI the projection call does it:
+     kvq_project_append writes the new rows straight into the fp16 window),
   3. decode attention over the in-kernel reconstruction of all cached tokens
      (Hadamard rotation of q and the output where the format rotates).
 The cache is first filled to the workload's context with the same kernels
@@ -14,8 +16,9 @@ Timing (HIP events on the launch stream):
          its own events -- by a 1 GiB write that evicts the 256 MB
          Infinity Cache (MALL) and the L2s, so every step streams its
          weights and cache from HBM.  ``value`` is B K / (sum of the K step
-         durations) and ``roofline`` uses the attention launches of these
-         steps;
+         durations), with events only at the step boundaries; a second cold
+         pass with events between the calls gives the per-call breakdown,
+         and ``roofline`` uses its attention launches;
   warm   the same K steps back to back from the same starting cache, with
          nothing in between (the serving loop as it runs): ``warm``.
 The K steps are bracketed by a device synchronize on both sides.
@@ -199,6 +202,7 @@ def main():
                      "copy_gbs": copy_gbs, "frac_of_copy": att["gbs"] / copy_gbs},
         "attention_us_per_step": att["us"],
         "projection": res["projection"],
+        "append_us_per_step": res["append_us"],
         "warm": res.get("warm"),
     }
     image = None
@@ -231,7 +235,8 @@ def summary(res):
     out = {"tokens_per_s": res["tokens_per_s"], "ms_per_step": res["ms_per_step"],
            "attention_us": a["us"], "attention_gbs": a["gbs"], "attention_frac": a["gbs"] / HBM_PEAK_GBS,
            "attention_bytes": a["bytes_per_launch"],
-           "projection_us": p["us"], "projection_gbs": p["gbs"], "projection_frac": p["gbs"] / HBM_PEAK_GBS}
+           "projection_us": p["us"], "projection_gbs": p["gbs"], "projection_frac": p["gbs"] / HBM_PEAK_GBS,
+           "fused_append": p["fused_append"], "append_us": res["append_us"]}
     if res.get("warm"):
         w = res["warm"]
         out.update({"warm_tokens_per_s": w["tokens_per_s"], "warm_attention_us": w["attention_us"],
@@ -277,11 +282,20 @@ def fill_cache(wl, W, A, Bm, alloc_proj, dev, synth, kvq, torch, T_max):
     return cache
 
 
+def fused_window_step(wl) -> bool:
+    """Whether a decode step can use kvq_project_append (window formats:
+    the new K and V go straight into the fp16 window)."""
+    f = wl.fmt
+    return f["flush"] > 0 and f["rotate"] == 0 and f["sink"] == 0 and wl.B <= 32
+
+
 def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, bf16, np, torch, configs, kvq,
                synth):
     """Fill the cache, then time `steps` decode steps cold (a MALL flush
     before each, outside its events) and, with `with_warm`, the same steps
-    back to back.  Returns (results, objects to keep alive)."""
+    back to back.  The step timings carry events only at step boundaries;
+    a second cold pass with events between the calls gives the breakdown.
+    Returns (results, objects to keep alive)."""
     B, Hq, Hkv, D = wl.B, wl.H_q, wl.H_kv, wl.D
     W, A, Bm = (bf16(x) for x in synth.layer_weights(wl))
     cache = fill_cache(wl, W, A, Bm, alloc_proj, dev, synth, kvq, torch, wl.context + wl.decode_steps)
@@ -293,6 +307,7 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
     sm = 1.0 / float(np.sqrt(D))
     Kv, Vv, Qv = Kd.view(B, 1, Hkv, D), Vd.view(B, 1, Hkv, D), Qd.view(B, Hq, D)
     Hsteps = [Hdec[i] for i in range(wl.decode_steps)]
+    fused = fused_window_step(wl)
     flush_val = [0]
 
     def flush():
@@ -308,14 +323,22 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
         return [torch.cuda.Event(enable_timing=True) for _ in range(k)]
 
     def step(i, ev=None):
+        """One decode step; ev = 4 events: before, after the projection (and
+        the fused append), after the append, after the attention."""
         if ev is not None:
             ev[0].record()
-        kvq.project_qkv(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
-        if ev is not None:
-            ev[1].record()
-        cache.append(Kv, Vv)
-        if ev is not None:
-            ev[2].record()
+        if fused:
+            kvq.project_append(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, cache, 1, wsd)
+            if ev is not None:
+                ev[1].record()
+                ev[2].record()
+        else:
+            kvq.project_qkv(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
+            if ev is not None:
+                ev[1].record()
+            cache.append(Kv, Vv)
+            if ev is not None:
+                ev[2].record()
         cache.decode_attn(Qv, Hq, sm, O, wsa)
         if ev is not None:
             ev[3].record()
@@ -336,22 +359,35 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
         step(i % wl.decode_steps)
     torch.cuda.synchronize()
 
-    # cold: a flush before every step, outside the step's events
-    restart()
-    evs = [new_events(4) for _ in range(steps)]
-    n_at = []
-    torch.cuda.synchronize()
-    for i in range(steps):
-        j = i % wl.decode_steps
-        if j == 0 and i:
-            restart()
-        flush()
-        n_at.append(wl.context + j + 1)
-        step(j, evs[i])
-    torch.cuda.synchronize()
-    step_ms = np.array([e[0].elapsed_time(e[3]) for e in evs])
-    proj_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
-    attn_ms = np.array([e[2].elapsed_time(e[3]) for e in evs])
+    def cold(breakdown):
+        """The timed steps, a flush before each outside its events."""
+        restart()
+        n_at, evs = [], []
+        torch.cuda.synchronize()
+        for i in range(steps):
+            j = i % wl.decode_steps
+            if j == 0 and i:
+                restart()
+            flush()
+            n_at.append(wl.context + j + 1)
+            if breakdown:
+                evs.append(new_events(4))
+                step(j, evs[-1])
+            else:
+                e = new_events(2)
+                e[0].record()
+                step(j)
+                e[1].record()
+                evs.append(e)
+        torch.cuda.synchronize()
+        return n_at, evs
+
+    n_at, evs = cold(False)
+    step_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    _, bev = cold(True)
+    proj_ms = np.array([e[0].elapsed_time(e[1]) for e in bev])
+    app_ms = np.array([e[1].elapsed_time(e[2]) for e in bev])
+    attn_ms = np.array([e[2].elapsed_time(e[3]) for e in bev])
     bytes_launch = np.array([configs.attention_bytes(wl, n) for n in n_at], dtype=np.float64)
     proj_bytes = configs.projection_weight_bytes(wl.d_in, wl.d_q, wl.d_kv, wl.rank) + 2 * B * (wl.d_in + wl.d_qkv)
     res = {
@@ -361,22 +397,29 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
                       "gbs": float(bytes_launch.mean() / (attn_ms.mean() * 1e-3) / 1e9)},
         "projection": {"us": float(proj_ms.mean() * 1e3), "bytes_per_call": int(proj_bytes),
                        "gbs": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9),
-                       "frac": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9 / HBM_PEAK_GBS)},
+                       "frac": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9 / HBM_PEAK_GBS),
+                       "fused_append": fused},
+        "append_us": float(app_ms.mean() * 1e3),
     }
     if with_warm:
         # the same steps back to back (at most one pass over the decode
         # inputs: the fp16 window cannot be restored inside the loop)
         done = min(steps, wl.decode_steps)
         restart()
-        wev = [new_events(4) for _ in range(done)]
         torch.cuda.synchronize()
         t0, t1 = new_events(2)
         t0.record()
         for i in range(done):
-            step(i, wev[i])
+            step(i)
         t1.record()
         torch.cuda.synchronize()
         warm_ms = t0.elapsed_time(t1) / done
+        restart()
+        wev = [new_events(4) for _ in range(done)]
+        torch.cuda.synchronize()
+        for i in range(done):
+            step(i, wev[i])
+        torch.cuda.synchronize()
         wa = np.array([e[2].elapsed_time(e[3]) for e in wev])
         res["warm"] = {"tokens_per_s": B / (warm_ms * 1e-3), "ms_per_step": warm_ms, "steps": done,
                        "attention_us": float(wa.mean() * 1e3),

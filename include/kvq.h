@@ -187,10 +187,15 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
  * write, without the bf16 K and V ever reaching memory.  The rows of H are
  * (sequence, token) pairs, sequence-major: M = B * n_new, n_new new tokens
  * of each of the cache's B sequences.  Arguments as kvq_project_qkv, plus
- * the cache (d_kv = H_kv * D).  Supported: M >= 256 (the tiled path), d_q
- * and d_kv multiples of 256, n_new and the cache length multiples of 32,
- * formats with per-token key groups and no window, rotation or sink;
- * otherwise KVQ_ERR_FORMAT (format) or KVQ_ERR_ARG (shapes) and nothing
+ * the cache (d_kv = H_kv * D).  Two cases are supported:
+ *   - window formats (flush > 0, e.g. KIVI), one decode step: n_new = 1,
+ *     M = B <= 32, no rotation or sink.  K and V go straight into the fp16
+ *     window; a flush that falls due is coded from the window in the same
+ *     call.
+ *   - formats without a window, prefill chunks: M >= 256 (the tiled path),
+ *     d_q and d_kv multiples of 256, n_new and the cache length multiples
+ *     of 32, per-token key groups, no rotation or sink.
+ * Otherwise KVQ_ERR_FORMAT (format) or KVQ_ERR_ARG (shapes) and nothing
  * changes.  On success the cache length grows by n_new. */
 kvq_status kvq_project_append(const void* H, int M, int d_in, const void* W, int d_q, int d_kv,
                               const void* A, const void* Bm, int rank, float lora_scale, void* Q,

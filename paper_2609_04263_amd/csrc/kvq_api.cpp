@@ -142,6 +142,101 @@ int num_coded(const kvq_format& f, int n)
 
 }  // namespace kvq
 
+namespace {
+
+// One decode step of a window format through the projection: row b of H is
+// sequence b's new token (M = B).  The stream kernel writes Q, and K and V
+// straight into the token's fp16 window slot; a flush that falls due (the
+// oldest tokens of a full window leaving it) is then coded from the window
+// by the block coder, exactly as kvq_append of the same bf16 K and V does.
+// The new token is never among the flushed ones (the window keeps at least
+// `residual` >= 1 tokens), so the coder reads only window rows.
+kvq_status project_append_window(const void* H, int M, int d_in, const void* W, int d_q, int d_kv, const void* A,
+                                 const void* Bm, int rank, float lora_scale, void* Q, kvq_cache* c, void* workspace,
+                                 size_t ws_bytes, void* stream)
+{
+    const kvq_format& f = c->fmt;
+    if (f.rotate != 0 || f.sink != 0 || f.residual < 1)
+        return KVQ_ERR_FORMAT;
+    if (M != c->B || M > 32 || d_in < 64 || d_in % 64 != 0 || d_q < 16 || d_q % 16 != 0 || d_kv != c->H * c->D)
+        return KVQ_ERR_ARG;
+    if (rank < 0 || rank > 64 || !isfinite(lora_scale))
+        return KVQ_ERR_ARG;
+    if (!H || !W || !Q || !aligned16(H) || !aligned16(W) || !aligned16(Q))
+        return KVQ_ERR_ARG;
+    if (rank > 0) {
+        if (!A || !Bm || !aligned16(A) || !aligned16(Bm) || !workspace || !aligned16(workspace))
+            return KVQ_ERR_ARG;
+        if (ws_bytes < kvq::project_workspace_bytes(M, rank))
+            return KVQ_ERR_WORKSPACE;
+    }
+    if ((long long)c->n + 1 > c->T_max)
+        return KVQ_ERR_CAPACITY;
+    hipStream_t s = (hipStream_t)stream;
+    const int n0 = c->n, n1 = n0 + 1, ring = f.residual + f.flush;
+    kvq::ProjParams p = {};
+    p.x = (const uint16_t*)H;
+    p.w = (const uint16_t*)W;
+    p.a = (const uint16_t*)A;
+    p.bm = (const uint16_t*)Bm;
+    p.t = (const float*)workspace;
+    p.y0 = (uint16_t*)Q;
+    p.M = M;
+    p.K = d_in;
+    p.N = d_q + 2 * d_kv;
+    p.n1 = d_q;
+    p.n2 = d_q + d_kv;
+    p.rank = rank;
+    p.scale = lora_scale;
+    p.kr = at<uint16_t>(c, 6);
+    p.vr = at<uint16_t>(c, 7);
+    p.rslots = ring;
+    p.rslot = n0 % ring;
+    p.cH = c->H;
+    p.cD = c->D;
+    if (kvq::launch_project_decode(p, s) != hipSuccess)
+        return KVQ_ERR_DEVICE;
+    const int q0 = kvq::num_coded(f, n0), q1 = kvq::num_coded(f, n1);
+    if (q1 > q0) {
+        kvq::AppendParams a = {};
+        a.kc = at<uint32_t>(c, 0);
+        a.ks = at<float>(c, 1);
+        a.kz = at<float>(c, 2);
+        a.vc = at<uint32_t>(c, 3);
+        a.vs = at<float>(c, 4);
+        a.vz = at<float>(c, 5);
+        a.kr = p.kr;
+        a.vr = p.vr;
+        a.kin = p.kr;  // never read: every flushed token is in the window
+        a.vin = p.vr;
+        a.B = c->B;
+        a.H = c->H;
+        a.T = c->T_alloc;
+        a.n_new = 1;
+        a.k_bits = f.k_bits;
+        a.v_bits = f.v_bits;
+        a.k_mode = f.k_mode;
+        a.v_mode = f.v_mode;
+        a.k_axis = f.k_axis;
+        a.k_group = f.k_group;
+        a.v_group = f.v_group;
+        a.rotate = 0;
+        a.rot_c = rotation_constant(c->D);
+        a.meta16 = f.meta_fp16;
+        a.n0 = n0;
+        a.q0 = q0;
+        a.q1 = q1;
+        a.ring = ring;
+        a.ring_lo = n1;  // the new row is already in its slot
+        if (kvq::launch_append(a, c->D, s) != hipSuccess)
+            return KVQ_ERR_DEVICE;
+    }
+    c->n = n1;
+    return KVQ_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* kvq_strerror(kvq_status s)
@@ -339,6 +434,9 @@ kvq_status kvq_project_append(const void* H, int M, int d_in, const void* W, int
     if (!c || n_new < 0)
         return KVQ_ERR_ARG;
     const kvq_format& f = c->fmt;
+    if (n_new == 1 && f.flush > 0)
+        return project_append_window(H, M, d_in, W, d_q, d_kv, A, Bm, rank, lora_scale, Q, c, workspace, ws_bytes,
+                                     stream);
     if (f.k_axis != KVQ_PER_TOKEN || f.flush != 0 || f.rotate != 0 || f.sink != 0)
         return KVQ_ERR_FORMAT;
     if (M < 256 || d_in < 64 || d_in % 64 != 0 || d_q % 256 != 0 || d_kv % 256 != 0 || d_kv != c->H * c->D)

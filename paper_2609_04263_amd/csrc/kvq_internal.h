@@ -84,8 +84,16 @@ struct ProjParams {
     float* vz;
     int cH, cD, cT, cn0, cn_new;  // KV heads, head size, T_alloc, first position, tokens per sequence
     int k_bits, v_bits, k_mode, v_mode, k_group, v_group, meta16;
+    // Fused window append (decode path, M <= 32): with kr set, row m's K and
+    // V go to slot rslot of sequence m's fp16 window ([B][cH][rslots][cD]
+    // halves, the bf16-rounded values converted to fp16) instead of y1 / y2.
+    uint16_t* kr;
+    uint16_t* vr;
+    int rslots, rslot;
 };
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
+// The decode path (M <= 32) of launch_project.
+hipError_t launch_project_decode(const ProjParams& p, hipStream_t stream);
 // Upper bound on the K slices of the decode path's partial adapter activations.
 constexpr int kProjTSlices = 16;
 // Workspace bytes of the projection for M rows and adapter rank r.

@@ -453,15 +453,24 @@ __global__ __launch_bounds__(kSWaves * 64, 1) void proj_stream_kernel(ProjParams
 #pragma unroll
     for (int e = 0; e < 4; ++e)
         o4[e] = f32_to_bf16(out[e]);
-    const uint2 pk = {o4[0] | ((uint32_t)o4[1] << 16), o4[2] | ((uint32_t)o4[3] << 16)};
     uint16_t* dst;
-    if (n < p.n1)
+    if (n < p.n1) {
         dst = p.y0 + (size_t)m * p.n1 + n;
-    else if (n < p.n2)
+    } else if (p.kr) {
+        // window append: the bf16 value converted to fp16 (as the append of
+        // the bf16 K / V stores it), at head h, channel d of the new slot
+        const bool isv = n >= p.n2;
+        const int col = n - (isv ? p.n2 : p.n1), h = col / p.cD, d = col % p.cD;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            o4[e] = f32_to_f16_bits(bf16_to_f32(o4[e]));
+        dst = (isv ? p.vr : p.kr) + (((size_t)m * p.cH + h) * p.rslots + p.rslot) * p.cD + d;
+    } else if (n < p.n2) {
         dst = p.y1 + (size_t)m * (p.n2 - p.n1) + (n - p.n1);
-    else
+    } else {
         dst = p.y2 + (size_t)m * (p.N - p.n2) + (n - p.n2);
-    *(uint2*)dst = pk;
+    }
+    *(uint2*)dst = uint2{o4[0] | ((uint32_t)o4[1] << 16), o4[2] | ((uint32_t)o4[3] << 16)};
 }
 
 // Partial adapter activations: workgroup (jt, ks) computes

@@ -98,3 +98,96 @@ def check_fused(name, fmt, D, H, rank, B, n_new, calls, d_in, d_q, seed, lora_sc
                 diff = np.nonzero(a != b)[0]
                 raise AssertionError(f"{name} call {call}: section {i} differs at {diff.size} bytes, "
                                      f"first at {diff[0]}")
+
+
+# Decode steps of window formats (one new token per sequence, M = B <= 32):
+# the projection writes K and V straight into the fp16 window and a due
+# flush is coded from the window.  (format, D, H, rank, B, prefill tokens,
+# decode steps): the steps cross at least two flushes.
+WINDOW = {
+    "kivi_d128_b4": (configs.make_format(2, 2, k_axis=configs.PER_CHANNEL, k_group=32, v_group=32,
+                                         residual=32, flush=32), 128, 2, 16, 4, 40, 70),
+    "kivi_d64_b32_r8": (configs.make_format(2, 2, k_axis=configs.PER_CHANNEL, k_group=32, v_group=32,
+                                            residual=64, flush=32), 64, 4, 8, 32, 90, 70),
+    "token_window_d256_b1_r32": (configs.make_format(4, 4, k_group=64, v_group=64, residual=32, flush=32), 256, 1,
+                                 32, 1, 0, 100),
+    "kivi_meta16_sym_d128_b3_rank0": (configs.make_format(4, 2, k_mode=1, v_mode=1, k_axis=configs.PER_CHANNEL,
+                                                          k_group=32, v_group=32, residual=64, flush=32,
+                                                          meta_fp16=1), 128, 2, 0, 3, 33, 100),
+    "window8_d64_b5_r64": (configs.make_format(8, 8, k_group=32, v_group=64, residual=32, flush=32), 64, 2, 64,
+                           5, 7, 95),
+}
+
+
+@pytest.mark.parametrize("name", list(WINDOW))
+def test_fused_decode_window_steps(name):
+    from paper_2609_04263_amd import kvq
+    fmt, D, H, rank, B, n_pre, steps = WINDOW[name]
+    seed = 300 + D + B
+    d_in, d_q = 256, 256
+    d_kv = H * D
+    N = d_q + 2 * d_kv
+    W = dev_bf16(synth.normal_bf16(seed, "W", (N, d_in), std=1.0 / np.sqrt(d_in)))
+    A = dev_bf16(synth.normal_bf16(seed, "A", (3 * max(rank, 1), d_in), std=1.0 / np.sqrt(d_in)))
+    Bm = dev_bf16(synth.normal_bf16(seed, "B", (N, max(rank, 1)), std=0.14))
+    T = n_pre + steps
+    ref = oracle.Cache(fmt, B, H, D, T)
+    gc = kvq.Cache(fmt, B, H, D, T)
+    bits = lambda t: t.view(torch.int16).cpu().numpy().view(np.uint16)
+    if n_pre:
+        M = B * n_pre
+        ws = torch.empty(max(16, kvq.project_workspace_bytes(M, rank)), dtype=torch.uint8, device="cuda")
+        Hm = dev_bf16(synth.normal_bf16(seed, "Hpre", (M, d_in)))
+        Qp = torch.empty((M, d_q), dtype=torch.bfloat16, device="cuda")
+        Kp = torch.empty((M, d_kv), dtype=torch.bfloat16, device="cuda")
+        Vp = torch.empty((M, d_kv), dtype=torch.bfloat16, device="cuda")
+        kvq.project_qkv(Hm, W, A, Bm, rank, 2.0, d_q, d_kv, Qp, Kp, Vp, ws)
+        gc.append(Kp.view(B, n_pre, H, D), Vp.view(B, n_pre, H, D))
+        torch.cuda.synchronize()
+        ref.append(bits(Kp).reshape(B, n_pre, H, D), bits(Vp).reshape(B, n_pre, H, D))
+    ws = torch.empty(max(16, kvq.project_workspace_bytes(B, rank)), dtype=torch.uint8, device="cuda")
+    Hd = dev_bf16(synth.normal_bf16(seed, "Hdec", (steps, B, d_in)))
+    flushes = 0
+    for i in range(steps):
+        Qr = torch.empty((B, d_q), dtype=torch.bfloat16, device="cuda")
+        Kr = torch.empty((B, d_kv), dtype=torch.bfloat16, device="cuda")
+        Vr = torch.empty((B, d_kv), dtype=torch.bfloat16, device="cuda")
+        kvq.project_qkv(Hd[i], W, A, Bm, rank, 2.0, d_q, d_kv, Qr, Kr, Vr, ws)
+        Q = torch.full((B, d_q), float("nan"), dtype=torch.bfloat16, device="cuda")
+        coded_before = gc.length()[1]
+        kvq.project_append(Hd[i], W, A, Bm, rank, 2.0, d_q, d_kv, Q, gc, 1, ws)
+        torch.cuda.synchronize()
+        ref.append(bits(Kr).reshape(B, 1, H, D), bits(Vr).reshape(B, 1, H, D))
+        assert np.array_equal(bits(Q), bits(Qr)), f"{name}: Q differs at step {i}"
+        assert gc.length() == (ref.n, ref.n_coded), f"{name}: lengths at step {i}"
+        flushes += gc.length()[1] > coded_before
+        if i % 7 == 6 or i == steps - 1 or gc.length()[1] > coded_before:
+            img = image(gc)
+            for s in range(10):
+                o, ln = ref.offsets[s], ref.lengths[s]
+                a, b = img[o:o + ln], ref.image[o:o + ln]
+                if not np.array_equal(a, b):
+                    diff = np.nonzero(a != b)[0]
+                    raise AssertionError(f"{name} step {i}: section {s} differs at {diff.size} bytes, first at {diff[0]}")
+    assert flushes >= 2, f"{name}: the steps crossed {flushes} flushes"
+
+
+def test_fused_decode_window_unsupported_formats():
+    from paper_2609_04263_amd import kvq
+    B, H, D, rank, d_in, d_q = 2, 2, 64, 8, 256, 128
+    d_kv = H * D
+    N = d_q + 2 * d_kv
+    W = torch.zeros((N, d_in), dtype=torch.bfloat16, device="cuda")
+    A = torch.zeros((3 * rank, d_in), dtype=torch.bfloat16, device="cuda")
+    Bm = torch.zeros((N, rank), dtype=torch.bfloat16, device="cuda")
+    Hm = torch.zeros((B, d_in), dtype=torch.bfloat16, device="cuda")
+    Q = torch.empty((B, d_q), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(kvq.project_workspace_bytes(B, rank), dtype=torch.uint8, device="cuda")
+    for fmt in (configs.make_format(4, 4, k_mode=1, v_mode=1, k_group=64, v_group=64, residual=32, flush=32,
+                                    rotate=64),
+                configs.make_format(4, 4, k_group=64, v_group=64, residual=32, flush=32, sink=32)):
+        gc = kvq.Cache(fmt, B, H, D, 64)
+        with pytest.raises(kvq.KvqError) as e:
+            kvq.project_append(Hm, W, A, Bm, rank, 2.0, d_q, d_kv, Q, gc, 1, ws)
+        assert e.value.status == kvq.ERR_FORMAT
+        assert gc.length() == (0, 0)
