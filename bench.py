@@ -11,7 +11,8 @@ The cache is first filled to the workload's context with the same kernels
 (prefill projection in chunks, then append).  Inputs are synthetic, seeded
 and resident in HBM before the timed region.
 
-Timing (HIP events on the launch stream):
+Timing (HIP events on the launch stream, created without the system-scope
+fence that torch's events carry):
   cold   the K timed steps run one after another, each preceded -- outside
          its own events -- by a 1 GiB write that evicts the 256 MB
          Infinity Cache (MALL) and the L2s, so every step streams its
@@ -84,6 +85,47 @@ def parse():
                     help="before the timed region, copy a buffer of this many MiB once (a kernel of known "
                          "bytes for calibrating rocprofv3 FETCH_SIZE/WRITE_SIZE counters)")
     return ap.parse_args()
+
+
+class FenceFreeEvent:
+    """A HIP timing event created with hipEventDisableSystemFence and recorded
+    on the current stream.  torch's events carry a system-scope fence (a
+    cache writeback and invalidate) at every record, which costs several
+    microseconds on this GPU and disturbs the caches of the work that
+    follows; the timings of the decode steps use these instead."""
+    _lib = None
+
+    def __init__(self, torch):
+        import ctypes
+        if FenceFreeEvent._lib is None:
+            lib = ctypes.CDLL("libamdhip64.so")
+            lib.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+            lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+            lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            FenceFreeEvent._lib = lib
+        self._torch = torch
+        self._ev = ctypes.c_void_p()
+        if FenceFreeEvent._lib.hipEventCreateWithFlags(ctypes.byref(self._ev), 0x20000000) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
+
+    def record(self):
+        if FenceFreeEvent._lib.hipEventRecord(self._ev, self._torch.cuda.current_stream().cuda_stream) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_time(self, end) -> float:
+        """Milliseconds from this event to `end` (both recorded and complete)."""
+        import ctypes
+        FenceFreeEvent._lib.hipEventSynchronize(end._ev)
+        ms = ctypes.c_float()
+        if FenceFreeEvent._lib.hipEventElapsedTime(ctypes.byref(ms), self._ev, end._ev) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def __del__(self):
+        if FenceFreeEvent._lib is not None and self._ev:
+            FenceFreeEvent._lib.hipEventDestroy(self._ev)
 
 
 def kernel_source_hash() -> str:
@@ -320,7 +362,7 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
         cache.restore(wl.context)
 
     def new_events(k):
-        return [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+        return [FenceFreeEvent(torch) for _ in range(k)]
 
     def step(i, ev=None):
         """One decode step; ev = 4 events: before, after the projection (and
