@@ -395,11 +395,15 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
         p.scale = lora_scale;
         return kvq::launch_project(p, s) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
     }
+    // large-M pass: with the adapter streamed as extra K stages the
+    // activation pass writes bf16 hi / lo activations instead of fp32
+    const bool hilo = kvq::project_adapter_stages(M, d_in, d_q, d_kv, rank);
     if (rank > 0) {
         kvq::ProjParams a = {};
         a.x = (const uint16_t*)H;
         a.w = (const uint16_t*)A;
         a.yf = (float*)workspace;
+        a.t_hilo = hilo;
         a.M = M;
         a.K = d_in;
         a.N = 3 * rank;
@@ -424,6 +428,7 @@ kvq_status kvq_project_qkv(const void* H, int M, int d_in, const void* W, int d_
     p.n2 = d_q + d_kv;
     p.rank = rank;
     p.scale = 1.0f;
+    p.t_hilo = hilo;
     return kvq::launch_project(p, s) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 

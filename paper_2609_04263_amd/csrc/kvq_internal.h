@@ -71,6 +71,8 @@ struct ProjParams {
     float scale;          // multiplies the fp32 output (activation pass); the adapter scale (fused path)
     int nxcd;             // XCDs the large-M tile order spreads over (set at launch)
     int tslices;          // K slices of the partial adapter activations (M <= 32, set at launch)
+    int t_hilo;           // activations as bf16 hi and lo, [M][3][2 rank] (written by the activation pass
+                          // through yf, read by the large-M pass as extra K stages; see project_adapter_stages)
     // Fused append (large-M path only): with fuse set, the K and V tiles are
     // coded into the cache instead of stored.  Rows are (sequence, token)
     // pairs, cn_new tokens per sequence starting at cache position cn0 (a
@@ -94,6 +96,11 @@ struct ProjParams {
 hipError_t launch_project(const ProjParams& p, hipStream_t stream);
 // The decode path (M <= 32) of launch_project.
 hipError_t launch_project_decode(const ProjParams& p, hipStream_t stream);
+// Whether the large-M pass of an M x d_in x (d_q + 2 d_kv) projection with
+// adapter rank `rank` streams the adapter as extra K stages (its activation
+// pass then writes t_hilo activations): 256x256 tiles that never straddle
+// Q, K and V, and a rank that is a multiple of 16.
+bool project_adapter_stages(int M, int d_in, int d_q, int d_kv, int rank);
 // Upper bound on the K slices of the decode path's partial adapter activations.
 constexpr int kProjTSlices = 16;
 // Workspace bytes of the projection for M rows and adapter rank r.

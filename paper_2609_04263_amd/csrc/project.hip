@@ -65,7 +65,22 @@ __device__ __forceinline__ void store_out(const ProjParams& p, int m, int n, flo
     if (m >= p.M || n >= p.N)
         return;
     if (p.yf) {
-        p.yf[(size_t)m * p.N + n] = v * p.scale;
+        const float t = v * p.scale;
+        if (p.t_hilo) {
+            // bf16 hi (nearest) and lo (remainder, nearest) of the scaled
+            // activation (split_bf16x8's operands, precomputed), [M][3][2 r]:
+            // in projection n / r's segment, rank column j's hi at
+            // 32 (j / 16) + j % 16 and its lo 16 further, so that K stages
+            // of 32 meet hi then lo of each 16 columns, the order in which
+            // the K-extension after the main loop adds them
+            const int r = p.N / 3, pj = n / r, j = n - pj * r;
+            uint16_t* row = (uint16_t*)p.yf + (size_t)m * 2 * p.N + (size_t)pj * 2 * r + 32 * (j >> 4) + (j & 15);
+            const uint16_t hi = f32_to_bf16(t);
+            row[0] = hi;
+            row[16] = f32_to_bf16(t - bf16_to_f32(hi));
+        } else {
+            p.yf[(size_t)m * p.N + n] = t;
+        }
         return;
     }
     uint16_t o = f32_to_bf16(v);
@@ -579,30 +594,36 @@ hipError_t launch_stream_fa(const ProjParams& p, int G, hipStream_t stream)
 }
 
 // --------------------------------------------------------------------- big
-// 128x128 output tile, four waves in a 2x2 grid of 64x64 sub-tiles, K step
-// 64 through double-buffered LDS (rows padded by 16 bytes).
+// (32 MI)x128 output tile, four waves in a 2x2 grid of (16 MI)x64 sub-tiles,
+// K step 64 through double-buffered LDS (rows padded by 16 bytes).  MI = 4
+// (128-row tiles), or MI = 1 for an activation pass (N = 3 r <= 192
+// columns) too short to cover the compute units with 128-row tiles.
 // MFMA roles: A = H rows (M-dim = tokens), B = W^T (N-dim = weight rows).
 // Output lane layout: token m = row base + 4 qg + i, column n = base + lane % 16.
 constexpr int kBM = 128, kBN = 128, kBK = 64, kLdsRow = kBK + 8;
 
+template <int MI>
 __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
 {
-    __shared__ uint16_t As[2][kBM * kLdsRow];
+    constexpr int BM = 32 * MI;
+    __shared__ uint16_t As[2][BM * kLdsRow];
     __shared__ uint16_t Bs[2][kBN * kLdsRow];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r = lane & 15, qg = lane >> 4;
     const int wm = wave >> 1, wn = wave & 1;
-    const int m0 = blockIdx.y * kBM, n0 = blockIdx.x * kBN;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * kBN;
 
-    // Global -> register staging: 4 x 16 bytes per thread per operand.
-    u32x4 ra[4], rb[4];
+    // Global -> register staging: 16-byte chunks, MI per thread for the H
+    // rows and 4 for the W rows.
+    u32x4 ra[MI], rb[4];
     auto gload = [&](int k0) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             int idx = tid + kThreads * i;      // 0..1023
             int row = idx >> 3, c8 = (idx & 7) * 8;
             int m = m0 + row, n = n0 + row;
-            ra[i] = m < p.M ? *(const u32x4*)(p.x + (size_t)m * p.K + k0 + c8) : u32x4{0u, 0u, 0u, 0u};
+            if (i < MI)
+                ra[i] = m < p.M ? *(const u32x4*)(p.x + (size_t)m * p.K + k0 + c8) : u32x4{0u, 0u, 0u, 0u};
             rb[i] = n < p.N ? *(const u32x4*)(p.w + (size_t)n * p.K + k0 + c8) : u32x4{0u, 0u, 0u, 0u};
         }
     };
@@ -611,14 +632,15 @@ __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
         for (int i = 0; i < 4; ++i) {
             int idx = tid + kThreads * i;
             int row = idx >> 3, c8 = (idx & 7) * 8;
-            *(u32x4*)(&As[buf][row * kLdsRow + c8]) = ra[i];
+            if (i < MI)
+                *(u32x4*)(&As[buf][row * kLdsRow + c8]) = ra[i];
             *(u32x4*)(&Bs[buf][row * kLdsRow + c8]) = rb[i];
         }
     };
 
-    floatx4 acc[4][4];
+    floatx4 acc[MI][4];
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
             acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -633,17 +655,17 @@ __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
             gload((ks + 1) * kBK);
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            bf16x8 af[4], bfr[4];
+            bf16x8 af[MI], bfr[4];
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
+            for (int mi = 0; mi < MI; ++mi)
                 af[mi] = __builtin_bit_cast(
-                    bf16x8, *(const u32x4*)(&As[buf][(wm * 64 + 16 * mi + r) * kLdsRow + 32 * kk + 8 * qg]));
+                    bf16x8, *(const u32x4*)(&As[buf][(wm * 16 * MI + 16 * mi + r) * kLdsRow + 32 * kk + 8 * qg]));
 #pragma unroll
             for (int ni = 0; ni < 4; ++ni)
                 bfr[ni] = __builtin_bit_cast(
                     bf16x8, *(const u32x4*)(&Bs[buf][(wn * 64 + 16 * ni + r) * kLdsRow + 32 * kk + 8 * qg]));
 #pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
+            for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
                 for (int ni = 0; ni < 4; ++ni)
                     acc[mi][ni] = mfma16_bf16(af[mi], bfr[ni], acc[mi][ni]);
@@ -664,9 +686,9 @@ __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
                 for (int ni = 0; ni < 4; ++ni)
                     wop[ni] = lora_weight_operand(p, n0 + wn * 64 + 16 * ni + r, proj, kk, qg);
 #pragma unroll
-                for (int mi = 0; mi < 4; ++mi) {
+                for (int mi = 0; mi < MI; ++mi) {
                     bf16x8 hi, lo;
-                    lora_token_operand(p, m0 + wm * 64 + 16 * mi + r, proj, kk, qg, &hi, &lo);
+                    lora_token_operand(p, m0 + wm * 16 * MI + 16 * mi + r, proj, kk, qg, &hi, &lo);
 #pragma unroll
                     for (int ni = 0; ni < 4; ++ni) {
                         acc[mi][ni] = mfma16_bf16(hi, wop[ni], acc[mi][ni]);
@@ -677,12 +699,12 @@ __global__ __launch_bounds__(kThreads) void proj_big_kernel(ProjParams p)
         }
     }
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                store_out(p, m0 + wm * 64 + 16 * mi + 4 * qg + i, n0 + wn * 64 + 16 * ni + r, acc[mi][ni][i]);
+                store_out(p, m0 + wm * 16 * MI + 16 * mi + 4 * qg + i, n0 + wn * 64 + 16 * ni + r, acc[mi][ni][i]);
 }
 
 
@@ -1051,6 +1073,308 @@ __global__ __launch_bounds__(kThreads) void proj_gemm_kernel(ProjParams p)
     }
 }
 
+// Large-M main pass with plain outputs (the fused append keeps the kernel
+// above): the same 256x256 output tile and tile order, computed by eight
+// waves, two per SIMD, each owning a 64x128 sub-tile (2x4 accumulators of
+// v_mfma_f32_32x32x16_bf16, 128 registers).  Operands reach LDS by
+// global_load_lds_dwordx4 (16 bytes per lane straight into LDS, no
+// registers) in a ring of kPNst stages of K = 32: rows of 64 bytes, chunk c
+// of row r at chunk position c ^ ((r >> 2) & 3), which measured free of bank
+// conflicts for the 32-row fragment reads (the xor of bits 1 and 3 left four
+// conflict cycles per read).  The two waves of a SIMD alternate roles at
+// every barrier: while one runs the 16 MFMAs of a stage from registers, the
+// other reads its next stage's fragments from LDS and issues its copies four
+// stages ahead (waves 0-3 copy the A rows, 4-7 the B rows).  A stage's LDS
+// traffic (96 KiB of fragment reads, 32 KiB of copies) is what bounds this
+// kernel; the four-wave kernel reads a third less per MFMA but cannot hide
+// its barrier and copy latency with one wave per SIMD.
+constexpr int kPThreads = 512, kPK = 32, kPNst = 5;
+constexpr int kPStage = (kGM + kGN) * kPK * 2;    // 32 KiB: A rows then B rows
+constexpr size_t kPLds = (size_t)kPNst * kPStage;  // 160 KiB
+
+__device__ __forceinline__ int pp_swz(int row)
+{
+    return (row >> 2) & 3;
+}
+
+// 16 bytes per lane from global memory to LDS address lds_addr + 16 lane
+// (lds_addr wave-uniform, held in M0 while the copy issues).  Inline
+// assembly, so that the compiler does not make LDS reads wait for every
+// outstanding copy; the kernel's own vmcnt waits order them.
+__device__ __forceinline__ void pp_copy16(uint64_t base, uint32_t voff, uint32_t lds_addr)
+{
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" : : "s"(m0v), "v"(voff), "s"(base) : "memory");
+}
+
+__global__ __launch_bounds__(kPThreads, 1) void proj_gemm_pp_kernel(ProjParams p)
+{
+    extern __shared__ __attribute__((aligned(16))) uint8_t glds[];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = wave >> 2, wm = wave & 3, wn = wave >> 2;
+    // tile order as in proj_gemm_kernel
+    const int nbn = (p.N + kGN - 1) / kGN, nbm = (p.M + kGM - 1) / kGM;
+    const int ntiles = nbn * nbm, nx = p.nxcd;
+    const int per = (ntiles + nx - 1) / nx;
+    const int t = (blockIdx.x % nx) * per + blockIdx.x / nx;
+    if (t >= ntiles)
+        return;
+    constexpr int kGroupM = 4;
+    const int g = t / (kGroupM * nbn), rem = t % (kGroupM * nbn);
+    const int gm = min(kGroupM, nbm - g * kGroupM);
+    const int m0 = (g * kGroupM + rem % gm) * kGM, n0 = (rem / gm) * kGN;
+
+    // copies: a stage is 32 copies of 1 KiB (16 rows x 64 bytes), 0..15 the A
+    // rows and 16..31 the B rows; wave w moves copies 4 w .. 4 w + 3.  Lane i
+    // of a copy writes LDS row 16 j + i / 4, chunk position i % 4, which holds
+    // source chunk (i % 4) ^ swz(row).  Rows past M (N) re-read the last row;
+    // their results are never stored.
+    const bool wisb = wave >= 4;
+    const uint64_t gbase = wisb ? (uint64_t)(p.w + (size_t)n0 * p.K) : (uint64_t)(p.x + (size_t)m0 * p.K);
+    const int rlast = wisb ? p.N - 1 - n0 : p.M - 1 - m0;
+    uint32_t voff[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const int row = 16 * ((4 * wave + c) & 15) + (lane >> 2);
+        voff[c] = (uint32_t)min(row, rlast) * (uint32_t)p.K * 2u + 16u * (uint32_t)((lane & 3) ^ pp_swz(row));
+    }
+    const uint32_t lbase = (uint32_t)(uintptr_t)glds;
+    const int nks = p.K / kPK;
+    // With t_hilo the adapter follows as rank / 16 more stages: stage e's A
+    // rows are the tile's activation rows (hi then lo of rank columns
+    // 16 e .. 16 e + 15, of the tile's projection), its B rows the tile's
+    // B_p rows at those 16 columns, twice.
+    const bool ext = p.t_hilo && p.rank > 0;
+    const int nst = nks + (ext ? p.rank / 16 : 0);
+    const int tproj = proj_of(p, n0);
+    constexpr int kAhead = kPNst - 1;  // stages in flight ahead of the one being read
+    // copies of stage ks into ring slot ks % kPNst; stages past the end
+    // re-load the last one into a slot that is never read again
+    auto copy_stage = [&](int ks) {
+        const int kc = min(ks, nst - 1);
+        const uint32_t lds_at = lbase + (ks % kPNst) * kPStage;
+        if (kc < nks) {
+            const uint64_t b = gbase + (uint64_t)kc * (kPK * 2);
+            const uint32_t bl = __builtin_amdgcn_readfirstlane((uint32_t)b);
+            const uint32_t bh = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+            const uint64_t bs = ((uint64_t)bh << 32) | bl;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+                pp_copy16(bs, voff[c], lds_at + (4 * wave + c) * 1024);
+        } else {
+            const int e = kc - nks, r = p.rank;
+            const uint64_t b = wisb ? (uint64_t)(p.bm + (size_t)n0 * r)
+                                    : (uint64_t)((const uint16_t*)p.t + (size_t)m0 * 6 * r + (size_t)tproj * 2 * r + 32 * e);
+            const uint32_t bl = __builtin_amdgcn_readfirstlane((uint32_t)b);
+            const uint32_t bh = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+            const uint64_t bs = ((uint64_t)bh << 32) | bl;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int row = 16 * ((4 * wave + c) & 15) + (lane >> 2);
+                const int src = (lane & 3) ^ pp_swz(row);
+                const uint32_t rc = (uint32_t)min(row, rlast);
+                const uint32_t vo = wisb ? rc * 2u * (uint32_t)r + 2u * (uint32_t)(16 * e + 8 * (src & 1))
+                                         : rc * 12u * (uint32_t)r + 16u * (uint32_t)src;
+                pp_copy16(bs, vo, lds_at + (4 * wave + c) * 1024);
+            }
+        }
+    };
+
+    // fragments: A rows 64 wm + 32 i + l % 32, B rows 128 wn + 32 j + l % 32,
+    // chunk 2 kt + l / 32 of a stage
+    const int fr = lane & 31, fk = lane >> 5;
+    uint32_t aoff[2][2], boff[2][4];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int r = 64 * wm + 32 * i + fr;
+            aoff[kt][i] = r * 64 + 16 * ((2 * kt + fk) ^ pp_swz(r));
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = 128 * wn + 32 * j + fr;
+            boff[kt][j] = kGM * 64 + r * 64 + 16 * ((2 * kt + fk) ^ pp_swz(r));
+        }
+    }
+    floatx16 acc[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            acc[i][j] = floatx16{};
+    bf16x8 fa[2][2], fb[2][4];
+    // memory role: this stage's fragments into registers, copies kAhead stages ahead
+    auto mem_phase = [&](int ks) {
+        const uint8_t* sb = glds + (ks % kPNst) * kPStage;
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                fa[kt][i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sb + aoff[kt][i]));
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                fb[kt][j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sb + boff[kt][j]));
+        }
+        copy_stage(ks + kAhead);
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the reads are done before the slot is handed on
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // compute role: the stage's 16 MFMAs
+    auto mfma_phase = [&]() {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    acc[i][j] = mfma32_bf16(fa[kt][i], fb[kt][j], acc[i][j]);
+    };
+    // barrier between roles; before it every wave waits for its copies of
+    // all but the two newest stages (vmcnt(8)), so the stage read next has
+    // landed in LDS whichever wave copied it
+    auto swap = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(0x0F78);  // vmcnt(8)
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    uint32_t m0_saved;
+    asm volatile("s_mov_b32 %0, m0" : "=s"(m0_saved));
+#pragma unroll
+    for (int ks = 0; ks < kAhead; ++ks)
+        copy_stage(ks);
+    swap();
+    // Wave group 1 reads stage ks while group 0 computes stage ks - 1, then
+    // the roles swap; both groups pass 2 nst + 1 barriers.
+    if (grp == 1) {
+        for (int ks = 0; ks < nst; ++ks) {
+            mem_phase(ks);
+            swap();
+            mfma_phase();
+            swap();
+        }
+    } else {
+        for (int ks = 0; ks < nst; ++ks) {
+            if (ks > 0)
+                mfma_phase();
+            swap();
+            mem_phase(ks);
+            swap();
+        }
+        mfma_phase();
+    }
+    asm volatile("s_mov_b32 m0, %0" ::"s"(m0_saved));
+    __builtin_amdgcn_s_waitcnt(0);  // the trailing copies have landed before the ring is reused
+
+    // adapter branch without t_hilo: K-extension over the rank, 16 at a
+    // time, after the main loop (its loads are then a latency of their own).
+    // With the rank a multiple of 16 a lane's eight B_p values and eight
+    // activations are two or three 16-byte loads (rows past M or N clamped,
+    // their operands zeroed), all issued before the MFMAs of their step.
+    if (p.rank > 0 && !ext) {
+        const bool vec = (p.rank & 15) == 0;
+        const int p_lo = proj_of(p, n0), p_hi = proj_of(p, min(n0 + kGN, p.N) - 1);
+        for (int proj = p_lo; proj <= p_hi; ++proj) {
+            for (int k0 = 0; k0 < p.rank; k0 += 16) {
+                bf16x8 wop[4];
+                float tv[2][8];
+#pragma unroll
+                for (int ni = 0; ni < 4; ++ni) {
+                    const int n = n0 + wn * 128 + 32 * ni + fr;
+                    const bool ok = n < p.N && proj_of(p, n) == proj;
+                    if (vec) {
+                        const u32x4 w4 = *(const u32x4*)(p.bm + (size_t)min(n, p.N - 1) * p.rank + k0 + 8 * fk);
+                        wop[ni] = ok ? __builtin_bit_cast(bf16x8, w4) : zero_bf16x8();
+                    } else {
+                        uint16_t v[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const int k = k0 + 8 * fk + e;
+                            v[e] = (ok && k < p.rank) ? p.bm[(size_t)n * p.rank + k] : (uint16_t)0;
+                        }
+                        u32x4 w4;
+                        w4.x = v[0] | ((uint32_t)v[1] << 16);
+                        w4.y = v[2] | ((uint32_t)v[3] << 16);
+                        w4.z = v[4] | ((uint32_t)v[5] << 16);
+                        w4.w = v[6] | ((uint32_t)v[7] << 16);
+                        wop[ni] = __builtin_bit_cast(bf16x8, w4);
+                    }
+                }
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi) {
+                    const int m = m0 + wm * 64 + 32 * mi + fr;
+                    if (vec) {
+                        const float* tr = p.t + (size_t)min(m, p.M - 1) * 3 * p.rank + proj * p.rank + k0 + 8 * fk;
+                        const float4 a = *(const float4*)tr, b = *(const float4*)(tr + 4);
+                        const bool ok = m < p.M;
+                        tv[mi][0] = ok ? a.x : 0.0f;
+                        tv[mi][1] = ok ? a.y : 0.0f;
+                        tv[mi][2] = ok ? a.z : 0.0f;
+                        tv[mi][3] = ok ? a.w : 0.0f;
+                        tv[mi][4] = ok ? b.x : 0.0f;
+                        tv[mi][5] = ok ? b.y : 0.0f;
+                        tv[mi][6] = ok ? b.z : 0.0f;
+                        tv[mi][7] = ok ? b.w : 0.0f;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const int k = k0 + 8 * fk + e;
+                            tv[mi][e] = (m < p.M && k < p.rank) ? p.t[(size_t)m * 3 * p.rank + proj * p.rank + k] : 0.0f;
+                        }
+                    }
+                }
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi) {
+                    bf16x8 hi, lo;
+                    split_bf16x8(tv[mi], &hi, &lo);
+#pragma unroll
+                    for (int ni = 0; ni < 4; ++ni) {
+                        acc[mi][ni] = mfma32_bf16(hi, wop[ni], acc[mi][ni]);
+                        acc[mi][ni] = mfma32_bf16(lo, wop[ni], acc[mi][ni]);
+                    }
+                }
+            }
+        }
+    }
+
+
+    // Output, one 32-row slice of the wave's sub-tile at a time through the
+    // wave's own LDS region (the ring is free once every wave is past the
+    // barrier below): accumulator element e of lane l is row 8 (e / 4) +
+    // 4 (l / 32) + e % 4, column l % 32 of its block; each lane then writes a
+    // pair of adjacent columns of every row, rounded to bf16.
+    __syncthreads();
+    float* xo = (float*)glds + wave * (32 * 128);
+    const int cpair = n0 + wn * 128 + 2 * lane;
+    const int proj = proj_of(p, min(cpair, p.N - 1));
+    uint16_t* ybase = proj == 0 ? p.y0 : proj == 1 ? p.y1 : p.y2;
+    const int ywidth = proj == 0 ? p.n1 : proj == 1 ? p.n2 - p.n1 : p.N - p.n2;
+    const int ycol = cpair - (proj == 0 ? 0 : proj == 1 ? p.n1 : p.n2);
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi) {
+        // a wave's LDS accesses are performed in order: its reads of the
+        // previous slice are done before these writes, and these before the reads
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                xo[(8 * (e >> 2) + 4 * fk + (e & 3)) * 128 + 32 * ni + fr] = acc[mi][ni][e];
+        const int mrow0 = m0 + wm * 64 + 32 * mi;
+        for (int r = 0; r < 32; ++r) {
+            const int m = mrow0 + r;
+            const float2 v = *(const float2*)(xo + r * 128 + 2 * lane);
+            if (m < p.M && cpair < p.N) {
+                const uint32_t w = (uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+                *(uint32_t*)(ybase + (size_t)m * ywidth + ycol) = w;
+            }
+        }
+    }
+}
+
 // XCDs of the current device (1 when unknown), cached per device.
 int gemm_xcds()
 {
@@ -1067,6 +1391,12 @@ int gemm_xcds()
 }
 
 }  // namespace
+
+bool project_adapter_stages(int M, int d_in, int d_q, int d_kv, int rank)
+{
+    return rank > 0 && rank % 16 == 0 && M >= kGM && d_q + 2 * d_kv >= kGN && d_in % kGK == 0 && d_q % kGN == 0 &&
+           d_kv % kGN == 0;
+}
 
 hipError_t launch_project_decode(const ProjParams& p, hipStream_t stream)
 {
@@ -1102,9 +1432,12 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
 {
     if (p.M <= 0)
         return hipSuccess;
+    const bool tiled = p.M >= kGM && p.N >= kGN && !p.yf && p.K % kGK == 0;
+    if (p.t_hilo && !p.yf && (!tiled || p.fuse || p.rank % 16 != 0))
+        return hipErrorInvalidValue;  // only the large-M pass reads bf16 hi / lo activations
     if (p.M <= 32 && !p.yf) {
         return launch_project_decode(p, stream);
-    } else if (p.M >= kGM && p.N >= kGN && !p.yf && p.K % kGK == 0) {
+    } else if (tiled) {
         const int tiles = ((p.M + kGM - 1) / kGM) * ((p.N + kGN - 1) / kGN);
         ProjParams q = p;
         q.nxcd = gemm_xcds();
@@ -1112,10 +1445,17 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
         if (q.fuse)
             hipLaunchKernelGGL(proj_gemm_kernel<true>, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
         else
-            hipLaunchKernelGGL(proj_gemm_kernel<false>, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
+            hipLaunchKernelGGL(proj_gemm_pp_kernel, dim3(per * q.nxcd), dim3(kPThreads), kPLds, stream, q);
+    } else if (p.yf && p.N <= 2 * kBN && p.M < 256 * kBM) {
+        // activation pass with fewer than 256 row tiles of 128: 32-row tiles
+        // (every workgroup also reads all of A, so more tiles only pay
+        // until the grid covers the compute units; measured 80 -> 66 us at
+        // M = 16384, slower at M = 65536)
+        dim3 grid((p.N + kBN - 1) / kBN, (p.M + 31) / 32);
+        hipLaunchKernelGGL(proj_big_kernel<1>, grid, dim3(kThreads), 0, stream, p);
     } else {
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + kBM - 1) / kBM);
-        hipLaunchKernelGGL(proj_big_kernel, grid, dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL(proj_big_kernel<4>, grid, dim3(kThreads), 0, stream, p);
     }
     return hipGetLastError();
 }
