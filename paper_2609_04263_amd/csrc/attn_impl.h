@@ -228,9 +228,10 @@ __device__ constexpr float code_bias()
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 // Bit constants of the conversion, kept in registers (a VOP3 operation
-// cannot take two literals on gfx950).
+// cannot take two literals on gfx950); mag16 is the exponent pair of 16 for
+// the 2-bit conversion with mixed biases.
 struct CodeBits {
-    uint32_t mask, magic;
+    uint32_t mask, magic, mag16;
 };
 
 template <int BITS>
@@ -242,15 +243,28 @@ __device__ __forceinline__ CodeBits code_bits()
     // 2-bit: code at mantissa bits 8..9 under exponent 2^2 (4 + c).
     uint32_t mask = BITS == 8 ? 0xE480E480u : BITS == 4 ? 0x03C003C0u : 0x03000300u;
     uint32_t magic = BITS == 8 ? 0x64006400u : BITS == 4 ? 0x4C004C00u : 0x44004400u;
-    // opaque to constant folding, so both stay in registers
+    uint32_t mag16 = 0x4C004C00u;
+    // opaque to constant folding, so they stay in registers
     asm volatile("" : "+v"(mask), "+v"(magic));
-    return CodeBits{mask, magic};
+    if constexpr (BITS == 2)
+        asm volatile("" : "+v"(mag16));
+    return CodeBits{mask, magic, mag16};
 }
 
 // Piece k (eight codes, code j at bits BITS j) of a lane's words -> the
 // MFMA operand (B0 + c_j, B0 + c_{j+4}) in dword j, i.e. element e holds
-// code perm4(e).
+// code perm4(e).  MIXED (2-bit codes): dwords 0 and 2 take their codes at
+// mantissa bits 6..7 under 2^4 (B = 16), dwords 1 and 3 at bits 8..9 under
+// 2^2 (B = 4), so that one shift serves two dwords: seven operations per
+// piece instead of nine.  The extra 12 of dwords 0 and 2 is folded into the
+// staged offsets with the rest of B.
 template <int BITS>
+__host__ __device__ constexpr float mixed_extra_bias(int j)
+{
+    return BITS == 2 && (j & 1) == 0 ? 12.0f : 0.0f;
+}
+
+template <int BITS, bool MIXED = false>
 __device__ __forceinline__ half8 biased_codes(const uint32_t* w, int k, const CodeBits& cb)
 {
     u32x4 v;
@@ -273,6 +287,15 @@ __device__ __forceinline__ half8 biased_codes(const uint32_t* w, int k, const Co
         v.y = ((x << 2) & cb.mask) | cb.magic;
         v.z = ((x >> 2) & cb.mask) | cb.magic;
         v.w = ((x >> 6) & cb.mask) | cb.magic;
+    } else if constexpr (MIXED) {
+        // codes j, j + 4 at bits 2j, 16 + 2j of z; z << 6 puts codes 0 and 1
+        // at bits 6..7 and 8..9, z << 2 codes 2 and 3
+        const uint32_t z = __builtin_amdgcn_perm(0u, w[k >> 1], (k & 1) ? 0x0c030c02u : 0x0c010c00u);
+        const uint32_t t1 = z << 6, t2 = z << 2;
+        v.x = (t1 & 0x00C000C0u) | cb.mag16;
+        v.y = (t1 & cb.mask) | cb.magic;
+        v.z = (t2 & 0x00C000C0u) | cb.mag16;
+        v.w = (t2 & cb.mask) | cb.magic;
     } else {
         // bytes (c0..c3) and (c4..c7) of the piece to bytes 0 and 2
         const uint32_t z = __builtin_amdgcn_perm(0u, w[k >> 1], (k & 1) ? 0x0c030c02u : 0x0c010c00u);
@@ -520,8 +543,12 @@ struct Split {
                 const int ds = key ? c : 2 * mm.kp + (c - mm.kp);
                 const int dz = key ? mm.kp + c : 2 * mm.kp + vp + (c - mm.kp);
                 wl[ds] = float4{sv[0] * fs, sv[1] * fs, sv[2] * fs, sv[3] * fs};
-                wl[dz] = float4{(z0 * zv[0] + zs * sv[0]) * f, (z0 * zv[1] + zs * sv[1]) * f,
-                                (z0 * zv[2] + zs * sv[2]) * f, (z0 * zv[3] + zs * sv[3]) * f};
+                // the mixed 2-bit operands' extra bias of even components
+                // (channel or token i of a chunk sits in operand dword i)
+                const float xb = key ? (C::PERCH ? mixed_extra_bias<C::KBITS>(0) : 0.0f) : mixed_extra_bias<C::VBITS>(0);
+                const float zse = zs - xb;
+                wl[dz] = float4{(z0 * zv[0] + zse * sv[0]) * f, (z0 * zv[1] + zs * sv[1]) * f,
+                                (z0 * zv[2] + zse * sv[2]) * f, (z0 * zv[3] + zs * sv[3]) * f};
             }
         }
         const float4* ks = wl;
@@ -600,8 +627,8 @@ struct Split {
             for (int kb = 0; kb < NKB; ++kb) {
                 const half8 bh = *(const half8*)(pc.slots + pc.rbase + 128 * kb);
                 const half8 bl = *(const half8*)(pc.slots + pc.rbase + 128 * kb + 16);
-                const half8 a0 = biased_codes<C::KBITS>(r.k[0], kb, kcb);
-                const half8 a1 = biased_codes<C::KBITS>(r.k[1], kb, kcb);
+                const half8 a0 = biased_codes<C::KBITS, true>(r.k[0], kb, kcb);
+                const half8 a1 = biased_codes<C::KBITS, true>(r.k[1], kb, kcb);
                 acc0 = mfma16(a0, bh, acc0);
                 acc0 = mfma16(a0, bl, acc0);
                 acc1 = mfma16(a1, bh, acc1);
@@ -658,7 +685,7 @@ struct Split {
 #pragma unroll
             for (int j = 0; j < C::MBPG; ++j) {
                 const int mb = pass * C::MBPG + j;
-                const half8 a = biased_codes<C::VBITS>(r.v, mb, vcb);
+                const half8 a = biased_codes<C::VBITS, true>(r.v, mb, vcb);
                 oacc[mb] = mfma16(a, ph, oacc[mb]);
                 oacc[mb] = mfma16(a, pl, oacc[mb]);
             }
@@ -921,7 +948,8 @@ __device__ __forceinline__ void split_body(const AttnParams& p, uint8_t* lds)
         __syncthreads();
     }
 
-    const CodeBits kcb = code_bits<C::KBITS>(), vcb = code_bits<C::VBITS>();
+    const CodeBits kcb = code_bits<C::KBITS>();
+    const CodeBits vcb = C::KBITS == C::VBITS ? kcb : code_bits<C::VBITS>();
     {
         float4* wl = (float4*)region;
         // NBUF register sets rotate: while block blk is computed, the loads
