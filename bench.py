@@ -18,8 +18,13 @@ fence that torch's events carry):
          Infinity Cache (MALL) and the L2s, so every step streams its
          weights and cache from HBM.  ``value`` is B K / (sum of the K step
          durations), with events only at the step boundaries; a second cold
-         pass with events between the calls gives the per-call breakdown,
-         and ``roofline`` uses its attention launches;
+         pass with events between the calls gives the per-call breakdown
+         (``*_marker_events``: each recorded event is a packet of its own,
+         about 4 µs on this GPU), and a third times the projection and the
+         attention calls with events recorded by their kernels' own
+         dispatches (kvq_time_launches: first kernel's start to last
+         kernel's end, as a profiler's kernel trace measures them);
+         ``roofline`` and the per-call times use the third;
   warm   the same K steps back to back from the same starting cache, with
          nothing in between (the serving loop as it runs): ``warm``.
 The K steps are bracketed by a device synchronize on both sides.
@@ -113,6 +118,11 @@ class FenceFreeEvent:
     def record(self):
         if FenceFreeEvent._lib.hipEventRecord(self._ev, self._torch.cuda.current_stream().cuda_stream) != 0:
             raise RuntimeError("hipEventRecord failed")
+
+    @property
+    def handle(self) -> int:
+        """The hipEvent_t, for kvq_time_launches (recorded by the kernels' own dispatches)."""
+        return self._ev.value
 
     def elapsed_time(self, end) -> float:
         """Milliseconds from this event to `end` (both recorded and complete)."""
@@ -241,6 +251,7 @@ def main():
                      "achieved": att["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": att["gbs"] / HBM_PEAK_GBS, "traffic": traffic,
                      "bytes_per_launch": att["bytes_per_launch"], "us_per_launch": att["us"],
+                     "us_per_launch_marker_events": att["us_marker_events"],
                      "copy_gbs": copy_gbs, "frac_of_copy": att["gbs"] / copy_gbs},
         "attention_us_per_step": att["us"],
         "projection": res["projection"],
@@ -278,7 +289,8 @@ def summary(res):
            "attention_us": a["us"], "attention_gbs": a["gbs"], "attention_frac": a["gbs"] / HBM_PEAK_GBS,
            "attention_bytes": a["bytes_per_launch"],
            "projection_us": p["us"], "projection_gbs": p["gbs"], "projection_frac": p["gbs"] / HBM_PEAK_GBS,
-           "fused_append": p["fused_append"], "append_us": res["append_us"]}
+           "fused_append": p["fused_append"], "append_us": res["append_us"],
+           "attention_us_marker_events": a["us_marker_events"], "projection_us_marker_events": p["us_marker_events"]}
     if res.get("warm"):
         w = res["warm"]
         out.update({"warm_tokens_per_s": w["tokens_per_s"], "warm_attention_us": w["attention_us"],
@@ -364,24 +376,37 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
     def new_events(k):
         return [FenceFreeEvent(torch) for _ in range(k)]
 
-    def step(i, ev=None):
+    def step(i, ev=None, dev=None):
         """One decode step; ev = 4 events: before, after the projection (and
-        the fused append), after the append, after the attention."""
+        the fused append), after the append, after the attention.  dev = 4
+        events recorded by the kernels' own dispatches (kvq_time_launches):
+        the projection call's first kernel start and last kernel end, then
+        the attention call's."""
         if ev is not None:
             ev[0].record()
+        if dev is not None:
+            kvq.time_launches(dev[0].handle, dev[1].handle)
         if fused:
             kvq.project_append(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, cache, 1, wsd)
+            if dev is not None:
+                kvq.time_launches(None, None)
             if ev is not None:
                 ev[1].record()
                 ev[2].record()
         else:
             kvq.project_qkv(Hsteps[i], W, A, Bm, wl.rank, wl.lora_scale, wl.d_q, wl.d_kv, Qd, Kd, Vd, wsd)
+            if dev is not None:
+                kvq.time_launches(None, None)
             if ev is not None:
                 ev[1].record()
             cache.append(Kv, Vv)
             if ev is not None:
                 ev[2].record()
+        if dev is not None:
+            kvq.time_launches(dev[2].handle, dev[3].handle)
         cache.decode_attn(Qv, Hq, sm, O, wsa)
+        if dev is not None:
+            kvq.time_launches(None, None)
         if ev is not None:
             ev[3].record()
 
@@ -412,7 +437,10 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
                 restart()
             flush()
             n_at.append(wl.context + j + 1)
-            if breakdown:
+            if breakdown == "dispatch":
+                evs.append(new_events(4))
+                step(j, dev=evs[-1])
+            elif breakdown:
                 evs.append(new_events(4))
                 step(j, evs[-1])
             else:
@@ -427,19 +455,25 @@ def decode_run(wl, steps, warmup, with_warm, flush_buf, args, dev, alloc_proj, b
     n_at, evs = cold(False)
     step_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     _, bev = cold(True)
-    proj_ms = np.array([e[0].elapsed_time(e[1]) for e in bev])
+    proj_mk = np.array([e[0].elapsed_time(e[1]) for e in bev])
     app_ms = np.array([e[1].elapsed_time(e[2]) for e in bev])
-    attn_ms = np.array([e[2].elapsed_time(e[3]) for e in bev])
+    attn_mk = np.array([e[2].elapsed_time(e[3]) for e in bev])
+    # the calls' device time from their kernels' own dispatch timestamps
+    _, dev = cold("dispatch")
+    proj_ms = np.array([e[0].elapsed_time(e[1]) for e in dev])
+    attn_ms = np.array([e[2].elapsed_time(e[3]) for e in dev])
     bytes_launch = np.array([configs.attention_bytes(wl, n) for n in n_at], dtype=np.float64)
     proj_bytes = configs.projection_weight_bytes(wl.d_in, wl.d_q, wl.d_kv, wl.rank) + 2 * B * (wl.d_in + wl.d_qkv)
     res = {
         "tokens_per_s": B * steps / (step_ms.sum() * 1e-3),
         "ms_per_step": float(step_ms.mean()),
         "attention": {"us": float(attn_ms.mean() * 1e3), "bytes_per_launch": float(bytes_launch.mean()),
-                      "gbs": float(bytes_launch.mean() / (attn_ms.mean() * 1e-3) / 1e9)},
+                      "gbs": float(bytes_launch.mean() / (attn_ms.mean() * 1e-3) / 1e9),
+                      "us_marker_events": float(attn_mk.mean() * 1e3)},
         "projection": {"us": float(proj_ms.mean() * 1e3), "bytes_per_call": int(proj_bytes),
                        "gbs": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9),
                        "frac": float(proj_bytes / (proj_ms.mean() * 1e-3) / 1e9 / HBM_PEAK_GBS),
+                       "us_marker_events": float(proj_mk.mean() * 1e3),
                        "fused_append": fused},
         "append_us": float(app_ms.mean() * 1e3),
     }

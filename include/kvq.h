@@ -291,6 +291,20 @@ kvq_status kvq_decode_attn_noalloc(const kvq_cache* cache, const void* Q, int H_
 kvq_status kvq_prefill_attn(const kvq_cache* cache, const void* Q, int C, int H_q, float sm_scale, void* O,
                             void* stream);
 
+/* Measurement hook for benchmarks (not part of the method).  While set
+ * (both events non-null), every kernel the library launches from this host
+ * thread records stop_event when it completes, and the first of them after
+ * this call also records start_event when it begins, both from the
+ * kernels' own dispatch timestamps (hipExtLaunchKernel).  After one library
+ * call, hipEventElapsedTime(start, stop) is that call's device time, from
+ * its first kernel's start to its last kernel's end, without the marker
+ * packets that hipEventRecord would add on either side.  The events are
+ * hipEvent_t values created by the caller with timing enabled and owned by
+ * it; kvq_time_launches(NULL, NULL) clears the request.  The request is
+ * per host thread and launches nothing itself.  Returns KVQ_ERR_ARG when
+ * exactly one of the two events is null. */
+kvq_status kvq_time_launches(void* start_event, void* stop_event);
+
 /* Static description of a status code. */
 const char* kvq_strerror(kvq_status status);
 

@@ -495,22 +495,22 @@ hipError_t launch_append_d(const AppendParams& p, hipStream_t stream)
 {
     const int units = p.B * p.H;
     if (p.n_new == 1 && p.ring == 0 && p.k_axis == KVQ_PER_TOKEN) {
-        hipLaunchKernelGGL(append_token_kernel<D>, dim3(units), dim3(D), 0, stream, p);
+        launch_kernel(append_token_kernel<D>, dim3(units), dim3(D), 0, stream, p);
         return hipGetLastError();
     }
     if (p.q1 > p.q0) {
         const int nblk = (p.q1 + kBlockTok - 1) / kBlockTok - p.q0 / kBlockTok;
         if (p.k_axis == KVQ_PER_CHANNEL)
-            hipLaunchKernelGGL((append_code_kernel<D, true>), dim3(nblk, units), dim3(kThreads), 0, stream, p);
+            launch_kernel((append_code_kernel<D, true>), dim3(nblk, units), dim3(kThreads), 0, stream, p);
         else
-            hipLaunchKernelGGL((append_code_kernel<D, false>), dim3(nblk, units), dim3(kThreads), 0, stream, p);
+            launch_kernel((append_code_kernel<D, false>), dim3(nblk, units), dim3(kThreads), 0, stream, p);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
     }
     int n1 = p.n0 + p.n_new;
     if (p.ring && n1 > p.ring_lo) {
-        hipLaunchKernelGGL(append_ring_kernel<D>, dim3(n1 - p.ring_lo, units), dim3(kThreads), 0, stream, p);
+        launch_kernel(append_ring_kernel<D>, dim3(n1 - p.ring_lo, units), dim3(kThreads), 0, stream, p);
         return hipGetLastError();
     }
     return hipSuccess;
@@ -520,7 +520,7 @@ template <int D>
 hipError_t launch_rows_d(const AppendParams& p, int hi, hipStream_t stream)
 {
     if (hi > p.ring_lo)
-        hipLaunchKernelGGL(append_ring_kernel<D>, dim3(hi - p.ring_lo, p.B * p.H), dim3(kThreads), 0, stream, p);
+        launch_kernel(append_ring_kernel<D>, dim3(hi - p.ring_lo, p.B * p.H), dim3(kThreads), 0, stream, p);
     return hipGetLastError();
 }
 

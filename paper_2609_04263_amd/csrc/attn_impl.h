@@ -1159,7 +1159,7 @@ int resident_per_cu(const AttnParams& p)
 template <class C>
 hipError_t launch_split(const AttnParams& p, hipStream_t stream)
 {
-    hipLaunchKernelGGL(decode_split_kernel<C>, dim3(p.S_tot, p.B * p.H), dim3(C::THREADS), p.lds_bytes, stream, p);
+    launch_kernel(decode_split_kernel<C>, dim3(p.S_tot, p.B * p.H), dim3(C::THREADS), p.lds_bytes, stream, p);
     return hipGetLastError();
 }
 
@@ -1218,7 +1218,7 @@ template <int D>
 hipError_t launch_merge(const AttnParams& p, hipStream_t stream)
 {
     const int rows = p.B * p.H_q, per = kMergeThreads / D;
-    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3((rows + per - 1) / per), dim3(kMergeThreads), 0, stream, p);
+    launch_kernel(decode_merge_kernel<D>, dim3((rows + per - 1) / per), dim3(kMergeThreads), 0, stream, p);
     return hipGetLastError();
 }
 

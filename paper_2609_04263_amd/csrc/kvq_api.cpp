@@ -126,6 +126,12 @@ T* at(const kvq_cache* c, int section)
 
 namespace kvq {
 
+LaunchTiming& launch_timing()
+{
+    static thread_local LaunchTiming t;
+    return t;
+}
+
 int num_tail(const kvq_format& f, int n)
 {
     return n > f.sink ? n - f.sink : 0;
@@ -238,6 +244,16 @@ kvq_status project_append_window(const void* H, int M, int d_in, const void* W, 
 }  // namespace
 
 extern "C" {
+
+kvq_status kvq_time_launches(void* start_event, void* stop_event)
+{
+    if ((start_event == nullptr) != (stop_event == nullptr))
+        return KVQ_ERR_ARG;
+    kvq::LaunchTiming& t = kvq::launch_timing();
+    t.start = (hipEvent_t)start_event;
+    t.stop = (hipEvent_t)stop_event;
+    return KVQ_OK;
+}
 
 const char* kvq_strerror(kvq_status s)
 {

@@ -2,6 +2,7 @@
 // Nothing here is part of the public C ABI (include/kvq.h).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -19,6 +20,26 @@ struct kvq_cache {
 };
 
 namespace kvq {
+
+// Launch timing requested by kvq_time_launches on this host thread: while
+// stop is set, every kernel the library launches records stop when it
+// completes and the first one records start when it begins, from the
+// kernel's own dispatch timestamps.
+struct LaunchTiming {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchTiming& launch_timing();
+
+// Every kernel launch of the library (hipExtLaunchKernelGGL with the
+// requested events, null when none are).
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t stream, Args... args)
+{
+    LaunchTiming& t = launch_timing();
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, stream, t.stop ? t.start : nullptr, t.stop, 0u, args...);
+    if (t.stop)
+        t.start = nullptr;
+}
 
 // Tail tokens (past the sink) at length n.
 int num_tail(const kvq_format& f, int n);

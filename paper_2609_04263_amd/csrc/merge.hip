@@ -163,7 +163,7 @@ hipError_t launch_merge(const MergeParams& p, hipStream_t stream)
     if (p.rank < 1 || p.rank > kMaxRank)
         return hipErrorInvalidValue;
     dim3 grid((p.d_in + kMC - 1) / kMC, (N + kMT - 1) / kMT);
-    hipLaunchKernelGGL(merge_kernel, grid, dim3(256), merge_lds_bytes(p), stream, p);
+    launch_kernel(merge_kernel, grid, dim3(256), merge_lds_bytes(p), stream, p);
     return hipGetLastError();
 }
 

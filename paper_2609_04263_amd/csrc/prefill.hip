@@ -567,7 +567,7 @@ hipError_t launch(const AttnParams& p, hipStream_t stream)
     const bool w8 = p.k_bits == 8;  // 8-bit codes come as K and V both 8-bit
     void (*kern)(AttnParams) = w8 ? prefill_kernel<D, true> : prefill_kernel<D, false>;
     const size_t lds = w8 ? lds_bytes<D, true>() : lds_bytes<D, false>();
-    hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, stream, p);
+    launch_kernel(kern, grid, dim3(kThreads), lds, stream, p);
     return hipGetLastError();
 }
 

@@ -563,7 +563,7 @@ hipError_t launch_stream(const ProjParams& p, hipStream_t stream)
 {
     using S = StreamShape<G, GH, FA>;
     const size_t lds = S::TL_OFFSET + (p.rank > 0 ? stream_tl_bytes(p.M, p.rank) : 0);
-    hipLaunchKernelGGL((proj_stream_kernel<G, GH, FA>), dim3((p.N + S::RG - 1) / S::RG), dim3(kSWaves * 64), lds,
+    launch_kernel((proj_stream_kernel<G, GH, FA>), dim3((p.N + S::RG - 1) / S::RG), dim3(kSWaves * 64), lds,
                        stream, p);
     return hipGetLastError();
 }
@@ -1415,9 +1415,9 @@ hipError_t launch_project_decode(const ProjParams& p, hipStream_t stream)
         a.yf = (float*)p.t;
         dim3 grid((3 * p.rank + 15) / 16, q.tslices);
         if (p.M <= 16)
-            hipLaunchKernelGGL(proj_tpart_kernel<1>, grid, dim3(kTWaves * 64), 0, stream, a, 64 * per);
+            launch_kernel(proj_tpart_kernel<1>, grid, dim3(kTWaves * 64), 0, stream, a, 64 * per);
         else
-            hipLaunchKernelGGL(proj_tpart_kernel<2>, grid, dim3(kTWaves * 64), 0, stream, a, 64 * per);
+            launch_kernel(proj_tpart_kernel<2>, grid, dim3(kTWaves * 64), 0, stream, a, 64 * per);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
@@ -1443,19 +1443,19 @@ hipError_t launch_project(const ProjParams& p, hipStream_t stream)
         q.nxcd = gemm_xcds();
         const int per = (tiles + q.nxcd - 1) / q.nxcd;
         if (q.fuse)
-            hipLaunchKernelGGL(proj_gemm_kernel<true>, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
+            launch_kernel(proj_gemm_kernel<true>, dim3(per * q.nxcd), dim3(kThreads), kGLds, stream, q);
         else
-            hipLaunchKernelGGL(proj_gemm_pp_kernel, dim3(per * q.nxcd), dim3(kPThreads), kPLds, stream, q);
+            launch_kernel(proj_gemm_pp_kernel, dim3(per * q.nxcd), dim3(kPThreads), kPLds, stream, q);
     } else if (p.yf && p.N <= 2 * kBN && p.M < 256 * kBM) {
         // activation pass with fewer than 256 row tiles of 128: 32-row tiles
         // (every workgroup also reads all of A, so more tiles only pay
         // until the grid covers the compute units; measured 80 -> 66 us at
         // M = 16384, slower at M = 65536)
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + 31) / 32);
-        hipLaunchKernelGGL(proj_big_kernel<1>, grid, dim3(kThreads), 0, stream, p);
+        launch_kernel(proj_big_kernel<1>, grid, dim3(kThreads), 0, stream, p);
     } else {
         dim3 grid((p.N + kBN - 1) / kBN, (p.M + kBM - 1) / kBM);
-        hipLaunchKernelGGL(proj_big_kernel<4>, grid, dim3(kThreads), 0, stream, p);
+        launch_kernel(proj_big_kernel<4>, grid, dim3(kThreads), 0, stream, p);
     }
     return hipGetLastError();
 }

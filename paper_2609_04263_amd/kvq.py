@@ -66,10 +66,12 @@ def _load() -> C.CDLL:
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
     L.kvq_decode_attn_noalloc.argtypes = [P, P, I, C.c_float, P, P]
     L.kvq_prefill_attn.argtypes = [P, P, I, I, C.c_float, P, P]
+    L.kvq_time_launches.argtypes = [P, P]
     for name in ("kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section", "kvq_cache_reset",
                  "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_project_workspace_bytes",
                  "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
-                 "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn"):
+                 "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn",
+                 "kvq_time_launches"):
         getattr(L, name).restype = I
     return L
 
@@ -78,7 +80,8 @@ _lib = _load()
 EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section",
             "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
             "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
-            "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn")
+            "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn",
+            "kvq_time_launches")
 
 
 def lib() -> C.CDLL:
@@ -249,3 +252,12 @@ def merge_adapter(W, A, Bm, rank: int, lora_scale: float, d_q: int, d_kv: int, W
                                 _stream(stream))
     if st:
         _check(st, "merge_adapter")
+
+
+def time_launches(start_event, stop_event) -> None:
+    """Measurement hook: while set, the library's kernels record the two
+    hipEvent_t handles (ints) from their own dispatches (see
+    kvq_time_launches); time_launches(None, None) clears it."""
+    st = _lib.kvq_time_launches(start_event, stop_event)
+    if st:
+        _check(st, "time_launches")

@@ -224,3 +224,11 @@ class _Shape(FakeStorage):
     def __init__(self, M, d_in):
         super().__init__(0, FAKE)
         self.shape = (M, d_in)
+
+
+def test_time_launches_argument_checks(kvq):
+    """The measurement hook takes both events or neither; it launches nothing."""
+    lib = kvq.lib()
+    assert lib.kvq_time_launches(C.c_void_p(FAKE), None) == 1          # KVQ_ERR_ARG
+    assert lib.kvq_time_launches(None, C.c_void_p(FAKE)) == 1
+    assert lib.kvq_time_launches(None, None) == 0
