@@ -648,15 +648,16 @@ def bench_prefill_attn(args, wl, cache, sm, dev, synth, torch):
     C, n = wl.chunk, wl.context
     Q = synth.normal_bf16_device(wl.seed, "prefill-attn-q", (B, C, Hq, D), device=dev)
     O = torch.empty((B, C, Hq, D), dtype=torch.float32, device=dev)
+    ws = cache.prefill_workspace(dev)
     for _ in range(args.warmup):
-        cache.prefill_attn(Q, C, Hq, sm, O)
+        cache.prefill_attn(Q, C, Hq, sm, O, ws)
     steps = args.steps or 20
     torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record()
     for _ in range(steps):
-        cache.prefill_attn(Q, C, Hq, sm, O)
+        cache.prefill_attn(Q, C, Hq, sm, O, ws)
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps

@@ -285,11 +285,22 @@ kvq_status kvq_decode_attn_noalloc(const kvq_cache* cache, const void* Q, int H_
  * Reconstructed keys and values (after rotation, for a rotating format)
  * enter the products as binary16 MFMA operands, so their magnitudes must
  * stay below 65504 (binary16's largest finite value).
- * H_q a multiple of H_kv.  No workspace.  Pointers 16-byte aligned device
- * memory owned by the caller; invalid arguments return KVQ_ERR_ARG before
- * any launch. */
+ * H_q a multiple of H_kv.  Pointers 16-byte aligned device memory owned by
+ * the caller; invalid arguments return KVQ_ERR_ARG before any launch.
+ *   workspace  device scratch for the reconstructed blocks of each (b, h):
+ *              every visible 32-token block is reconstructed once per call
+ *              (192 D bytes each) and read back by all the chunk's query
+ *              tiles.  kvq_prefill_workspace_bytes gives the size that
+ *              serves all B H_kv units in one pass; a smaller workspace
+ *              (at least one unit's share, that size / (B H_kv)) makes the
+ *              call process the units in groups that fit, with more
+ *              launches.  Below one unit's share: KVQ_ERR_WORKSPACE.
+ *              Calls that share a workspace must not overlap. */
 kvq_status kvq_prefill_attn(const kvq_cache* cache, const void* Q, int C, int H_q, float sm_scale, void* O,
-                            void* stream);
+                            void* workspace, size_t ws_bytes, void* stream);
+/* Workspace bytes for kvq_prefill_attn on the cache at its current length
+ * (all units in one pass). */
+kvq_status kvq_prefill_workspace_bytes(const kvq_cache* cache, size_t* bytes);
 
 /* Measurement hook for benchmarks (not part of the method).  While set
  * (both events non-null), every kernel the library launches from this host

@@ -776,12 +776,37 @@ kvq_status kvq_decode_attn_noalloc(const kvq_cache* c, const void* Q, int H_q, f
     return kvq::launch_decode(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 
-kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, float sm_scale, void* O, void* stream)
+// Block images per (b, h) unit that a chunked prefill reconstructs: the sink
+// blocks holding tokens, then the tail's 32-token blocks.
+static void prefill_blocks(const kvq_cache* c, int* nsb, int* nvb)
+{
+    const int n_sink = c->n < c->fmt.sink ? c->n : c->fmt.sink;
+    const int tail = c->n > c->fmt.sink ? c->n - c->fmt.sink : 0;
+    *nsb = (n_sink + 31) / 32;
+    *nvb = *nsb + (tail + 31) / 32;
+}
+
+kvq_status kvq_prefill_workspace_bytes(const kvq_cache* c, size_t* bytes)
+{
+    if (!c || !bytes)
+        return KVQ_ERR_ARG;
+    int nsb, nvb;
+    prefill_blocks(c, &nsb, &nvb);
+    *bytes = (size_t)c->B * c->H * nvb * kvq::prefill_image_bytes(c->D);
+    return KVQ_OK;
+}
+
+kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, float sm_scale, void* O,
+                            void* workspace, size_t ws_bytes, void* stream)
 {
     if (!c || !Q || !O || !aligned16(Q) || !aligned16(O) || !isfinite(sm_scale))
         return KVQ_ERR_ARG;
     if (H_q < c->H || H_q % c->H != 0 || C < 1 || C > c->n)
         return KVQ_ERR_ARG;
+    int nsb, nvb;
+    prefill_blocks(c, &nsb, &nvb);
+    if (!workspace || !aligned16(workspace) || ws_bytes < (size_t)nvb * kvq::prefill_image_bytes(c->D))
+        return KVQ_ERR_WORKSPACE;
     const kvq_format& f = c->fmt;
     kvq::AttnParams p = {};
     p.nq = kvq::num_coded(f, c->n);
@@ -820,7 +845,10 @@ kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, f
     p.sm_log2 = sm_scale * 1.4426950408889634f;
     p.rot_c = rotation_constant(c->D);
     p.meta16 = f.meta_fp16;
-    return kvq::launch_prefill(p, c->D, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
+    p.pf_ws = (uint8_t*)workspace;
+    p.pf_nvb = nvb;
+    p.pf_nsb = nsb;
+    return kvq::launch_prefill(p, c->D, ws_bytes, (hipStream_t)stream) == hipSuccess ? KVQ_OK : KVQ_ERR_DEVICE;
 }
 
 }  // extern "C"

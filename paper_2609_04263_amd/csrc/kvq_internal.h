@@ -171,6 +171,12 @@ struct AttnParams {
     size_t lds_bytes;     // dynamic LDS of the split kernel
     int C;                // chunked prefill: query tokens (the newest C of the cache); q is [B][C][H_q][D]
     int meta16;           // scales and offsets stored as fp16 (ks..vz then point at halves)
+    // chunked prefill: workspace of block images [units of a group][pf_nvb][192 D bytes]
+    uint8_t* pf_ws;
+    int pf_u0;            // first unit (b H + h) of the group
+    int pf_nvb;           // images per unit: pf_nsb sink blocks, then the tail blocks
+    int pf_nsb;
+    int pf_tiles;         // query tiles per unit
 };
 // Workgroups of the split kernel that fit the device at once (all fields of p
 // that select the kernel instance and its LDS must be set).
@@ -185,6 +191,9 @@ int decode_split_bound(int B, int H);
 // Dynamic LDS of the split kernel.
 size_t decode_lds_bytes(int D, const kvq_format& f, int G);
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
-hipError_t launch_prefill(const AttnParams& p, int D, hipStream_t stream);
+// Bytes of one reconstructed 32-token block (prefill workspace unit).
+size_t prefill_image_bytes(int D);
+// Chunked prefill over units in groups that fit ws_bytes (at least one unit).
+hipError_t launch_prefill(const AttnParams& p, int D, size_t ws_bytes, hipStream_t stream);
 
 }  // namespace kvq

@@ -2,33 +2,39 @@
 // consumes chunks; the chunk's states are coded and appended, then its
 // queries attend causally over the reconstruction of everything stored).
 //
-// One workgroup per (sequence, KV head, tile of query rows); query rows are
-// the (chunk token, head of the KV group) pairs in token-major order.  Each
-// of the eight waves owns 16 QN query rows (the block reconstruction below
-// is shared by all of them, so a workgroup takes as many rows as the
-// registers allow: 128 / 256 / 512 at D = 256 / 128 / 64); the workgroup
-// walks the 32-token key blocks up to its newest query's position:
-//   1. the block is reconstructed into LDS (all 512 threads, one eight-code
-//      piece of K and one of V each per step) from a raw copy of its codes
-//      and metadata that was fetched into LDS while the previous block was
-//      computed (each section of the cache is blocked by 32 tokens, so a
-//      block's bytes are six contiguous ranges): k_hat in fp32 stored as
-//      fp16 hi + lo (hi + lo carries ~22 bits) as [token][D], v_hat as fp16,
-//      transposed [D][token];
-//   2. scores S^T = K Q^T with v_mfma_f32_16x16x32_f16 (keys as rows, query
-//      rows as columns; hi x hi + hi x lo + lo x hi), queries pre-scaled by
-//      sm_scale * log2(e) so the softmax runs in base 2, online per column
-//      (the running maximum moves only in steps of more than 2^8);
-//   3. O^T += V^T P^T in fp16 (probabilities in [0, 1] and values each
-//      carry an 11-bit relative rounding, well inside the output bound; the
-//      logits are the precision-critical product).  A lane holds
-//      score rows 4 q + i of the block's two 16-key tiles, which are exactly
-//      the eight k-slots 8 q .. 8 q + 7 its next MFMA operand needs when the
-//      keys of slot 8 q + e are taken as 4 q + e (e < 4) and 16 + 4 q + e - 4:
-//      V^T is read in that key order, so probabilities never cross lanes.
-// Sink tokens (fp16 rows) are walked first as blocks of their own, so every
-// query row holds a finite running maximum before the coded tail; fp16
-// window tokens past the coded ones are read from the ring in step 1.
+// Two launches per group of (sequence, KV head) units:
+//   1. dequant_kernel reconstructs every visible 32-token block of a unit
+//      once into a workspace "block image" (192 D bytes): k_hat in fp32
+//      stored as fp16 hi + lo (hi + lo carries ~22 bits) as [token][D] rows,
+//      v_hat as fp16 transposed [D][32 key slots].  The image is laid out
+//      exactly as the attention kernel reads it from LDS (16-byte chunks
+//      xor-swizzled by row so that the fragment reads are free of bank
+//      conflicts), so it moves to LDS with plain linear copies.
+//   2. attn_kernel: one workgroup per (unit, tile of query rows); query rows
+//      are the (chunk token, head of the KV group) pairs in token-major
+//      order.  Each of the eight waves owns 16 QN query rows (128 / 256 / 512
+//      rows per workgroup at D = 256 / 128 / 64).  Block images stream into
+//      a ring of LDS stages with global_load_lds_dwordx4 (no registers, no
+//      vector work), several blocks ahead, and per block:
+//      - scores S^T = K Q^T with v_mfma_f32_16x16x32_f16 (keys as rows,
+//        query rows as columns; hi x hi + hi x lo + lo x hi), queries
+//        pre-scaled by sm_scale * log2(e) so the softmax runs in base 2,
+//        online per column (the running maximum moves only in steps of more
+//        than 2^8);
+//      - O^T += V^T P^T in fp16 (probabilities in [0, 1] and values each
+//        carry an 11-bit relative rounding, well inside the output bound;
+//        the logits are the precision-critical product).  A lane holds
+//        score rows 4 q + i of the block's two 16-key tiles, which are
+//        exactly the eight k-slots 8 q .. 8 q + 7 its next MFMA operand
+//        needs when the keys of slot 8 q + e are taken as 4 q + e (e < 4)
+//        and 16 + 4 q + e - 4; the image stores V^T in that key order, so
+//        probabilities never cross lanes and a value operand is one read.
+// Reconstructing once per unit instead of once per query tile is what the
+// workspace buys: a 2048-token chunk has 4096 query rows per KV head at
+// grouping 2, i.e. 32 tiles that would each rebuild every block.
+// Sink tokens (fp16 rows) come first as blocks of their own, so every query
+// row holds a finite running maximum before the coded tail; fp16 window
+// tokens past the coded ones are copied into the image from the ring.
 // Rotated formats transform the queries (FWHT in LDS) and the outputs back.
 
 #include "kvq_internal.h"
@@ -37,7 +43,7 @@
 namespace kvq {
 namespace pre {
 
-constexpr int kWaves = 8, kThreads = 512;
+constexpr int kWaves = 8, kThreads = 512, kDqThreads = 256;
 
 // query rows per wave (16 QN): the accumulators take D QN / 4 registers
 template <int D>
@@ -52,27 +58,43 @@ constexpr int rows_per_tile()
     return kWaves * 16 * qn<D>();
 }
 
-// Raw bytes of one 32-token block: codes (4 D pieces of at most 4 bytes, 8
-// for 8-bit codes) and metadata (at most D floats per section) of K and V.
-template <int D, bool W8>
-constexpr int raw_bytes()
-{
-    return 2 * 4 * D * (W8 ? 8 : 4) + 4 * D * 4;
-}
-
-// LDS (bytes): K hi/lo [32][D + 8], V^T [D][40] (fp16), then the raw block;
-// the query and output rotation buffers ([rows][D] fp32) reuse the K/V part.
+// One reconstructed 32-token block: K hi [32][D], K lo [32][D] (fp16), then
+// V^T [D][32] (fp16).
 template <int D>
-constexpr size_t kv_bytes()
+constexpr int image_bytes()
 {
-    return 2 * 32 * (D + 8) * 2 + D * 40 * 2;
+    return 192 * D;
 }
 
-template <int D, bool W8>
-constexpr size_t lds_bytes()
+// LDS ring depth (block images in flight)
+template <int D>
+constexpr int stages()
 {
-    constexpr size_t rot = (size_t)rows_per_tile<D>() * D * 4;
-    return (kv_bytes<D>() > rot ? kv_bytes<D>() : rot) + raw_bytes<D, W8>();
+    return D == 256 ? 3 : 4;
+}
+
+// LDS: the ring, or the query / output staging [rows][D] fp32 when larger
+// (both are used by the same workgroup at different times).
+template <int D>
+constexpr size_t attn_lds_bytes()
+{
+    constexpr size_t ring = (size_t)stages<D>() * image_bytes<D>();
+    constexpr size_t rows = (size_t)rows_per_tile<D>() * D * 4;
+    return ring > rows ? ring : rows;
+}
+
+// 16-byte chunk c of K row r sits at chunk c ^ kswz(r): the 16 lanes of a
+// fragment read (16 rows, one chunk each) then cover all 64 banks.
+template <int D>
+__host__ __device__ constexpr int kswz(int r)
+{
+    return D >= 128 ? (r & 15) : ((r >> 1) & 7);
+}
+
+// key-slot chunk q of V^T row d sits at chunk q ^ vswz(d) (64-byte rows)
+__host__ __device__ constexpr int vswz(int d)
+{
+    return (d >> 2) & 3;
 }
 
 __device__ __forceinline__ float dq(int mode, int bits, uint32_t c, float s, float z)
@@ -81,35 +103,16 @@ __device__ __forceinline__ float dq(int mode, int bits, uint32_t c, float s, flo
 }
 
 // scale or offset i of a raw metadata range (fp32, or fp16 with meta16)
-__device__ __forceinline__ float meta(const uint8_t* sec, int i, bool m16)
+__device__ __forceinline__ float meta(const uint8_t* sec, size_t i, bool m16)
 {
     return m16 ? f16_bits_to_f32(((const uint16_t*)sec)[i]) : ((const float*)sec)[i];
 }
 
-// eight consecutive scales or offsets from element i (a multiple of 8)
-__device__ __forceinline__ void meta8(const uint8_t* sec, int i, bool m16, float* v)
-{
-    if (m16) {
-        const u32x4 h = *(const u32x4*)(sec + 2 * i);
-        const uint32_t w[4] = {h.x, h.y, h.z, h.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            v[e] = f16_bits_to_f32((uint16_t)(w[e >> 1] >> (16 * (e & 1))));
-    } else {
-        const floatx4 a = *(const floatx4*)(sec + 4 * i), b = *(const floatx4*)(sec + 4 * i + 16);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            v[e] = a[e];
-            v[e + 4] = b[e];
-        }
-    }
-}
-
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
-// Eight codes of piece idx of a raw code range (8-bit: two u32; 4-bit: one
-// u32; 2-bit: one u16), as the words holding codes 0..3 and 4..7 (the same
-// word unless the codes are 8-bit).
+// Eight codes of piece idx of a block's code range (8-bit: two u32; 4-bit:
+// one u32; 2-bit: one u16), as the words holding codes 0..3 and 4..7 (the
+// same word unless the codes are 8-bit).
 struct Piece {
     uint32_t lo, hi;
 };
@@ -132,13 +135,9 @@ __device__ __forceinline__ uint32_t code_of(const Piece& w, int bits, int e)
     return (x >> ((bits * e) & 31)) & ((1u << bits) - 1u);
 }
 
-
-__device__ __forceinline__ void split8(const float* v, uint16_t* hi, uint16_t* lo)
+__device__ __forceinline__ float half_bits(const uint16_t* row, size_t i)
 {
-    half8 h, l;
-    split_half8(v, &h, &l);
-    *(u32x4*)hi = __builtin_bit_cast(u32x4, h);
-    *(u32x4*)lo = __builtin_bit_cast(u32x4, l);
+    return f16_bits_to_f32(row[i]);
 }
 
 // In-place unnormalized FWHT of rows [rows][D] fp32 in LDS, then * c.
@@ -160,26 +159,200 @@ __device__ void fwht_rows(float* x, int rows, float c)
     __syncthreads();
 }
 
-// W8: both code widths are 8 bits (a raw block twice as large); otherwise
-// 2 or 4 bits each.
+// ---------------------------------------------------------------------------
+// 1. Block images.  Grid (blocks per unit, units of the group); workspace
+// block v of a unit is sink block v for v < pf_nsb, else tail block
+// v - pf_nsb.  Tokens past the end (sink rows beyond n_sink, tail tokens
+// beyond n) are zeros: the causal mask removes them, and zero values keep
+// 0 * v finite.  W8: both code widths are 8 bits.
 template <int D, bool W8>
-__global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
+__global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
+{
+    const int v = blockIdx.x;
+    const int unit = p.pf_u0 + blockIdx.y;
+    uint8_t* img = p.pf_ws + ((size_t)blockIdx.y * p.pf_nvb + v) * (size_t)image_bytes<D>();
+    const bool sinkblk = v < p.pf_nsb;
+    const int blk = v - p.pf_nsb;
+
+    const int kbits = W8 ? 8 : p.k_bits, vbits = W8 ? 8 : p.v_bits;
+    const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
+    const bool m16 = p.meta16 != 0;
+    const int msz = m16 ? 2 : 4;
+    // byte lengths of one block's sections: codes, scales, offsets of K and V
+    const int len0 = 4 * D * kbits;
+    const int kmeta = p.k_axis == KVQ_PER_TOKEN ? (D / p.k_group) * 32 * msz : D * msz;
+    const int len3 = 4 * D * vbits, vmeta = (D / p.v_group) * 32 * msz;
+    const size_t ibf = (size_t)unit * (p.T >> 5) + (sinkblk ? 0 : blk);
+    const uint8_t* rkc = (const uint8_t*)p.kc + ibf * len0;
+    const uint8_t* rks = (const uint8_t*)p.ks + ibf * kmeta;
+    const uint8_t* rkz = kaff ? (const uint8_t*)p.kz + ibf * kmeta : nullptr;
+    const uint8_t* rvc = (const uint8_t*)p.vc + ibf * len3;
+    const uint8_t* rvs = (const uint8_t*)p.vs + ibf * vmeta;
+    const uint8_t* rvz = vaff ? (const uint8_t*)p.vz + ibf * vmeta : nullptr;
+    const size_t sbase = (size_t)unit * p.sink;
+    const size_t rbase = (size_t)unit * p.ring;
+
+    for (int pc = threadIdx.x; pc < 4 * D; pc += kDqThreads) {
+        // K piece: token tau = pc / (D / 8), channels 8 P .. 8 P + 7
+        {
+            const int tau = pc / (D / 8), P = pc % (D / 8);
+            float x[8];
+            const uint16_t* row = nullptr;  // fp16 source row (sink or window)
+            bool coded = false;
+            if (sinkblk) {
+                const int ts = 32 * v + tau;
+                if (ts < p.n_sink)
+                    row = p.kq + (sbase + ts) * D;
+            } else {
+                const int t = 32 * blk + tau;
+                if (t < p.nq)
+                    coded = true;
+                else if (t < p.n)
+                    row = p.kr + (rbase + t % p.ring) * D;
+            }
+            if (coded) {
+                const int r = 4 * (tau / 8) + tau % 4, half = (tau / 4) % 2;
+                const int idx = (half * 64 + r + 16 * (P % 4)) * (D / 32) + P / 4;
+                const Piece w = piece<W8>(rkc, idx, kbits);
+                if (p.k_axis == KVQ_PER_TOKEN) {
+                    const int mi = ((8 * P) / p.k_group) * 32 + tau;
+                    const float sc = meta(rks, mi, m16), z = kaff ? meta(rkz, mi, m16) : 0.0f;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        x[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), sc, z);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int mi = 8 * P + e;
+                        x[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), meta(rks, mi, m16),
+                                  kaff ? meta(rkz, mi, m16) : 0.0f);
+                    }
+                }
+            } else if (row) {
+                const u32x4 rw = *(const u32x4*)(row + 8 * P);
+                const uint32_t w4[4] = {rw.x, rw.y, rw.z, rw.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    x[e] = f16_bits_to_f32((uint16_t)(w4[e >> 1] >> (16 * (e & 1))));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    x[e] = 0.0f;
+            }
+            half8 h, l;
+            split_half8(x, &h, &l);
+            const size_t off = (size_t)tau * 2 * D + 16 * (P ^ kswz<D>(tau));
+            *(u32x4*)(img + off) = __builtin_bit_cast(u32x4, h);
+            *(u32x4*)(img + 64 * D + off) = __builtin_bit_cast(u32x4, l);
+        }
+        // V piece: channel d, key-slot chunk q (keys 4 q .. 4 q + 3 and
+        // 16 + 4 q .. 16 + 4 q + 3)
+        {
+            const int d = pc % D, q = pc / D;
+            float x[8];
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int tk0 = 16 * half + 4 * q;  // first key of the half
+                Piece w = {0u, 0u};
+                const int o = tk0 / 8;  // raw octet holding keys tk0 .. tk0 + 3
+                if (!sinkblk && 32 * blk + tk0 < p.nq)
+                    w = piece<W8>(rvc, (d % 16 + 16 * o) * (D / 16) + d / 16, vbits);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int tk = tk0 + e;
+                    float val = 0.0f;
+                    if (sinkblk) {
+                        const int ts = 32 * v + tk;
+                        if (ts < p.n_sink)
+                            val = half_bits(p.vq, (sbase + ts) * D + d);
+                    } else {
+                        const int t = 32 * blk + tk;
+                        if (t < p.nq) {
+                            const int mi = (d / p.v_group) * 32 + tk;
+                            val = dq(p.v_mode, vbits, code_of(w, vbits, tk % 8), meta(rvs, mi, m16),
+                                     vaff ? meta(rvz, mi, m16) : 0.0f);
+                        } else if (t < p.n) {
+                            val = half_bits(p.vr, (rbase + t % p.ring) * D + d);
+                        }
+                    }
+                    x[4 * half + e] = val;
+                }
+            }
+            *(u32x4*)(img + 128 * D + 64 * d + 16 * (q ^ vswz(d))) = __builtin_bit_cast(u32x4, pack_half8(x));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 2. Attention over the block images.
+
+// 16 bytes per lane from global memory to LDS address lds_addr + 16 lane
+// (lds_addr wave-uniform, held in M0 while the copy issues).  Inline
+// assembly, so that the compiler does not make LDS reads wait for every
+// outstanding copy; the kernel's own vmcnt waits order them.
+__device__ __forceinline__ void copy16(uint64_t base, uint32_t voff, uint32_t lds_addr)
+{
+    const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" : : "s"(m0v), "v"(voff), "s"(base) : "memory");
+}
+
+// s_waitcnt vmcnt(n) for a wave-uniform n (expcnt and lgkmcnt not waited)
+__device__ __forceinline__ void wait_vm(int n)
+{
+    switch (n) {
+#define KVQ_WAIT_VM(k)                              \
+    case k:                                         \
+        __builtin_amdgcn_s_waitcnt(0x0F70 | (k)); \
+        break;
+        KVQ_WAIT_VM(1)
+        KVQ_WAIT_VM(2)
+        KVQ_WAIT_VM(3)
+        KVQ_WAIT_VM(4)
+        KVQ_WAIT_VM(5)
+        KVQ_WAIT_VM(6)
+        KVQ_WAIT_VM(7)
+        KVQ_WAIT_VM(8)
+        KVQ_WAIT_VM(9)
+        KVQ_WAIT_VM(10)
+        KVQ_WAIT_VM(11)
+        KVQ_WAIT_VM(12)
+#undef KVQ_WAIT_VM
+    default:
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+    }
+}
+
+// The copies of this wave that precede the newest `after` of its issued
+// copies have landed, then every wave is past the same point.
+__device__ __forceinline__ void ring_sync(int after)
+{
+    wait_vm(after);
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 {
     constexpr int QN = qn<D>(), RT = rows_per_tile<D>(), NKS = D / 32, NCT = D / 16;
-    constexpr int KP = D + 8, VP = 40;  // LDS pitches (fp16 units)
+    constexpr int BI = image_bytes<D>(), NST = stages<D>();
+    constexpr int WI = BI / 1024;  // 1 KiB wave copies per image
     extern __shared__ __attribute__((aligned(16))) uint8_t plds[];
-    uint16_t* kh = (uint16_t*)plds;
-    uint16_t* kl = kh + 32 * KP;
-    uint16_t* vh = kl + 32 * KP;
-    constexpr size_t kRawOff = lds_bytes<D, W8>() - raw_bytes<D, W8>();
-    uint8_t* raw = plds + kRawOff;
 
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int col = lane & 15, qg = lane >> 4;
-    const int unit = blockIdx.y, b = unit / p.H, h = unit % p.H;
+    // Tiles of one unit run on one XCD (workgroup w goes to XCD w mod 8), so
+    // that the unit's block images are read from that XCD's L2 by all of
+    // its tiles; the longest (newest) tiles start first.
+    const int NT = p.pf_tiles, W = gridDim.x;
+    const int L = (W & 7) == 0 ? (blockIdx.x & 7) * (W >> 3) + (blockIdx.x >> 3) : blockIdx.x;
+    const int uloc = L / NT, tile = NT - 1 - L % NT;
+    const int unit = p.pf_u0 + uloc, b = unit / p.H, h = unit % p.H;
     const int G = p.G, C = p.C;
     const int rows = C * G;
-    const int r0 = blockIdx.x * RT;
+    const int r0 = tile * RT;
     // Positions are tail indices (token minus sink); sink tokens sit at
     // -sink .. -1, so a chunk that starts in the sink has negative positions.
     const int first_pos = p.n - C;  // position of chunk token 0
@@ -218,23 +391,19 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
                 split_half8(v, &qh[c][ks], &ql[c][ks]);
             }
         }
-        __syncthreads();  // the K/V buffers overwrite the query rows
+        __syncthreads();  // the ring overwrites the query rows
     }
 
     // position of each of this lane's query columns (kNoRow: no such row,
     // every key masked)
     constexpr int kNoRow = -(1 << 30);
     int qpos[QN];
-    int newest;
 #pragma unroll
     for (int c = 0; c < QN; ++c) {
         const int R = r0 + 16 * (QN * wave + c) + col;
         qpos[c] = R < rows ? first_pos + R / G : kNoRow;
     }
-    {
-        const int Rlast = min(r0 + RT, rows) - 1;
-        newest = first_pos + Rlast / G;
-    }
+    const int newest = first_pos + (min(r0 + RT, rows) - 1) / G;
 
     floatx4 acc[QN][NCT];
     float m[QN], lsum[QN];
@@ -247,202 +416,42 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
             acc[c][t] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
-    const int NB = p.T >> 5;
-    const size_t ub0 = (size_t)unit * NB;
     const int nkb = newest >= 0 ? newest / 32 + 1 : 0;  // coded-tail blocks
     // sink blocks holding a token no later than the newest query
     const int nsb = min((p.n_sink + 31) >> 5, (newest + p.sink) / 32 + 1);
     const int sb0 = p.sink >> 5;  // sink block j is tail block j - sb0
-    const int kbits = W8 ? 8 : p.k_bits, vbits = W8 ? 8 : p.v_bits;
-    const bool kaff = p.k_mode == KVQ_AFFINE, vaff = p.v_mode == KVQ_AFFINE;
+    const int nvis = nsb + nkb;
 
-    // Byte ranges of one block's raw data, in the order they sit in LDS: Kc,
-    // Ks, Kz, Vc, Vs, Vz (Kz, Vz empty for symmetric codes).  Kept in scalars
-    // (selects, no indexed arrays) so nothing lands in scratch memory.
-    const int msz = p.meta16 ? 2 : 4;  // bytes per scale or offset
-    const int kmeta = p.k_axis == KVQ_PER_TOKEN ? (D / p.k_group) * 32 * msz : D * msz;
-    const int vmeta = (D / p.v_group) * 32 * msz;
-    const int len0 = 4 * D * kbits, len1 = kmeta, len2 = kaff ? kmeta : 0;
-    const int len3 = 4 * D * vbits, len4 = vmeta, len5 = vaff ? vmeta : 0;
-    const int st1 = len0, st2 = st1 + len1, st3 = st2 + len2, st4 = st3 + len3, st5 = st4 + len4;
-    const int st6 = st5 + len5;
-    // this thread's 16-byte units of a block's raw data
-    constexpr int UPT = (raw_bytes<D, W8>() / 16 + kThreads - 1) / kThreads;
-    u32x4 pre[UPT];
-    auto fetch_raw = [&](int blk) {
-        const size_t ibf = ub0 + blk;
+    // This wave's copies of an image: wave copies wave, wave + 8, ... < WI.
+    const int cw = (WI - wave + 7) / 8;
+    const uint32_t lbase = (uint32_t)(uintptr_t)plds;
+    const uint8_t* ws_unit = p.pf_ws + (size_t)uloc * p.pf_nvb * BI;
+    auto issue = [&](int it) {
+        const int vs = it < nsb ? it : p.pf_nsb + (it - nsb);  // workspace block
+        const uint64_t base = (uint64_t)(ws_unit + (size_t)vs * BI);
+        const uint32_t at = lbase + (uint32_t)((it % NST) * BI);
 #pragma unroll
-        for (int k = 0; k < UPT; ++k) {
-            const int off = 16 * ((int)threadIdx.x + kThreads * k);
-            pre[k] = u32x4{0u, 0u, 0u, 0u};
-            if (off < st6) {
-                const uint8_t* src;
-                if (off < st1)
-                    src = (const uint8_t*)p.kc + ibf * len0 + off;
-                else if (off < st2)
-                    src = (const uint8_t*)p.ks + ibf * len1 + (off - st1);
-                else if (off < st3)
-                    src = (const uint8_t*)p.kz + ibf * len2 + (off - st2);
-                else if (off < st4)
-                    src = (const uint8_t*)p.vc + ibf * len3 + (off - st3);
-                else if (off < st5)
-                    src = (const uint8_t*)p.vs + ibf * len4 + (off - st4);
-                else
-                    src = (const uint8_t*)p.vz + ibf * len5 + (off - st5);
-                pre[k] = *(const u32x4*)src;
-            }
+        for (int i = 0; i < (WI + 7) / 8; ++i) {
+            const int k = wave + 8 * i;
+            if (k < WI)
+                copy16(base, (uint32_t)(1024 * k + 16 * lane), at + 1024 * k);
         }
     };
-    auto store_raw = [&]() {
-#pragma unroll
-        for (int k = 0; k < UPT; ++k) {
-            const int off = 16 * ((int)threadIdx.x + kThreads * k);
-            if (off < st6)
-                *(u32x4*)(raw + off) = pre[k];
-        }
-    };
-    const uint8_t* rkc = raw;
-    const uint8_t* rks = raw + st1;
-    const uint8_t* rkz = raw + st2;
-    const uint8_t* rvc = raw + st3;
-    const uint8_t* rvs = raw + st4;
-    const uint8_t* rvz = raw + st5;
-    const bool m16 = p.meta16 != 0;
 
-    if (nkb > 0) {
-        fetch_raw(0);
-        store_raw();
-    }
-    __syncthreads();
-    for (int it = 0; it < nsb + nkb; ++it) {
+    uint32_t m0_saved;
+    asm volatile("s_mov_b32 %0, m0" : "=s"(m0_saved));
+    // prologue: images 0 .. NST - 2 in flight, image 0 landed
+    for (int it = 0; it < NST - 1 && it < nvis; ++it)
+        issue(it);
+    ring_sync(NST - 1 <= nvis ? cw * (NST - 2) : 0);
+
+    for (int it = 0; it < nvis; ++it) {
         const int blk = it < nsb ? it - sb0 : it - nsb;
-        if (blk >= 0 && blk + 1 < nkb)
-            fetch_raw(blk + 1);  // lands while this block is computed
-        if (blk < 0) {
-            // ---- a sink block: fp16 rows, tokens past n_sink zero
-            const size_t sbase = (size_t)unit * p.sink;
-            for (int pc = threadIdx.x; pc < 4 * D; pc += kThreads) {
-                {
-                    const int tau = pc / (D / 8), P = pc % (D / 8);
-                    const int t = p.sink + 32 * blk + tau;
-                    float v[8];
-                    if (t < p.n_sink) {
-                        const u32x4 rw = *(const u32x4*)(p.kq + (sbase + t) * D + 8 * P);
-                        const uint32_t w4[4] = {rw.x, rw.y, rw.z, rw.w};
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            v[e] = f16_bits_to_f32((uint16_t)(w4[e >> 1] >> (16 * (e & 1))));
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            v[e] = 0.0f;
-                    }
-                    split8(v, kh + tau * KP + 8 * P, kl + tau * KP + 8 * P);
-                }
-                {
-                    const int o = pc / D, d = pc % D;
-                    const int t0 = p.sink + 32 * blk + 8 * o;
-                    uint16_t hv[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        hv[e] = t0 + e < p.n_sink ? p.vq[(sbase + t0 + e) * D + d] : (uint16_t)0;
-                    *(u32x4*)(vh + d * VP + 8 * o) =
-                        u32x4{hv[0] | ((uint32_t)hv[1] << 16), hv[2] | ((uint32_t)hv[3] << 16),
-                              hv[4] | ((uint32_t)hv[5] << 16), hv[6] | ((uint32_t)hv[7] << 16)};
-                }
-            }
-        } else {
-        // ---- reconstruct the block into LDS: 4 D pieces of K and of V
-        for (int pc = threadIdx.x; pc < 4 * D; pc += kThreads) {
-            // K piece: token tau = pc / (D / 8), channels 8 P .. 8 P + 7
-            {
-                const int tau = pc / (D / 8), P = pc % (D / 8);
-                const int t = 32 * blk + tau;
-                float v[8];
-                if (t < p.nq) {
-                    const int row = 4 * (tau / 8) + tau % 4, half = (tau / 4) % 2;
-                    const int idx = (half * 64 + row + 16 * (P % 4)) * (D / 32) + P / 4;
-                    const Piece w = piece<W8>(rkc, idx, kbits);
-                    if (p.k_axis == KVQ_PER_TOKEN) {
-                        const int mi = ((8 * P) / p.k_group) * 32 + tau;
-                        const float sc = meta(rks, mi, m16), z = kaff ? meta(rkz, mi, m16) : 0.0f;
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            v[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), sc, z);
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const int mi = 8 * P + e;
-                            v[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), meta(rks, mi, m16),
-                                      kaff ? meta(rkz, mi, m16) : 0.0f);
-                        }
-                    }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e)
-                        v[e] = 0.0f;
-                }
-                split8(v, kh + tau * KP + 8 * P, kl + tau * KP + 8 * P);
-            }
-            // V piece: octet o = pc / D (tokens 8 o .. 8 o + 7), channel d
-            {
-                const int o = pc / D, d = pc % D;
-                float v[8];
-                const int t0 = 32 * blk + 8 * o;
-                const int idx = (d % 16 + 16 * o) * (D / 16) + d / 16;
-                const Piece w = t0 < p.nq ? piece<W8>(rvc, idx, vbits) : Piece{0u, 0u};
-                // the octet's eight scales (and offsets) are consecutive
-                const int mi = (d / p.v_group) * 32 + 8 * o;
-                float sv[8], zv[8];
-                meta8(rvs, mi, m16, sv);
-                if (vaff)
-                    meta8(rvz, mi, m16, zv);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float sc = sv[e], z = vaff ? zv[e] : 0.0f;
-                    v[e] = t0 + e < p.nq ? dq(p.v_mode, vbits, code_of(w, vbits, e), sc, z) : 0.0f;
-                }
-                *(u32x4*)(vh + d * VP + 8 * o) = __builtin_bit_cast(u32x4, pack_half8(v));
-            }
-        }
-        // tokens of the fp16 window (past the coded ones): the same pieces,
-        // from the ring in global memory, in a pass of their own so that
-        // the coded pass never waits on global loads
-        if (32 * blk + 31 >= p.nq && 32 * blk < p.n) {
-            for (int pc = threadIdx.x; pc < 4 * D; pc += kThreads) {
-                {
-                    const int tau = pc / (D / 8), P = pc % (D / 8);
-                    const int t = 32 * blk + tau;
-                    if (t >= p.nq && t < p.n) {
-                        const u32x4 rw = *(const u32x4*)(p.kr + (((size_t)unit * p.ring) + t % p.ring) * D + 8 * P);
-                        const uint32_t w4[4] = {rw.x, rw.y, rw.z, rw.w};
-                        float v[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e)
-                            v[e] = f16_bits_to_f32((uint16_t)(w4[e >> 1] >> (16 * (e & 1))));
-                        split8(v, kh + tau * KP + 8 * P, kl + tau * KP + 8 * P);
-                    }
-                }
-                {
-                    const int o = pc / D, d = pc % D;
-                    const int t0 = 32 * blk + 8 * o;
-                    if (t0 + 7 >= p.nq && t0 < p.n) {
-                        uint16_t hv[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const int t = t0 + e;
-                            hv[e] = (t >= p.nq && t < p.n) ? p.vr[(((size_t)unit * p.ring) + t % p.ring) * D + d]
-                                                           : vh[d * VP + 8 * o + e];
-                        }
-                        *(u32x4*)(vh + d * VP + 8 * o) =
-                            u32x4{hv[0] | ((uint32_t)hv[1] << 16), hv[2] | ((uint32_t)hv[3] << 16),
-                                  hv[4] | ((uint32_t)hv[5] << 16), hv[6] | ((uint32_t)hv[7] << 16)};
-                    }
-                }
-            }
-        }
-        }  // coded-tail block
-        __syncthreads();
+        if (it + NST - 1 < nvis)
+            issue(it + NST - 1);  // into the stage image it - 1 used
+        const uint8_t* kh = plds + (it % NST) * BI;
+        const uint8_t* kl = kh + 64 * D;
+        const uint8_t* vt = kh + 128 * D;
 
         // ---- scores S^T (keys x query rows), two 16-key tiles
         floatx4 s[QN][2];
@@ -451,9 +460,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
             s[c][0] = s[c][1] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
+            const int row = 16 * kt + col;
 #pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
-                const int off = (16 * kt + col) * KP + 32 * ks + 8 * qg;
+                const int off = row * 2 * D + 16 * ((4 * ks + qg) ^ kswz<D>(row));
                 const half8 ah = __builtin_bit_cast(half8, *(const u32x4*)(kh + off));
                 const half8 al = __builtin_bit_cast(half8, *(const u32x4*)(kl + off));
 #pragma unroll
@@ -505,17 +515,16 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
 #pragma unroll
         for (int t = 0; t < NCT; ++t) {
             const int d = 16 * t + col;
-            const uint2 h0 = *(const uint2*)(vh + d * VP + 4 * qg);
-            const uint2 h1 = *(const uint2*)(vh + d * VP + 16 + 4 * qg);
-            const half8 ah = __builtin_bit_cast(half8, u32x4{h0.x, h0.y, h1.x, h1.y});
+            const half8 av = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
 #pragma unroll
             for (int c = 0; c < QN; ++c)
-                acc[c][t] = mfma16(ah, ph[c], acc[c][t]);
+                acc[c][t] = mfma16(av, ph[c], acc[c][t]);
         }
-        if (blk >= 0 && blk + 1 < nkb)
-            store_raw();  // the raw block was consumed before the barrier above
-        __syncthreads();  // the next block overwrites K, V and the raw copy
+        // image it + 1 has landed (all of this wave's copies but those of
+        // the images after it), and no wave reads stage it any more
+        ring_sync(it + NST - 1 < nvis ? cw * (NST - 2) : 0);
     }
+    asm volatile("s_mov_b32 m0, %0" ::"s"(m0_saved));
 
     // ---- normalize and write: lane holds O[row][16 t + 4 qg + i]
     float inv[QN];
@@ -560,28 +569,44 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(AttnParams p)
 }
 
 template <int D>
-hipError_t launch(const AttnParams& p, hipStream_t stream)
+hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
 {
     constexpr int RT = rows_per_tile<D>();
-    const dim3 grid((p.C * p.G + RT - 1) / RT, p.B * p.H);
-    const bool w8 = p.k_bits == 8;  // 8-bit codes come as K and V both 8-bit
-    void (*kern)(AttnParams) = w8 ? prefill_kernel<D, true> : prefill_kernel<D, false>;
-    const size_t lds = w8 ? lds_bytes<D, true>() : lds_bytes<D, false>();
-    launch_kernel(kern, grid, dim3(kThreads), lds, stream, p);
+    const int units = p0.B * p0.H;
+    const size_t per_unit = (size_t)p0.pf_nvb * image_bytes<D>();
+    const int group = (int)(ws_bytes / per_unit < (size_t)units ? ws_bytes / per_unit : (size_t)units);
+    if (group < 1)
+        return hipErrorInvalidValue;
+    const int tiles = (p0.C * p0.G + RT - 1) / RT;
+    const bool w8 = p0.k_bits == 8;  // 8-bit codes come as K and V both 8-bit
+    void (*deq)(AttnParams) = w8 ? dequant_kernel<D, true> : dequant_kernel<D, false>;
+    for (int u0 = 0; u0 < units; u0 += group) {
+        AttnParams p = p0;
+        p.pf_u0 = u0;
+        p.pf_tiles = tiles;
+        const int nu = units - u0 < group ? units - u0 : group;
+        launch_kernel(deq, dim3(p.pf_nvb, nu), dim3(kDqThreads), 0, stream, p);
+        launch_kernel(attn_kernel<D>, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(), stream, p);
+    }
     return hipGetLastError();
 }
 
 }  // namespace pre
 
-hipError_t launch_prefill(const AttnParams& p, int D, hipStream_t stream)
+size_t prefill_image_bytes(int D)
+{
+    return (size_t)192 * D;
+}
+
+hipError_t launch_prefill(const AttnParams& p, int D, size_t ws_bytes, hipStream_t stream)
 {
     switch (D) {
     case 64:
-        return pre::launch<64>(p, stream);
+        return pre::launch<64>(p, ws_bytes, stream);
     case 128:
-        return pre::launch<128>(p, stream);
+        return pre::launch<128>(p, ws_bytes, stream);
     case 256:
-        return pre::launch<256>(p, stream);
+        return pre::launch<256>(p, ws_bytes, stream);
     default:
         return hipErrorInvalidValue;
     }

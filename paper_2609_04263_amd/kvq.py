@@ -65,12 +65,14 @@ def _load() -> C.CDLL:
     L.kvq_decode_workspace_bytes.argtypes = [P, I, C.POINTER(S)]
     L.kvq_decode_attn.argtypes = [P, P, I, C.c_float, P, P, S, P]
     L.kvq_decode_attn_noalloc.argtypes = [P, P, I, C.c_float, P, P]
-    L.kvq_prefill_attn.argtypes = [P, P, I, I, C.c_float, P, P]
+    L.kvq_prefill_attn.argtypes = [P, P, I, I, C.c_float, P, P, S, P]
+    L.kvq_prefill_workspace_bytes.argtypes = [P, C.POINTER(S)]
     L.kvq_time_launches.argtypes = [P, P]
     for name in ("kvq_cache_bytes", "kvq_cache_init", "kvq_cache_section", "kvq_cache_reset",
                  "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_project_workspace_bytes",
                  "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
                  "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn",
+                 "kvq_prefill_workspace_bytes",
                  "kvq_time_launches"):
         getattr(L, name).restype = I
     return L
@@ -81,7 +83,7 @@ EXPORTED = ("kvq_strerror", "kvq_cache_bytes", "kvq_cache_init", "kvq_cache_sect
             "kvq_cache_reset", "kvq_cache_len", "kvq_cache_rewind", "kvq_cache_restore", "kvq_cache_destroy",
             "kvq_project_workspace_bytes", "kvq_project_qkv", "kvq_project_append", "kvq_merge_adapter", "kvq_append",
             "kvq_decode_workspace_bytes", "kvq_decode_attn", "kvq_decode_attn_noalloc", "kvq_prefill_attn",
-            "kvq_time_launches")
+            "kvq_prefill_workspace_bytes", "kvq_time_launches")
 
 
 def lib() -> C.CDLL:
@@ -205,11 +207,21 @@ class Cache:
         if st:
             _check(st, "decode_attn_noalloc")
 
-    def prefill_attn(self, Q, C_len: int, H_q: int, sm_scale: float, O, stream=None) -> None:
+    def prefill_workspace_bytes(self) -> int:
+        out = C.c_size_t()
+        _check(_lib.kvq_prefill_workspace_bytes(self.handle, C.byref(out)), "prefill_workspace_bytes")
+        return out.value
+
+    def prefill_workspace(self, device="cuda"):
+        """A workspace for prefill_attn at the cache's current length."""
+        return torch.empty(self.prefill_workspace_bytes(), dtype=torch.uint8, device=device)
+
+    def prefill_attn(self, Q, C_len: int, H_q: int, sm_scale: float, O, workspace, stream=None) -> None:
         """O[B, C, H_q, D] (fp32) <- causal attention of the newest C_len tokens'
         bf16 queries Q[B, C, H_q, D] over the cache."""
+        nbytes = workspace.numel() * workspace.element_size()
         st = _lib.kvq_prefill_attn(self.handle, Q.data_ptr(), C_len, H_q, sm_scale, O.data_ptr(),
-                                   _stream(stream))
+                                   workspace.data_ptr(), nbytes, _stream(stream))
         if st:
             _check(st, "prefill_attn")
 

@@ -201,6 +201,6 @@ def test_storage_contents_at_init_do_not_matter(name):
     C = 45
     Qc = synth.normal_bf16(101, "qc", (B, C, H_q, D))
     Oc = torch.empty((B, C, H_q, D), dtype=torch.float32, device="cuda")
-    gc.prefill_attn(dev_bf16(Qc), C, H_q, sm, Oc)
+    gc.prefill_attn(dev_bf16(Qc), C, H_q, sm, Oc, gc.prefill_workspace())
     torch.cuda.synchronize()
     assert_close(Oc.cpu().numpy(), ref.prefill_attn(Qc, sm), what=f"{name} NaN-filled storage prefill")

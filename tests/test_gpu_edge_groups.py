@@ -181,6 +181,6 @@ def test_edge_groups_append_decode_prefill(name):
     C = 100
     Qc = synth.normal_bf16(3001 + D, "qc", (B, C, H_q, D))
     Oc = torch.empty((B, C, H_q, D), dtype=torch.float32, device="cuda")
-    gc.prefill_attn(dev_bf16(Qc), C, H_q, sm, Oc)
+    gc.prefill_attn(dev_bf16(Qc), C, H_q, sm, Oc, gc.prefill_workspace())
     torch.cuda.synchronize()
     assert_close(Oc.cpu().numpy(), ref.prefill_attn(Qc, sm), what=f"{name} prefill")

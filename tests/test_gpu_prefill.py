@@ -7,8 +7,11 @@ fp64 causal attention over the reconstruction: |gpu - ref| <= 2e-3 +
 1e-2 |ref| elementwise.  Cases cover every cache format of the decode tests
 (fp16 windows, per-channel keys, rotation, head sizes 64/128/256), chunks of
 one token, chunks not aligned to the 32-token blocks, chunks that are the
-whole cache, grouped-query sizes that leave ragged query tiles, and a
-workload-shaped chunk.
+whole cache, grouped-query sizes that leave ragged query tiles, a
+workload-shaped chunk, and workspaces that hold only some of the (sequence,
+KV head) units (the call then runs the units in groups; outputs must not
+change by a bit).  Workspaces start filled with 0xFF bytes (fp16 NaN), so an
+image byte the reconstruction failed to write shows up in the output.
 """
 import numpy as np
 import pytest
@@ -23,7 +26,7 @@ from test_gpu_append import CASES
 pytestmark = pytest.mark.gpu
 
 
-def run(name, B, H, G, n, C, seed, sm=None):
+def run(name, B, H, G, n, C, seed, sm=None, ws_units=None):
     from paper_2609_04263_amd import kvq
     fmt, D = CASES[name]
     outlier = ("student_t", 3.0) if fmt["rotate"] else ("scale", 4, 20.0)
@@ -40,10 +43,15 @@ def run(name, B, H, G, n, C, seed, sm=None):
     Q = synth.normal_bf16(seed, ("chunk-q",), (B, C, H_q, D))
     sm = 1.0 / np.sqrt(D) if sm is None else sm
     O = torch.full((B, C, H_q, D), float("nan"), dtype=torch.float32, device="cuda")
-    gc.prefill_attn(dev_bf16(Q), C, H_q, sm, O)
+    full = gc.prefill_workspace_bytes()
+    assert full % (B * H) == 0
+    nbytes = full if ws_units is None else ws_units * (full // (B * H))
+    ws = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+    gc.prefill_attn(dev_bf16(Q), C, H_q, sm, O, ws)
     torch.cuda.synchronize()
     ref_o = ref.prefill_attn(Q, sm)
-    return assert_close(O.cpu().numpy(), ref_o, what=f"{name} n={n} C={C} G={G}")
+    assert_close(O.cpu().numpy(), ref_o, what=f"{name} n={n} C={C} G={G} ws_units={ws_units}")
+    return O.cpu().numpy()
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -66,3 +74,25 @@ def test_prefill_peaked_and_flat_softmax():
 def test_prefill_workload_shape_chunk():
     # a 256-token chunk at the end of 1280 tokens, D = 256, G = 2 (the 12B layer's shape)
     run("gqa12b", B=1, H=2, G=2, n=1280, C=256, seed=130)
+
+
+@pytest.mark.parametrize("name", ["tiny_b16", "kivi", "kvarn_sink"])
+def test_prefill_workspace_groups(name):
+    # B H = 6 units: one pass, groups of 4 + 2, and one unit at a time
+    outs = [run(name, B=3, H=2, G=2, n=170, C=60, seed=140, ws_units=u) for u in (None, 4, 1)]
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
+
+
+def test_prefill_workspace_too_small():
+    from paper_2609_04263_amd import kvq
+    fmt, D = CASES["tiny_b16"]
+    B, H, n = 2, 2, 64
+    K, V = synth.kv_tokens(150, B, n, H, D)
+    gc = kvq.Cache(fmt, B, H, D, n)
+    gc.append(dev_bf16(K), dev_bf16(V))
+    Q = dev_bf16(synth.normal_bf16(151, ("chunk-q",), (B, 8, 2 * H, D)))
+    O = torch.empty((B, 8, 2 * H, D), dtype=torch.float32, device="cuda")
+    share = gc.prefill_workspace_bytes() // (B * H)
+    with pytest.raises(kvq.KvqError) as e:
+        gc.prefill_attn(Q, 8, 2 * H, 0.125, O, torch.empty(share - 16, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == kvq.ERR_WORKSPACE

@@ -127,17 +127,32 @@ def test_prefill_argument_checks(kvq):
     f = configs.make_format()
     c = kvq.Cache(f, 2, 2, 64, 64, storage=FakeStorage(kvq.cache_bytes(f, 2, 2, 64, 64)))
     q = FakeStorage(0, FAKE)
+    ws = FakeStorage(1 << 20)
     # empty cache: no chunk can be attended
     with pytest.raises(kvq.KvqError) as e:
-        c.prefill_attn(q, 1, 4, 0.125, q, stream=0)
+        c.prefill_attn(q, 1, 4, 0.125, q, ws, stream=0)
     assert e.value.status == kvq.ERR_ARG
+    assert c.prefill_workspace_bytes() == 0
+    c.restore(40)  # two 32-token blocks per (b, h) unit
+    # workspace: one 192 D-byte image per visible block and unit
+    full = c.prefill_workspace_bytes()
+    assert full == 2 * 2 * 2 * 192 * 64
     # misaligned output, bad head grouping
     with pytest.raises(kvq.KvqError) as e:
-        c.prefill_attn(q, 1, 4, 0.125, FakeStorage(0, FAKE + 4), stream=0)
+        c.prefill_attn(q, 1, 4, 0.125, FakeStorage(0, FAKE + 4), ws, stream=0)
     assert e.value.status == kvq.ERR_ARG
     with pytest.raises(kvq.KvqError) as e:
-        c.prefill_attn(q, 1, 3, 0.125, q, stream=0)
+        c.prefill_attn(q, 1, 3, 0.125, q, ws, stream=0)
     assert e.value.status == kvq.ERR_ARG
+    # chunk longer than the cache
+    with pytest.raises(kvq.KvqError) as e:
+        c.prefill_attn(q, 41, 4, 0.125, q, ws, stream=0)
+    assert e.value.status == kvq.ERR_ARG
+    # workspace below one unit's share, misaligned or missing
+    for bad in (FakeStorage(full // 4 - 16), FakeStorage(full, FAKE + 8), FakeStorage(full, 0)):
+        with pytest.raises(kvq.KvqError) as e:
+            c.prefill_attn(q, 1, 4, 0.125, q, bad, stream=0)
+        assert e.value.status == kvq.ERR_WORKSPACE
 
 
 def test_project_append_argument_checks(kvq):
