@@ -135,6 +135,23 @@ __device__ __forceinline__ uint32_t code_of(const Piece& w, int bits, int e)
     return (x >> ((bits * e) & 31)) & ((1u << bits) - 1u);
 }
 
+// four consecutive scales or offsets from element i (a multiple of 4)
+__device__ __forceinline__ void meta4(const uint8_t* sec, int i, bool m16, float* v)
+{
+    if (m16) {
+        const uint2 h = *(const uint2*)(sec + 2 * i);
+        v[0] = f16_bits_to_f32((uint16_t)h.x);
+        v[1] = f16_bits_to_f32((uint16_t)(h.x >> 16));
+        v[2] = f16_bits_to_f32((uint16_t)h.y);
+        v[3] = f16_bits_to_f32((uint16_t)(h.y >> 16));
+    } else {
+        const floatx4 a = *(const floatx4*)(sec + 4 * i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = a[e];
+    }
+}
+
 __device__ __forceinline__ float half_bits(const uint16_t* row, size_t i)
 {
     return f16_bits_to_f32(row[i]);
@@ -246,36 +263,47 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
             *(u32x4*)(img + 64 * D + off) = __builtin_bit_cast(u32x4, l);
         }
         // V piece: channel d, key-slot chunk q (keys 4 q .. 4 q + 3 and
-        // 16 + 4 q .. 16 + 4 q + 3)
+        // 16 + 4 q .. 16 + 4 q + 3); the four chunks of a row go to four
+        // neighbouring lanes, so a wave's stores cover 1 KiB contiguously
         {
-            const int d = pc % D, q = pc / D;
+            const int d = pc >> 2, q = pc & 3;
             float x[8];
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
                 const int tk0 = 16 * half + 4 * q;  // first key of the half
-                Piece w = {0u, 0u};
-                const int o = tk0 / 8;  // raw octet holding keys tk0 .. tk0 + 3
-                if (!sinkblk && 32 * blk + tk0 < p.nq)
-                    w = piece<W8>(rvc, (d % 16 + 16 * o) * (D / 16) + d / 16, vbits);
+                if (!sinkblk && 32 * blk + tk0 < p.nq) {
+                    // raw octet tk0 / 8 holds keys tk0 .. tk0 + 3 as its codes
+                    // 4 (q & 1) .. + 3; their four scales (and offsets) are
+                    // consecutive
+                    const Piece w = piece<W8>(rvc, (d % 16 + 16 * (tk0 / 8)) * (D / 16) + d / 16, vbits);
+                    const int mi = (d / p.v_group) * 32 + tk0;
+                    float sc[4], zc[4] = {0.f, 0.f, 0.f, 0.f};
+                    meta4(rvs, mi, m16, sc);
+                    if (vaff)
+                        meta4(rvz, mi, m16, zc);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int tk = tk0 + e;
-                    float val = 0.0f;
-                    if (sinkblk) {
-                        const int ts = 32 * v + tk;
-                        if (ts < p.n_sink)
-                            val = half_bits(p.vq, (sbase + ts) * D + d);
-                    } else {
-                        const int t = 32 * blk + tk;
-                        if (t < p.nq) {
-                            const int mi = (d / p.v_group) * 32 + tk;
-                            val = dq(p.v_mode, vbits, code_of(w, vbits, tk % 8), meta(rvs, mi, m16),
-                                     vaff ? meta(rvz, mi, m16) : 0.0f);
-                        } else if (t < p.n) {
-                            val = half_bits(p.vr, (rbase + t % p.ring) * D + d);
-                        }
+                    for (int e = 0; e < 4; ++e) {
+                        const int t = 32 * blk + tk0 + e;
+                        x[4 * half + e] = t < p.nq ? dq(p.v_mode, vbits, code_of(w, vbits, 4 * (q & 1) + e), sc[e], zc[e])
+                                        : t < p.n  ? half_bits(p.vr, (rbase + t % p.ring) * D + d)
+                                                   : 0.0f;
                     }
-                    x[4 * half + e] = val;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int tk = tk0 + e;
+                        float val = 0.0f;
+                        if (sinkblk) {
+                            const int ts = 32 * v + tk;
+                            if (ts < p.n_sink)
+                                val = half_bits(p.vq, (sbase + ts) * D + d);
+                        } else {
+                            const int t = 32 * blk + tk;
+                            if (t < p.n)
+                                val = half_bits(p.vr, (rbase + t % p.ring) * D + d);
+                        }
+                        x[4 * half + e] = val;
+                    }
                 }
             }
             *(u32x4*)(img + 128 * D + 64 * d + 16 * (q ^ vswz(d))) = __builtin_bit_cast(u32x4, pack_half8(x));
@@ -447,25 +475,48 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 
     for (int it = 0; it < nvis; ++it) {
         const int blk = it < nsb ? it - sb0 : it - nsb;
-        if (it + NST - 1 < nvis)
-            issue(it + NST - 1);  // into the stage image it - 1 used
         const uint8_t* kh = plds + (it % NST) * BI;
         const uint8_t* kl = kh + 64 * D;
         const uint8_t* vt = kh + 128 * D;
+        // copies of image it + NST - 1 (into the stage image it - 1 used),
+        // one per score step so that the wave never waits on a burst of them
+        const bool more = it + NST - 1 < nvis;
+        int nvs = 0;
+        uint64_t cbase = 0;
+        uint32_t cat = 0;
+        if (more) {
+            nvs = it + NST - 1;
+            const int vs = nvs < nsb ? nvs : p.pf_nsb + (nvs - nsb);
+            cbase = (uint64_t)(ws_unit + (size_t)vs * BI);
+            cat = lbase + (uint32_t)((nvs % NST) * BI);
+        }
 
-        // ---- scores S^T (keys x query rows), two 16-key tiles
+        // ---- scores S^T (keys x query rows), two 16-key tiles; the next
+        // step's K fragments are read while this step's MFMAs run
         floatx4 s[QN][2];
 #pragma unroll
         for (int c = 0; c < QN; ++c)
             s[c][0] = s[c][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+        half8 fa[2][2][2];  // [buffer][kt][hi, lo]
+        auto kread = [&](int ks, half8 (&f)[2][2]) {
 #pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-            const int row = 16 * kt + col;
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
+            for (int kt = 0; kt < 2; ++kt) {
+                const int row = 16 * kt + col;
                 const int off = row * 2 * D + 16 * ((4 * ks + qg) ^ kswz<D>(row));
-                const half8 ah = __builtin_bit_cast(half8, *(const u32x4*)(kh + off));
-                const half8 al = __builtin_bit_cast(half8, *(const u32x4*)(kl + off));
+                f[kt][0] = __builtin_bit_cast(half8, *(const u32x4*)(kh + off));
+                f[kt][1] = __builtin_bit_cast(half8, *(const u32x4*)(kl + off));
+            }
+        };
+        kread(0, fa[0]);
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            if (ks + 1 < NKS)
+                kread(ks + 1, fa[(ks + 1) & 1]);
+            if (ks < (WI + 7) / 8 && more && wave + 8 * ks < WI)
+                copy16(cbase, (uint32_t)(1024 * (wave + 8 * ks) + 16 * lane), cat + 1024 * (wave + 8 * ks));
+#pragma unroll
+            for (int kt = 0; kt < 2; ++kt) {
+                const half8 ah = fa[ks & 1][kt][0], al = fa[ks & 1][kt][1];
 #pragma unroll
                 for (int c = 0; c < QN; ++c) {
                     s[c][kt] = mfma16(ah, qh[c][ks], s[c][kt]);
@@ -473,6 +524,20 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
                     s[c][kt] = mfma16(al, qh[c][ks], s[c][kt]);
                 }
             }
+        }
+        // copies left over when an image needs more than NKS per wave
+#pragma unroll
+        for (int i = NKS; i < (WI + 7) / 8; ++i)
+            if (more && wave + 8 * i < WI)
+                copy16(cbase, (uint32_t)(1024 * (wave + 8 * i) + 16 * lane), cat + 1024 * (wave + 8 * i));
+
+        // the first value fragments, read while the softmax runs
+        constexpr int NVP = NCT < 4 ? NCT : 4;
+        half8 vf[NVP];
+#pragma unroll
+        for (int t = 0; t < NVP; ++t) {
+            const int d = 16 * t + col;
+            vf[t] = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
         }
 
         // ---- online softmax per query column; P^T operands
@@ -511,11 +576,15 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
             ph[c] = pack_half8(pv);
         }
 
-        // ---- O^T += V^T P^T, 16 channels per tile, keys in the slot order above
+        // ---- O^T += V^T P^T, 16 channels per tile, keys in the slot order
+        // above; fragment t + NVP is read while tile t's MFMAs run
 #pragma unroll
         for (int t = 0; t < NCT; ++t) {
-            const int d = 16 * t + col;
-            const half8 av = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
+            const half8 av = vf[t % NVP];
+            if (t + NVP < NCT) {
+                const int d = 16 * (t + NVP) + col;
+                vf[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
+            }
 #pragma unroll
             for (int c = 0; c < QN; ++c)
                 acc[c][t] = mfma16(av, ph[c], acc[c][t]);
