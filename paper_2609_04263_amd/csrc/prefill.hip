@@ -432,6 +432,10 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         qpos[c] = R < rows ? first_pos + R / G : kNoRow;
     }
     const int newest = first_pos + (min(r0 + RT, rows) - 1) / G;
+    // position of the wave's oldest query when every row of the wave exists
+    // (rows are token-major): blocks wholly before it need no causal mask
+    const int wrow0 = r0 + 16 * QN * wave;
+    const int wave_first = wrow0 + 16 * QN <= rows ? first_pos + wrow0 / G : kNoRow;
 
     floatx4 acc[QN][NCT];
     float m[QN], lsum[QN];
@@ -473,23 +477,25 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         issue(it);
     ring_sync(NST - 1 <= nvis ? cw * (NST - 2) : 0);
 
+    int stg = 0;  // stage of image it (it mod NST)
     for (int it = 0; it < nvis; ++it) {
         const int blk = it < nsb ? it - sb0 : it - nsb;
-        const uint8_t* kh = plds + (it % NST) * BI;
+        const uint8_t* kh = plds + stg * BI;
         const uint8_t* kl = kh + 64 * D;
         const uint8_t* vt = kh + 128 * D;
         // copies of image it + NST - 1 (into the stage image it - 1 used),
         // one per score step so that the wave never waits on a burst of them
         const bool more = it + NST - 1 < nvis;
-        int nvs = 0;
+        const int pstg = stg == 0 ? NST - 1 : stg - 1;
         uint64_t cbase = 0;
         uint32_t cat = 0;
         if (more) {
-            nvs = it + NST - 1;
+            const int nvs = it + NST - 1;
             const int vs = nvs < nsb ? nvs : p.pf_nsb + (nvs - nsb);
             cbase = (uint64_t)(ws_unit + (size_t)vs * BI);
-            cat = lbase + (uint32_t)((nvs % NST) * BI);
+            cat = lbase + (uint32_t)(pstg * BI);
         }
+        stg = stg + 1 == NST ? 0 : stg + 1;
 
         // ---- scores S^T (keys x query rows), two 16-key tiles; the next
         // step's K fragments are read while this step's MFMAs run
@@ -541,35 +547,51 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         }
 
         // ---- online softmax per query column; P^T operands
-        half8 ph[QN];
+        // The running maximum of a column is raised only when the block's
+        // maximum exceeds it by more than 8 (log2 units): probabilities stay
+        // below 2^8, and the accumulators are rescaled a few times per row,
+        // not per block.  The column maximum needs the column's four lanes;
+        // it is gathered only when some lane of the wave holds a score
+        // beyond its running maximum + 8 (otherwise no column is raised).
+        const bool nomask = 32 * blk + 31 <= wave_first;  // wave-uniform
+        float x[QN][8], lm[QN];
+        bool up = false;
 #pragma unroll
         for (int c = 0; c < QN; ++c) {
-            float x[8];
-            float bm = -INFINITY;
+            lm[c] = -INFINITY;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int key = 32 * blk + (e < 4 ? 4 * qg + e : 16 + 4 * qg + e - 4);
-                x[e] = key <= qpos[c] ? s[c][e >> 2][e & 3] : -INFINITY;
-                bm = fmaxf(bm, x[e]);
+                x[c][e] = nomask || key <= qpos[c] ? s[c][e >> 2][e & 3] : -INFINITY;
+                lm[c] = fmaxf(lm[c], x[c][e]);
             }
-            bm = xor_max16_32(bm);
-            // the running maximum is raised only when a block exceeds it by
-            // more than 8 (log2 units): probabilities stay below 2^8, and the
-            // accumulators are rescaled a few times per row, not per block
-            if (bm > m[c] + 8.0f) {
-                const float alpha = m[c] == -INFINITY ? 0.0f : fast_exp2(m[c] - bm);
-                m[c] = bm;
-                lsum[c] *= alpha;
+            up = up || lm[c] > m[c] + 8.0f;
+        }
+        if (__any(up)) {
 #pragma unroll
-                for (int t = 0; t < NCT; ++t)
-                    acc[c][t] *= alpha;
+            for (int c = 0; c < QN; ++c) {
+                const float bm = xor_max16_32(lm[c]);
+                if (bm > m[c] + 8.0f) {
+                    const float alpha = m[c] == -INFINITY ? 0.0f : fast_exp2(m[c] - bm);
+                    m[c] = bm;
+                    lsum[c] *= alpha;
+#pragma unroll
+                    for (int t = 0; t < NCT; ++t)
+                        acc[c][t] *= alpha;
+                }
             }
+        }
+        half8 ph[QN];
+#pragma unroll
+        for (int c = 0; c < QN; ++c) {
             const float mn = m[c];
             float pv[8];
             float ps = 0.0f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                pv[e] = x[e] == -INFINITY ? 0.0f : fast_exp2(x[e] - mn);
+                // unmasked scores are finite and m[c] is too once a block was
+                // seen (a masked -inf would make -inf - -inf)
+                pv[e] = nomask ? fast_exp2(x[c][e] - mn) : x[c][e] == -INFINITY ? 0.0f : fast_exp2(x[c][e] - mn);
                 ps += pv[e];
             }
             lsum[c] += ps;
