@@ -209,6 +209,7 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
     const size_t sbase = (size_t)unit * p.sink;
     const size_t rbase = (size_t)unit * p.ring;
 
+#pragma unroll
     for (int pc = threadIdx.x; pc < 4 * D; pc += kDqThreads) {
         // K piece: token tau = pc / (D / 8), channels 8 P .. 8 P + 7
         {
