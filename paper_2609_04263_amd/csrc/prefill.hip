@@ -91,10 +91,13 @@ __host__ __device__ constexpr int kswz(int r)
     return D >= 128 ? (r & 15) : ((r >> 1) & 7);
 }
 
-// key-slot chunk q of V^T row d sits at chunk q ^ vswz(d) (64-byte rows)
+// key-slot chunk q of V^T row d sits at chunk q ^ vswz(d) (64-byte rows):
+// free of bank conflicts for the value-operand read (16 rows, four chunks
+// each), where (d >> 2) & 3 costs four extra cycles per read (measured with
+// the LDS bank-conflict counter)
 __host__ __device__ constexpr int vswz(int d)
 {
-    return (d >> 2) & 3;
+    return (d >> 1) & 3;
 }
 
 __device__ __forceinline__ float dq(int mode, int bits, uint32_t c, float s, float z)
