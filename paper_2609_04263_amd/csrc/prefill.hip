@@ -179,6 +179,16 @@ __device__ void fwht_rows(float* x, int rows, float c)
     __syncthreads();
 }
 
+// Whether workspace block v (sink block when sinkblk, else tail block blk)
+// is a code block: per-token key groups and every token of the block coded.
+// Its image holds the key codes as exact fp16 values in place of k_hat's hi
+// half, and the group scales and offsets in place of the lo half.
+template <int D>
+__device__ __forceinline__ bool code_block(const AttnParams& p, bool sinkblk, int blk)
+{
+    return p.k_axis == KVQ_PER_TOKEN && !(D >= 256 && p.k_group == 32) && !sinkblk && 32 * blk + 31 < p.nq;
+}
+
 // ---------------------------------------------------------------------------
 // 1. Block images.  Grid (blocks per unit, units of the group); workspace
 // block v of a unit is sink block v for v < pf_nsb, else tail block
@@ -211,6 +221,9 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
     const uint8_t* rvz = vaff ? (const uint8_t*)p.vz + ibf * vmeta : nullptr;
     const size_t sbase = (size_t)unit * p.sink;
     const size_t rbase = (size_t)unit * p.ring;
+    // a wholly coded block of per-token keys keeps its key codes exact (the
+    // attention kernel applies the group scales to the score tiles)
+    const bool ck = code_block<D>(p, sinkblk, blk);
 
 #pragma unroll
     for (int pc = threadIdx.x; pc < 4 * D; pc += kDqThreads) {
@@ -235,7 +248,11 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
                 const int r = 4 * (tau / 8) + tau % 4, half = (tau / 4) % 2;
                 const int idx = (half * 64 + r + 16 * (P % 4)) * (D / 32) + P / 4;
                 const Piece w = piece<W8>(rkc, idx, kbits);
-                if (p.k_axis == KVQ_PER_TOKEN) {
+                if (ck) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        x[e] = (float)code_of(w, kbits, e);
+                } else if (p.k_axis == KVQ_PER_TOKEN) {
                     const int mi = ((8 * P) / p.k_group) * 32 + tau;
                     const float sc = meta(rks, mi, m16), z = kaff ? meta(rkz, mi, m16) : 0.0f;
 #pragma unroll
@@ -261,10 +278,11 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
                     x[e] = 0.0f;
             }
             half8 h, l;
-            split_half8(x, &h, &l);
+            split_half8(x, &h, &l);  // codes are exact: l = 0
             const size_t off = (size_t)tau * 2 * D + 16 * (P ^ kswz<D>(tau));
             *(u32x4*)(img + off) = __builtin_bit_cast(u32x4, h);
-            *(u32x4*)(img + 64 * D + off) = __builtin_bit_cast(u32x4, l);
+            if (!ck)
+                *(u32x4*)(img + 64 * D + off) = __builtin_bit_cast(u32x4, l);
         }
         // V piece: channel d, key-slot chunk q (keys 4 q .. 4 q + 3 and
         // 16 + 4 q .. 16 + 4 q + 3); the four chunks of a row go to four
@@ -311,6 +329,18 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
                 }
             }
             *(u32x4*)(img + 128 * D + 64 * d + 16 * (q ^ vswz(d))) = __builtin_bit_cast(u32x4, pack_half8(x));
+        }
+    }
+    // a code block's key scales s[g][t] and offsets z'[g][t] (fp32, in place
+    // of the lo half), with k_hat = c s + z': z' = z for affine codes,
+    // -2^(bits-1) s for symmetric ones
+    if (ck) {
+        const int ng = D / p.k_group;
+        float* ms = (float*)(img + 64 * D);
+        for (int i = threadIdx.x; i < 32 * ng; i += kDqThreads) {
+            const float sc = meta(rks, i, m16);
+            ms[i] = sc;
+            ms[32 * ng + i] = kaff ? meta(rkz, i, m16) : -(float)(1 << (kbits - 1)) * sc;
         }
     }
 }
@@ -364,7 +394,9 @@ __device__ __forceinline__ void ring_sync(int after)
     __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int D>
+// KG: 32-channel score steps per key group when the format's keys have
+// per-token groups (code blocks then take exact code operands), 0 otherwise.
+template <int D, int KG>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 {
     constexpr int QN = qn<D>(), RT = rows_per_tile<D>(), NKS = D / 32, NCT = D / 16;
@@ -389,8 +421,11 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     // -sink .. -1, so a chunk that starts in the sink has negative positions.
     const int first_pos = p.n - C;  // position of chunk token 0
 
-    // ---- queries: lane's columns are rows r0 + 16 (QN wave + c) + col
+    // ---- queries: lane's columns are rows r0 + 16 (QN wave + c) + col;
+    // for code blocks also the sums of each query over each key group
+    constexpr int NG = KG > 0 ? NKS / KG : 1;
     half8 qh[QN][NKS], ql[QN][NKS];
+    float qsum[QN][NG];
     {
         float* xq = (float*)plds;  // [RT][D] fp32
         for (int idx = threadIdx.x; idx < RT * (D / 8); idx += kThreads) {
@@ -415,13 +450,25 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         for (int c = 0; c < QN; ++c) {
             const int rr = 16 * (QN * wave + c) + col;
 #pragma unroll
+            for (int g = 0; g < NG; ++g)
+                qsum[c][g] = 0.0f;
+#pragma unroll
             for (int ks = 0; ks < NKS; ++ks) {
                 float v[8];
+                float part = 0.0f;
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
+                for (int e = 0; e < 8; ++e) {
                     v[e] = xq[rr * D + 32 * ks + 8 * qg + e] * p.sm_log2;
+                    part += v[e];
+                }
                 split_half8(v, &qh[c][ks], &ql[c][ks]);
+                if (KG > 0)
+                    qsum[c][ks / (KG > 0 ? KG : 1)] += part;
             }
+            // the column's four lanes hold a quarter of every group each
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+                qsum[c][g] = KG > 0 ? xor_sum16_32(qsum[c][g]) : 0.0f;
         }
         __syncthreads();  // the ring overwrites the query rows
     }
@@ -507,31 +554,85 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 #pragma unroll
         for (int c = 0; c < QN; ++c)
             s[c][0] = s[c][1] = floatx4{0.f, 0.f, 0.f, 0.f};
-        half8 fa[2][2][2];  // [buffer][kt][hi, lo]
-        auto kread = [&](int ks, half8 (&f)[2][2]) {
-#pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-                const int row = 16 * kt + col;
-                const int off = row * 2 * D + 16 * ((4 * ks + qg) ^ kswz<D>(row));
-                f[kt][0] = __builtin_bit_cast(half8, *(const u32x4*)(kh + off));
-                f[kt][1] = __builtin_bit_cast(half8, *(const u32x4*)(kl + off));
-            }
-        };
-        kread(0, fa[0]);
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-            if (ks + 1 < NKS)
-                kread(ks + 1, fa[(ks + 1) & 1]);
+        auto copy_step = [&](int ks) {
             if (ks < (WI + 7) / 8 && more && wave + 8 * ks < WI)
                 copy16(cbase, (uint32_t)(1024 * (wave + 8 * ks) + 16 * lane), cat + 1024 * (wave + 8 * ks));
+        };
+        if (KG > 0 && code_block<D>(p, it < nsb, blk)) {
+            // exact codes c: S = sum_g s_g (c_g . q_g) + z'_g (sum q_g), the
+            // products c q over a group in two MFMAs per step (q hi, lo),
+            // then one scaling per group
+            const float* ms = (const float*)kl;
+            const float* mz = ms + 32 * NG;
+            half8 fc[2][2];  // [buffer][kt]
+            auto cread = [&](int ks, half8 (&f)[2]) {
 #pragma unroll
-            for (int kt = 0; kt < 2; ++kt) {
-                const half8 ah = fa[ks & 1][kt][0], al = fa[ks & 1][kt][1];
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int row = 16 * kt + col;
+                    f[kt] = __builtin_bit_cast(half8, *(const u32x4*)(kh + row * 2 * D + 16 * ((4 * ks + qg) ^ kswz<D>(row))));
+                }
+            };
+            cread(0, fc[0]);
 #pragma unroll
-                for (int c = 0; c < QN; ++c) {
-                    s[c][kt] = mfma16(ah, qh[c][ks], s[c][kt]);
-                    s[c][kt] = mfma16(ah, ql[c][ks], s[c][kt]);
-                    s[c][kt] = mfma16(al, qh[c][ks], s[c][kt]);
+            for (int g = 0; g < NG; ++g) {
+                floatx4 sg[QN][2];
+#pragma unroll
+                for (int c = 0; c < QN; ++c)
+                    sg[c][0] = sg[c][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int j = 0; j < (KG > 0 ? KG : 1); ++j) {
+                    const int ks = g * (KG > 0 ? KG : 1) + j;
+                    if (ks + 1 < NKS)
+                        cread(ks + 1, fc[(ks + 1) & 1]);
+                    copy_step(ks);
+#pragma unroll
+                    for (int kt = 0; kt < 2; ++kt) {
+                        const half8 a = fc[ks & 1][kt];
+#pragma unroll
+                        for (int c = 0; c < QN; ++c) {
+                            sg[c][kt] = mfma16(a, qh[c][ks], sg[c][kt]);
+                            sg[c][kt] = mfma16(a, ql[c][ks], sg[c][kt]);
+                        }
+                    }
+                }
+                const floatx4 s0 = *(const floatx4*)(ms + 32 * g + 4 * qg);
+                const floatx4 s1 = *(const floatx4*)(ms + 32 * g + 16 + 4 * qg);
+                const floatx4 z0 = *(const floatx4*)(mz + 32 * g + 4 * qg);
+                const floatx4 z1 = *(const floatx4*)(mz + 32 * g + 16 + 4 * qg);
+#pragma unroll
+                for (int c = 0; c < QN; ++c)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        s[c][0][i] = fmaf(s0[i], sg[c][0][i], fmaf(z0[i], qsum[c][g], s[c][0][i]));
+                        s[c][1][i] = fmaf(s1[i], sg[c][1][i], fmaf(z1[i], qsum[c][g], s[c][1][i]));
+                    }
+            }
+        } else {
+            half8 fa[2][2][2];  // [buffer][kt][hi, lo]
+            auto kread = [&](int ks, half8 (&f)[2][2]) {
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const int row = 16 * kt + col;
+                    const int off = row * 2 * D + 16 * ((4 * ks + qg) ^ kswz<D>(row));
+                    f[kt][0] = __builtin_bit_cast(half8, *(const u32x4*)(kh + off));
+                    f[kt][1] = __builtin_bit_cast(half8, *(const u32x4*)(kl + off));
+                }
+            };
+            kread(0, fa[0]);
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                if (ks + 1 < NKS)
+                    kread(ks + 1, fa[(ks + 1) & 1]);
+                copy_step(ks);
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const half8 ah = fa[ks & 1][kt][0], al = fa[ks & 1][kt][1];
+#pragma unroll
+                    for (int c = 0; c < QN; ++c) {
+                        s[c][kt] = mfma16(ah, qh[c][ks], s[c][kt]);
+                        s[c][kt] = mfma16(ah, ql[c][ks], s[c][kt]);
+                        s[c][kt] = mfma16(al, qh[c][ks], s[c][kt]);
+                    }
                 }
             }
         }
@@ -675,13 +776,24 @@ hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
     const int tiles = (p0.C * p0.G + RT - 1) / RT;
     const bool w8 = p0.k_bits == 8;  // 8-bit codes come as K and V both 8-bit
     void (*deq)(AttnParams) = w8 ? dequant_kernel<D, true> : dequant_kernel<D, false>;
+    // per-token key groups of 32 KG channels (a power of two from 32 to D);
+    // groups of 32 at D = 256 keep the hi + lo path (the code path's eight
+    // group sums per query would spill)
+    const int kg = p0.k_axis == KVQ_PER_TOKEN ? p0.k_group / 32 : 0;
+    void (*att)(AttnParams) = kg == 1   ? attn_kernel<D, (D >= 256 ? 0 : 1)>
+                              : kg == 2 ? attn_kernel<D, 2>
+                              : kg == 4 ? attn_kernel<D, (D >= 128 ? 4 : 1)>
+                              : kg == 8 ? attn_kernel<D, (D >= 256 ? 8 : 1)>
+                                        : attn_kernel<D, 0>;
+    if (kg != 0 && kg != 1 && kg != 2 && !(kg == 4 && D >= 128) && !(kg == 8 && D >= 256))
+        return hipErrorInvalidValue;
     for (int u0 = 0; u0 < units; u0 += group) {
         AttnParams p = p0;
         p.pf_u0 = u0;
         p.pf_tiles = tiles;
         const int nu = units - u0 < group ? units - u0 : group;
         launch_kernel(deq, dim3(p.pf_nvb, nu), dim3(kDqThreads), 0, stream, p);
-        launch_kernel(attn_kernel<D>, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(), stream, p);
+        launch_kernel(att, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(), stream, p);
     }
     return hipGetLastError();
 }
