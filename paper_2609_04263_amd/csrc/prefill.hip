@@ -6,10 +6,13 @@
 //   1. dequant_kernel reconstructs every visible 32-token block of a unit
 //      once into a workspace "block image" (192 D bytes): k_hat in fp32
 //      stored as fp16 hi + lo (hi + lo carries ~22 bits) as [token][D] rows,
-//      v_hat as fp16 transposed [D][32 key slots].  The image is laid out
-//      exactly as the attention kernel reads it from LDS (16-byte chunks
-//      xor-swizzled by row so that the fragment reads are free of bank
-//      conflicts), so it moves to LDS with plain linear copies.
+//      v_hat as fp16 transposed [D][32 key slots].  A block of per-token
+//      key groups whose tokens are all coded (a "code block") keeps the key
+//      codes instead, as exact fp16 values, with the groups' scales and
+//      offsets in place of the lo half.  The image is laid out exactly as
+//      the attention kernel reads it from LDS (16-byte chunks xor-swizzled
+//      by row so that the fragment reads are free of bank conflicts), so it
+//      moves to LDS with plain linear copies.
 //   2. attn_kernel: one workgroup per (unit, tile of query rows); query rows
 //      are the (chunk token, head of the KV group) pairs in token-major
 //      order.  Each of the eight waves owns 16 QN query rows (128 / 256 / 512
@@ -20,7 +23,9 @@
 //        query rows as columns; hi x hi + hi x lo + lo x hi), queries
 //        pre-scaled by sm_scale * log2(e) so the softmax runs in base 2,
 //        online per column (the running maximum moves only in steps of more
-//        than 2^8);
+//        than 2^8); for a code block S = sum_g s_g (c_g . q_g) + z'_g sum q_g
+//        with exact products c q (q as hi + lo) and one fp32 scaling of
+//        each group's score tile;
 //      - O^T += V^T P^T in fp16 (probabilities in [0, 1] and values each
 //        carry an 11-bit relative rounding, well inside the output bound;
 //        the logits are the precision-critical product).  A lane holds
