@@ -42,6 +42,8 @@
 // tokens past the coded ones are copied into the image from the ring.
 // Rotated formats transform the queries (FWHT in LDS) and the outputs back.
 
+#include <type_traits>
+
 #include "kvq_internal.h"
 #include "kvq_device.h"
 
@@ -64,11 +66,38 @@ constexpr int rows_per_tile()
 }
 
 // One reconstructed 32-token block: K hi [32][D], K lo [32][D] (fp16), then
-// V^T [D][32] (fp16).
+// V^T hi [D][32] (fp16), 192 D bytes; with lo halves of the values (lo,
+// rotating formats) V^T lo [D][32] follows, 256 D bytes.  At D = 256 that
+// would leave room for two images in LDS, so there the image with lo halves
+// is 50 KiB: a code block holds K codes, its scales and offsets (2 KiB), V^T
+// hi and lo; another block K hi, K lo and V^T hi only (its values are exact
+// fp16 rows of the sink or the window, or the few coded tokens of the block
+// where the window starts, rounded to fp16).
 template <int D>
-constexpr int image_bytes()
+__host__ __device__ constexpr int image_bytes(bool lo)
 {
-    return 192 * D;
+    return !lo ? 192 * D : D == 256 ? 50 * 1024 : 256 * D;
+}
+
+// Byte offsets in an image of the K lo half (or a code block's scales and
+// offsets) and of V^T hi and lo (lo: -1 when the block has none; images
+// with lo halves only).  A code block's V^T hi moves only in those.
+template <int D>
+__host__ __device__ constexpr int klo_at()
+{
+    return 64 * D;
+}
+
+template <int D>
+__host__ __device__ constexpr int vhi_at(bool lo, bool code)
+{
+    return lo && D == 256 && code ? 64 * D + 2048 : 128 * D;
+}
+
+template <int D>
+__host__ __device__ constexpr int vlo_at(bool code)
+{
+    return D == 256 ? (code ? 128 * D + 2048 : -1) : 192 * D;
 }
 
 // LDS ring depth (block images in flight)
@@ -81,10 +110,10 @@ constexpr int stages()
 // LDS: the ring, or the query / output staging [rows][D] fp32 when larger
 // (both are used by the same workgroup at different times).
 template <int D>
-constexpr size_t attn_lds_bytes()
+constexpr size_t attn_lds_bytes(bool lo)
 {
-    constexpr size_t ring = (size_t)stages<D>() * image_bytes<D>();
-    constexpr size_t rows = (size_t)rows_per_tile<D>() * D * 4;
+    const size_t ring = (size_t)stages<D>() * image_bytes<D>(lo);
+    const size_t rows = (size_t)rows_per_tile<D>() * D * 4;
     return ring > rows ? ring : rows;
 }
 
@@ -205,7 +234,8 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
 {
     const int v = blockIdx.x;
     const int unit = p.pf_u0 + blockIdx.y;
-    uint8_t* img = p.pf_ws + ((size_t)blockIdx.y * p.pf_nvb + v) * (size_t)image_bytes<D>();
+    const bool lo = p.rotate != 0;  // values get lo halves
+    uint8_t* img = p.pf_ws + ((size_t)blockIdx.y * p.pf_nvb + v) * (size_t)image_bytes<D>(lo);
     const bool sinkblk = v < p.pf_nsb;
     const int blk = v - p.pf_nsb;
 
@@ -287,7 +317,7 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
             const size_t off = (size_t)tau * 2 * D + 16 * (P ^ kswz<D>(tau));
             *(u32x4*)(img + off) = __builtin_bit_cast(u32x4, h);
             if (!ck)
-                *(u32x4*)(img + 64 * D + off) = __builtin_bit_cast(u32x4, l);
+                *(u32x4*)(img + klo_at<D>() + off) = __builtin_bit_cast(u32x4, l);
         }
         // V piece: channel d, key-slot chunk q (keys 4 q .. 4 q + 3 and
         // 16 + 4 q .. 16 + 4 q + 3); the four chunks of a row go to four
@@ -333,7 +363,20 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
                     }
                 }
             }
-            *(u32x4*)(img + 128 * D + 64 * d + 16 * (q ^ vswz(d))) = __builtin_bit_cast(u32x4, pack_half8(x));
+            // hi + lo carries ~22 bits: with rotation, a reconstruction
+            // rounded to fp16 alone (11 bits) let outputs near zero (the
+            // inverse rotation cancels large terms) miss the
+            // 2e-3 + 1e-2 |ref| bar
+            const int voff = 64 * d + 16 * (q ^ vswz(d));
+            if (lo) {
+                half8 vhi, vlo;
+                split_half8(x, &vhi, &vlo);
+                *(u32x4*)(img + vhi_at<D>(true, ck) + voff) = __builtin_bit_cast(u32x4, vhi);
+                if (vlo_at<D>(ck) >= 0)
+                    *(u32x4*)(img + vlo_at<D>(ck) + voff) = __builtin_bit_cast(u32x4, vlo);
+            } else {
+                *(u32x4*)(img + vhi_at<D>(false, ck) + voff) = __builtin_bit_cast(u32x4, pack_half8(x));
+            }
         }
     }
     // a code block's key scales s[g][t] and offsets z'[g][t] (fp32, in place
@@ -341,7 +384,7 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
     // -2^(bits-1) s for symmetric ones
     if (ck) {
         const int ng = D / p.k_group;
-        float* ms = (float*)(img + 64 * D);
+        float* ms = (float*)(img + klo_at<D>());
         for (int i = threadIdx.x; i < 32 * ng; i += kDqThreads) {
             const float sc = meta(rks, i, m16);
             ms[i] = sc;
@@ -360,7 +403,12 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
 __device__ __forceinline__ void copy16(uint64_t base, uint32_t voff, uint32_t lds_addr)
 {
     const uint32_t m0v = __builtin_amdgcn_readfirstlane(lds_addr);
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" : : "s"(m0v), "v"(voff), "s"(base) : "memory");
+    // (the builtin returns int: widen both halves as unsigned, or a low
+    // word with bit 31 set would be sign-extended into the high word)
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)base);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
+    const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" : : "s"(m0v), "v"(voff), "s"(sb) : "memory");
 }
 
 // s_waitcnt vmcnt(n) for a wave-uniform n (expcnt and lgkmcnt not waited)
@@ -401,11 +449,16 @@ __device__ __forceinline__ void ring_sync(int after)
 
 // KG: 32-channel score steps per key group when the format's keys have
 // per-token groups (code blocks then take exact code operands), 0 otherwise.
-template <int D, int KG>
+// LO: values carry a lo half (rotating formats).  The inverse rotation sums
+// the fp16 rounding errors of all D channels of a value into every output
+// element, which can itself be near zero; without rotation an output element
+// is a convex combination of one channel's values, and their fp16 rounding
+// (2^-11 relative) stays well inside the relative part of the error bar.
+template <int D, int KG, bool LO>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 {
     constexpr int QN = qn<D>(), RT = rows_per_tile<D>(), NKS = D / 32, NCT = D / 16;
-    constexpr int BI = image_bytes<D>(), NST = stages<D>();
+    constexpr int BI = image_bytes<D>(LO), NST = stages<D>();
     constexpr int WI = BI / 1024;  // 1 KiB wave copies per image
     extern __shared__ __attribute__((aligned(16))) uint8_t plds[];
 
@@ -537,8 +590,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     for (int it = 0; it < nvis; ++it) {
         const int blk = it < nsb ? it - sb0 : it - nsb;
         const uint8_t* kh = plds + stg * BI;
-        const uint8_t* kl = kh + 64 * D;
-        const uint8_t* vt = kh + 128 * D;
+        const uint8_t* kl = kh + klo_at<D>();
+        const bool codeb = KG > 0 && code_block<D>(p, it < nsb, blk);
+        const uint8_t* vt = kh + vhi_at<D>(LO, codeb);
+        // V^T lo (D = 256: code blocks only; another block reads its hi
+        // half again, and the products of lo stay zero)
+        const uint8_t* vtl = LO && vlo_at<D>(codeb) >= 0 ? kh + vlo_at<D>(codeb) : nullptr;
+        const bool vlo = vtl != nullptr;
         // copies of image it + NST - 1 (into the stage image it - 1 used),
         // one per score step so that the wave never waits on a burst of them
         const bool more = it + NST - 1 < nvis;
@@ -563,7 +621,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
             if (ks < (WI + 7) / 8 && more && wave + 8 * ks < WI)
                 copy16(cbase, (uint32_t)(1024 * (wave + 8 * ks) + 16 * lane), cat + 1024 * (wave + 8 * ks));
         };
-        if (KG > 0 && code_block<D>(p, it < nsb, blk)) {
+        if (codeb) {
             // exact codes c: S = sum_g s_g (c_g . q_g) + z'_g (sum q_g), the
             // products c q over a group in two MFMAs per step (q hi, lo),
             // then one scaling per group
@@ -648,12 +706,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
                 copy16(cbase, (uint32_t)(1024 * (wave + 8 * i) + 16 * lane), cat + 1024 * (wave + 8 * i));
 
         // the first value fragments, read while the softmax runs
-        constexpr int NVP = NCT < 4 ? NCT : 4;
-        half8 vf[NVP];
+        constexpr int NVP = D == 256 ? 1 : 2;  // value fragments read ahead (hi and lo)
+        half8 vf[NVP], vfl[NVP];
 #pragma unroll
         for (int t = 0; t < NVP; ++t) {
             const int d = 16 * t + col;
-            vf[t] = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
+            const int off = 64 * d + 16 * (qg ^ vswz(d));
+            vf[t] = __builtin_bit_cast(half8, *(const u32x4*)(vt + off));
+            vfl[t] = vlo ? __builtin_bit_cast(half8, *(const u32x4*)(vtl + off)) : half8{};
         }
 
         // ---- online softmax per query column; P^T operands
@@ -710,17 +770,30 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 
         // ---- O^T += V^T P^T, 16 channels per tile, keys in the slot order
         // above; fragment t + NVP is read while tile t's MFMAs run
+        auto value_products = [&](auto lo_tag) {
+            constexpr bool VL = decltype(lo_tag)::value;
 #pragma unroll
-        for (int t = 0; t < NCT; ++t) {
-            const half8 av = vf[t % NVP];
-            if (t + NVP < NCT) {
-                const int d = 16 * (t + NVP) + col;
-                vf[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
+            for (int t = 0; t < NCT; ++t) {
+                const half8 av = vf[t % NVP], avl = vfl[t % NVP];
+                if (t + NVP < NCT) {
+                    const int d = 16 * (t + NVP) + col;
+                    const int off = 64 * d + 16 * (qg ^ vswz(d));
+                    vf[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vt + off));
+                    if (VL)
+                        vfl[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vtl + off));
+                }
+#pragma unroll
+                for (int c = 0; c < QN; ++c) {
+                    acc[c][t] = mfma16(av, ph[c], acc[c][t]);
+                    if (VL)
+                        acc[c][t] = mfma16(avl, ph[c], acc[c][t]);
+                }
             }
-#pragma unroll
-            for (int c = 0; c < QN; ++c)
-                acc[c][t] = mfma16(av, ph[c], acc[c][t]);
-        }
+        };
+        if (vlo)
+            value_products(std::true_type{});
+        else
+            value_products(std::false_type{});
         // image it + 1 has landed (all of this wave's copies but those of
         // the images after it), and no wave reads stage it any more
         ring_sync(it + NST - 1 < nvis ? cw * (NST - 2) : 0);
@@ -769,12 +842,23 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     }
 }
 
+template <int D, bool LO>
+void (*pick(int kg))(AttnParams)
+{
+    return kg == 1   ? attn_kernel<D, (D >= 256 ? 0 : 1), LO>
+           : kg == 2 ? attn_kernel<D, 2, LO>
+           : kg == 4 ? attn_kernel<D, (D >= 128 ? 4 : 1), LO>
+           : kg == 8 ? attn_kernel<D, (D >= 256 ? 8 : 1), LO>
+                     : attn_kernel<D, 0, LO>;
+}
+
 template <int D>
 hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
 {
     constexpr int RT = rows_per_tile<D>();
     const int units = p0.B * p0.H;
-    const size_t per_unit = (size_t)p0.pf_nvb * image_bytes<D>();
+    const bool lo = p0.rotate != 0;
+    const size_t per_unit = (size_t)p0.pf_nvb * image_bytes<D>(lo);
     const int group = (int)(ws_bytes / per_unit < (size_t)units ? ws_bytes / per_unit : (size_t)units);
     if (group < 1)
         return hipErrorInvalidValue;
@@ -785,11 +869,7 @@ hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
     // groups of 32 at D = 256 keep the hi + lo path (the code path's eight
     // group sums per query would spill)
     const int kg = p0.k_axis == KVQ_PER_TOKEN ? p0.k_group / 32 : 0;
-    void (*att)(AttnParams) = kg == 1   ? attn_kernel<D, (D >= 256 ? 0 : 1)>
-                              : kg == 2 ? attn_kernel<D, 2>
-                              : kg == 4 ? attn_kernel<D, (D >= 128 ? 4 : 1)>
-                              : kg == 8 ? attn_kernel<D, (D >= 256 ? 8 : 1)>
-                                        : attn_kernel<D, 0>;
+    void (*att)(AttnParams) = lo ? pick<D, true>(kg) : pick<D, false>(kg);
     if (kg != 0 && kg != 1 && kg != 2 && !(kg == 4 && D >= 128) && !(kg == 8 && D >= 256))
         return hipErrorInvalidValue;
     for (int u0 = 0; u0 < units; u0 += group) {
@@ -798,16 +878,23 @@ hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
         p.pf_tiles = tiles;
         const int nu = units - u0 < group ? units - u0 : group;
         launch_kernel(deq, dim3(p.pf_nvb, nu), dim3(kDqThreads), 0, stream, p);
-        launch_kernel(att, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(), stream, p);
+        launch_kernel(att, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(lo), stream, p);
     }
     return hipGetLastError();
 }
 
 }  // namespace pre
 
-size_t prefill_image_bytes(int D)
+size_t prefill_image_bytes(int D, bool rotate)
 {
-    return (size_t)192 * D;
+    switch (D) {
+    case 64:
+        return pre::image_bytes<64>(rotate);
+    case 128:
+        return pre::image_bytes<128>(rotate);
+    default:
+        return pre::image_bytes<256>(rotate);
+    }
 }
 
 hipError_t launch_prefill(const AttnParams& p, int D, size_t ws_bytes, hipStream_t stream)
