@@ -76,6 +76,13 @@ def test_prefill_workload_shape_chunk():
     run("gqa12b", B=1, H=2, G=2, n=1280, C=256, seed=130)
 
 
+def test_prefill_rotated_outputs_near_zero():
+    # rotated K4V2 with 128 sinks: outputs near zero missed the bar while
+    # each value entered the products as a single fp16 rounding (the inverse
+    # rotation sums the rounding errors of all D channels into every output)
+    run("kvarn_sink", B=2, H=2, G=2, n=505, C=406, seed=346969)
+
+
 @pytest.mark.parametrize("name", ["tiny_b16", "kivi", "kvarn_sink"])
 def test_prefill_workspace_groups(name):
     # B H = 6 units: one pass, groups of 4 + 2, and one unit at a time
