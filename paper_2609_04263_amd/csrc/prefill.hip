@@ -449,16 +449,19 @@ __device__ __forceinline__ void ring_sync(int after)
 
 // KG: 32-channel score steps per key group when the format's keys have
 // per-token groups (code blocks then take exact code operands), 0 otherwise.
-// LO: values carry a lo half (rotating formats).  The inverse rotation sums
-// the fp16 rounding errors of all D channels of a value into every output
-// element, which can itself be near zero; without rotation an output element
-// is a convex combination of one channel's values, and their fp16 rounding
-// (2^-11 relative) stays well inside the relative part of the error bar.
-template <int D, int KG, bool LO>
+// ROT: a rotating format, whose queries (rotated in fp32) and values carry
+// fp16 lo halves.  The inverse rotation sums the fp16 rounding errors of all
+// D channels of a value into every output element, which can itself be near
+// zero; without rotation an output element is a convex combination of one
+// channel's values, and their fp16 rounding (2^-11 relative) stays well
+// inside the relative part of the error bar.  A bf16 query of a non-rotating
+// format is exact in fp16 once scaled by a power of two, so its score steps
+// take one MFMA per key tile (code blocks) or two (hi and lo keys).
+template <int D, int KG, bool ROT>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 {
     constexpr int QN = qn<D>(), RT = rows_per_tile<D>(), NKS = D / 32, NCT = D / 16;
-    constexpr int BI = image_bytes<D>(LO), NST = stages<D>();
+    constexpr int BI = image_bytes<D>(ROT), NST = stages<D>();
     constexpr int WI = BI / 1024;  // 1 KiB wave copies per image
     extern __shared__ __attribute__((aligned(16))) uint8_t plds[];
 
@@ -480,10 +483,16 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     const int first_pos = p.n - C;  // position of chunk token 0
 
     // ---- queries: lane's columns are rows r0 + 16 (QN wave + c) + col;
-    // for code blocks also the sums of each query over each key group
+    // for code blocks also the sums of each query over each key group.
+    // Rotated queries are scaled by sm_scale log2(e) and split into fp16 hi
+    // + lo; others are scaled by qscale, sm_scale log2(e) rounded down to a
+    // power of two (exact in fp16 below 65504), and the scores take the
+    // rest, sscale.
     constexpr int NG = KG > 0 ? NKS / KG : 1;
     half8 qh[QN][NKS], ql[QN][NKS];
     float qsum[QN][NG];
+    const float qscale = ROT ? p.sm_log2 : __uint_as_float(__float_as_uint(p.sm_log2) & 0xFF800000u);
+    const float sscale = ROT ? 1.0f : qscale != 0.0f ? p.sm_log2 / qscale : 0.0f;
     {
         float* xq = (float*)plds;  // [RT][D] fp32
         for (int idx = threadIdx.x; idx < RT * (D / 8); idx += kThreads) {
@@ -516,10 +525,13 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
                 float part = 0.0f;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    v[e] = xq[rr * D + 32 * ks + 8 * qg + e] * p.sm_log2;
+                    v[e] = xq[rr * D + 32 * ks + 8 * qg + e] * qscale;
                     part += v[e];
                 }
-                split_half8(v, &qh[c][ks], &ql[c][ks]);
+                if (ROT)
+                    split_half8(v, &qh[c][ks], &ql[c][ks]);
+                else
+                    qh[c][ks] = pack_half8(v);
                 if (KG > 0)
                     qsum[c][ks / (KG > 0 ? KG : 1)] += part;
             }
@@ -592,10 +604,10 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         const uint8_t* kh = plds + stg * BI;
         const uint8_t* kl = kh + klo_at<D>();
         const bool codeb = KG > 0 && code_block<D>(p, it < nsb, blk);
-        const uint8_t* vt = kh + vhi_at<D>(LO, codeb);
+        const uint8_t* vt = kh + vhi_at<D>(ROT, codeb);
         // V^T lo (D = 256: code blocks only; another block reads its hi
         // half again, and the products of lo stay zero)
-        const uint8_t* vtl = LO && vlo_at<D>(codeb) >= 0 ? kh + vlo_at<D>(codeb) : nullptr;
+        const uint8_t* vtl = ROT && vlo_at<D>(codeb) >= 0 ? kh + vlo_at<D>(codeb) : nullptr;
         const bool vlo = vtl != nullptr;
         // copies of image it + NST - 1 (into the stage image it - 1 used),
         // one per score step so that the wave never waits on a burst of them
@@ -623,8 +635,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         };
         if (codeb) {
             // exact codes c: S = sum_g s_g (c_g . q_g) + z'_g (sum q_g), the
-            // products c q over a group in two MFMAs per step (q hi, lo),
-            // then one scaling per group
+            // products c q over a group in one MFMA per step and key tile
+            // (two, q hi and lo, when rotating), then one scaling per group
             const float* ms = (const float*)kl;
             const float* mz = ms + 32 * NG;
             half8 fc[2][2];  // [buffer][kt]
@@ -654,7 +666,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 #pragma unroll
                         for (int c = 0; c < QN; ++c) {
                             sg[c][kt] = mfma16(a, qh[c][ks], sg[c][kt]);
-                            sg[c][kt] = mfma16(a, ql[c][ks], sg[c][kt]);
+                            if (ROT)
+                                sg[c][kt] = mfma16(a, ql[c][ks], sg[c][kt]);
                         }
                     }
                 }
@@ -693,7 +706,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 #pragma unroll
                     for (int c = 0; c < QN; ++c) {
                         s[c][kt] = mfma16(ah, qh[c][ks], s[c][kt]);
-                        s[c][kt] = mfma16(ah, ql[c][ks], s[c][kt]);
+                        if (ROT)
+                            s[c][kt] = mfma16(ah, ql[c][ks], s[c][kt]);
                         s[c][kt] = mfma16(al, qh[c][ks], s[c][kt]);
                     }
                 }
@@ -732,7 +746,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 const int key = 32 * blk + (e < 4 ? 4 * qg + e : 16 + 4 * qg + e - 4);
-                x[c][e] = nomask || key <= qpos[c] ? s[c][e >> 2][e & 3] : -INFINITY;
+                const float se = ROT ? s[c][e >> 2][e & 3] : s[c][e >> 2][e & 3] * sscale;
+                x[c][e] = nomask || key <= qpos[c] ? se : -INFINITY;
                 lm[c] = fmaxf(lm[c], x[c][e]);
             }
             up = up || lm[c] > m[c] + 8.0f;
@@ -842,14 +857,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     }
 }
 
-template <int D, bool LO>
+template <int D, bool ROT>
 void (*pick(int kg))(AttnParams)
 {
-    return kg == 1   ? attn_kernel<D, (D >= 256 ? 0 : 1), LO>
-           : kg == 2 ? attn_kernel<D, 2, LO>
-           : kg == 4 ? attn_kernel<D, (D >= 128 ? 4 : 1), LO>
-           : kg == 8 ? attn_kernel<D, (D >= 256 ? 8 : 1), LO>
-                     : attn_kernel<D, 0, LO>;
+    return kg == 1   ? attn_kernel<D, (D >= 256 ? 0 : 1), ROT>
+           : kg == 2 ? attn_kernel<D, 2, ROT>
+           : kg == 4 ? attn_kernel<D, (D >= 128 ? 4 : 1), ROT>
+           : kg == 8 ? attn_kernel<D, (D >= 256 ? 8 : 1), ROT>
+                     : attn_kernel<D, 0, ROT>;
 }
 
 template <int D>
