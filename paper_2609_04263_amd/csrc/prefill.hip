@@ -492,7 +492,9 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     half8 qh[QN][NKS], ql[QN][NKS];
     float qsum[QN][NG];
     const float qscale = ROT ? p.sm_log2 : __uint_as_float(__float_as_uint(p.sm_log2) & 0xFF800000u);
-    const float sscale = ROT ? 1.0f : qscale != 0.0f ? p.sm_log2 / qscale : 0.0f;
+    // (qscale keeps the sign of the scale, so sscale > 0; a zero or
+    // subnormal scale gives zero queries, zero scores and sscale 1)
+    const float sscale = ROT || qscale == 0.0f ? 1.0f : p.sm_log2 / qscale;
     {
         float* xq = (float*)plds;  // [RT][D] fp32
         for (int idx = threadIdx.x; idx < RT * (D / 8); idx += kThreads) {
@@ -738,18 +740,28 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         // it is gathered only when some lane of the wave holds a score
         // beyond its running maximum + 8 (otherwise no column is raised).
         const bool nomask = 32 * blk + 31 <= wave_first;  // wave-uniform
+        // scores x are in the units of the MFMA sums; x sscale is the
+        // exponent (sscale > 0), and m is kept in exponent units
         float x[QN][8], lm[QN];
         bool up = false;
 #pragma unroll
         for (int c = 0; c < QN; ++c) {
             lm[c] = -INFINITY;
+            if (nomask) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int key = 32 * blk + (e < 4 ? 4 * qg + e : 16 + 4 * qg + e - 4);
-                const float se = ROT ? s[c][e >> 2][e & 3] : s[c][e >> 2][e & 3] * sscale;
-                x[c][e] = nomask || key <= qpos[c] ? se : -INFINITY;
-                lm[c] = fmaxf(lm[c], x[c][e]);
+                for (int e = 0; e < 8; ++e) {
+                    x[c][e] = s[c][e >> 2][e & 3];
+                    lm[c] = fmaxf(lm[c], x[c][e]);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int key = 32 * blk + (e < 4 ? 4 * qg + e : 16 + 4 * qg + e - 4);
+                    x[c][e] = key <= qpos[c] ? s[c][e >> 2][e & 3] : -INFINITY;
+                    lm[c] = fmaxf(lm[c], x[c][e]);
+                }
             }
+            lm[c] *= sscale;
             up = up || lm[c] > m[c] + 8.0f;
         }
         if (__any(up)) {
@@ -769,14 +781,15 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         half8 ph[QN];
 #pragma unroll
         for (int c = 0; c < QN; ++c) {
-            const float mn = m[c];
+            // m is finite once a column has seen a key (every existing query
+            // row sees a key of the first block); a column that has not
+            // takes 0, so that its masked -inf scores give 0, not NaN
+            const float mn = m[c] == -INFINITY ? 0.0f : m[c];
             float pv[8];
             float ps = 0.0f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                // unmasked scores are finite and m[c] is too once a block was
-                // seen (a masked -inf would make -inf - -inf)
-                pv[e] = nomask ? fast_exp2(x[c][e] - mn) : x[c][e] == -INFINITY ? 0.0f : fast_exp2(x[c][e] - mn);
+                pv[e] = fast_exp2(fmaf(x[c][e], sscale, -mn));
                 ps += pv[e];
             }
             lsum[c] += ps;
