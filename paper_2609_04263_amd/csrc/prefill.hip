@@ -489,8 +489,12 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     // power of two (exact in fp16 below 65504), and the scores take the
     // rest, sscale.
     constexpr int NG = KG > 0 ? NKS / KG : 1;
+    // Offset terms of code blocks as one fp32 MFMA per key tile (ZM) where
+    // that measured faster than their FMAs: one 16-row query set per wave,
+    // four key groups, no rotation (the rotated path's MFMA pipe is busier)
+    constexpr bool ZM = !ROT && QN == 1 && NG == 4;
     half8 qh[QN][NKS], ql[QN][NKS];
-    float qsum[QN][NG];
+    float qsum[QN][NG], qsb[QN];
     const float qscale = ROT ? p.sm_log2 : __uint_as_float(__float_as_uint(p.sm_log2) & 0xFF800000u);
     // (qscale keeps the sign of the scale, so sscale > 0; a zero or
     // subnormal scale gives zero queries, zero scores and sscale 1)
@@ -541,6 +545,12 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 #pragma unroll
             for (int g = 0; g < NG; ++g)
                 qsum[c][g] = KG > 0 ? xor_sum16_32(qsum[c][g]) : 0.0f;
+            // B operand of the offset product: lane (col, qg) holds the
+            // column's sum over group qg (zero beyond NG)
+            qsb[c] = 0.0f;
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+                qsb[c] = ZM && qg == g ? qsum[c][g] : qsb[c];
         }
         __syncthreads();  // the ring overwrites the query rows
     }
@@ -577,8 +587,9 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
     const int sb0 = p.sink >> 5;  // sink block j is tail block j - sb0
     const int nvis = nsb + nkb;
 
-    // This wave's copies of an image: wave copies wave, wave + 8, ... < WI.
-    const int cw = (WI - wave + 7) / 8;
+    // This wave's copies of an image: wave copies wave, wave + 8, ... < WI
+    // (the same count for every wave when WI is a multiple of 8).
+    const int cw = WI % 8 == 0 ? WI / 8 : (WI - wave + 7) / 8;
     const uint32_t lbase = (uint32_t)(uintptr_t)plds;
     const uint8_t* ws_unit = p.pf_ws + (size_t)uloc * p.pf_nvb * BI;
     auto issue = [&](int it) {
@@ -588,7 +599,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 #pragma unroll
         for (int i = 0; i < (WI + 7) / 8; ++i) {
             const int k = wave + 8 * i;
-            if (k < WI)
+            if (WI % 8 == 0 || k < WI)
                 copy16(base, (uint32_t)(1024 * k + 16 * lane), at + 1024 * k);
         }
     };
@@ -632,15 +643,27 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         for (int c = 0; c < QN; ++c)
             s[c][0] = s[c][1] = floatx4{0.f, 0.f, 0.f, 0.f};
         auto copy_step = [&](int ks) {
-            if (ks < (WI + 7) / 8 && more && wave + 8 * ks < WI)
+            if (ks < (WI + 7) / 8 && more && (WI % 8 == 0 || wave + 8 * ks < WI))
                 copy16(cbase, (uint32_t)(1024 * (wave + 8 * ks) + 16 * lane), cat + 1024 * (wave + 8 * ks));
         };
         if (codeb) {
             // exact codes c: S = sum_g s_g (c_g . q_g) + z'_g (sum q_g), the
             // products c q over a group in one MFMA per step and key tile
-            // (two, q hi and lo, when rotating), then one scaling per group
+            // (two, q hi and lo, when rotating), then one scaling per group;
+            // with ZM the offset terms are one fp32 product [16 keys x 4
+            // groups] x [4 groups x 16 queries] per key tile (A: lane (col,
+            // qg) holds z'[qg][key col])
             const float* ms = (const float*)kl;
             const float* mz = ms + 32 * NG;
+            if (ZM) {
+#pragma unroll
+                for (int kt = 0; kt < 2; ++kt) {
+                    const float za = mz[32 * qg + 16 * kt + col];
+#pragma unroll
+                    for (int c = 0; c < QN; ++c)
+                        s[c][kt] = __builtin_amdgcn_mfma_f32_16x16x4f32(za, qsb[c], s[c][kt], 0, 0, 0);
+                }
+            }
             half8 fc[2][2];  // [buffer][kt]
             auto cread = [&](int ks, half8 (&f)[2]) {
 #pragma unroll
@@ -675,14 +698,19 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
                 }
                 const floatx4 s0 = *(const floatx4*)(ms + 32 * g + 4 * qg);
                 const floatx4 s1 = *(const floatx4*)(ms + 32 * g + 16 + 4 * qg);
-                const floatx4 z0 = *(const floatx4*)(mz + 32 * g + 4 * qg);
-                const floatx4 z1 = *(const floatx4*)(mz + 32 * g + 16 + 4 * qg);
+                floatx4 z0 = {0.f, 0.f, 0.f, 0.f}, z1 = z0;
+                if (!ZM) {
+                    z0 = *(const floatx4*)(mz + 32 * g + 4 * qg);
+                    z1 = *(const floatx4*)(mz + 32 * g + 16 + 4 * qg);
+                }
 #pragma unroll
                 for (int c = 0; c < QN; ++c)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        s[c][0][i] = fmaf(s0[i], sg[c][0][i], fmaf(z0[i], qsum[c][g], s[c][0][i]));
-                        s[c][1][i] = fmaf(s1[i], sg[c][1][i], fmaf(z1[i], qsum[c][g], s[c][1][i]));
+                        const float o0 = ZM ? s[c][0][i] : fmaf(z0[i], qsum[c][g], s[c][0][i]);
+                        const float o1 = ZM ? s[c][1][i] : fmaf(z1[i], qsum[c][g], s[c][1][i]);
+                        s[c][0][i] = fmaf(s0[i], sg[c][0][i], o0);
+                        s[c][1][i] = fmaf(s1[i], sg[c][1][i], o1);
                     }
             }
         } else {
@@ -718,7 +746,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         // copies left over when an image needs more than NKS per wave
 #pragma unroll
         for (int i = NKS; i < (WI + 7) / 8; ++i)
-            if (more && wave + 8 * i < WI)
+            if (more && (WI % 8 == 0 || wave + 8 * i < WI))
                 copy16(cbase, (uint32_t)(1024 * (wave + 8 * i) + 16 * lane), cat + 1024 * (wave + 8 * i));
 
         // the first value fragments, read while the softmax runs
