@@ -289,14 +289,12 @@ kvq_status kvq_decode_attn_noalloc(const kvq_cache* cache, const void* Q, int H_
  * the caller; invalid arguments return KVQ_ERR_ARG before any launch.
  *   workspace  device scratch for the reconstructed blocks of each (b, h):
  *              every visible 32-token block is reconstructed once per call
- *              (192 D bytes each; 256 D, 50 KiB at D = 256, for a rotating
- *              format, whose values carry a second fp16 half) and read
- *              back by all the chunk's query tiles.
- *              kvq_prefill_workspace_bytes gives the size that serves all
- *              B H_kv units in one pass; a smaller workspace (at least
- *              one unit's share, that size / (B H_kv)) makes the call
- *              process the units in groups that fit, with more launches.
- *              Below one unit's share: KVQ_ERR_WORKSPACE.
+ *              (192 D bytes each) and read back by all the chunk's query
+ *              tiles.  kvq_prefill_workspace_bytes gives the size that
+ *              serves all B H_kv units in one pass; a smaller workspace
+ *              (at least one unit's share, that size / (B H_kv)) makes the
+ *              call process the units in groups that fit, with more
+ *              launches.  Below one unit's share: KVQ_ERR_WORKSPACE.
  *              Calls that share a workspace must not overlap. */
 kvq_status kvq_prefill_attn(const kvq_cache* cache, const void* Q, int C, int H_q, float sm_scale, void* O,
                             void* workspace, size_t ws_bytes, void* stream);

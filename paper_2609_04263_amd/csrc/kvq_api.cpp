@@ -792,7 +792,7 @@ kvq_status kvq_prefill_workspace_bytes(const kvq_cache* c, size_t* bytes)
         return KVQ_ERR_ARG;
     int nsb, nvb;
     prefill_blocks(c, &nsb, &nvb);
-    *bytes = (size_t)c->B * c->H * nvb * kvq::prefill_image_bytes(c->D, c->fmt.rotate != 0);
+    *bytes = (size_t)c->B * c->H * nvb * kvq::prefill_image_bytes(c->D);
     return KVQ_OK;
 }
 
@@ -805,7 +805,7 @@ kvq_status kvq_prefill_attn(const kvq_cache* c, const void* Q, int C, int H_q, f
         return KVQ_ERR_ARG;
     int nsb, nvb;
     prefill_blocks(c, &nsb, &nvb);
-    if (!workspace || !aligned16(workspace) || ws_bytes < (size_t)nvb * kvq::prefill_image_bytes(c->D, c->fmt.rotate != 0))
+    if (!workspace || !aligned16(workspace) || ws_bytes < (size_t)nvb * kvq::prefill_image_bytes(c->D))
         return KVQ_ERR_WORKSPACE;
     const kvq_format& f = c->fmt;
     kvq::AttnParams p = {};

@@ -191,9 +191,8 @@ int decode_split_bound(int B, int H);
 // Dynamic LDS of the split kernel.
 size_t decode_lds_bytes(int D, const kvq_format& f, int G);
 hipError_t launch_decode(const AttnParams& p, int D, hipStream_t stream);
-// Bytes of one reconstructed 32-token block (prefill workspace unit); a
-// rotating format's values carry lo halves.
-size_t prefill_image_bytes(int D, bool rotate);
+// Bytes of one reconstructed 32-token block (prefill workspace unit).
+size_t prefill_image_bytes(int D);
 // Chunked prefill over units in groups that fit ws_bytes (at least one unit).
 hipError_t launch_prefill(const AttnParams& p, int D, size_t ws_bytes, hipStream_t stream);
 

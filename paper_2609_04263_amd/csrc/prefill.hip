@@ -42,8 +42,6 @@
 // tokens past the coded ones are copied into the image from the ring.
 // Rotated formats transform the queries (FWHT in LDS) and the outputs back.
 
-#include <type_traits>
-
 #include "kvq_internal.h"
 #include "kvq_device.h"
 
@@ -66,22 +64,18 @@ constexpr int rows_per_tile()
 }
 
 // One reconstructed 32-token block: K hi [32][D], K lo [32][D] (fp16), then
-// V^T hi [D][32] (fp16), 192 D bytes; with lo halves of the values (lo,
-// rotating formats) V^T lo [D][32] follows, 256 D bytes.  At D = 256 that
-// would leave room for two images in LDS, so there the image with lo halves
-// is 50 KiB: a code block holds K codes, its scales and offsets (2 KiB), V^T
-// hi and lo; another block K hi, K lo and V^T hi only (its values are exact
-// fp16 rows of the sink or the window, or the few coded tokens of the block
-// where the window starts, rounded to fp16).
+// V^T [D][32] (fp16), 192 D bytes.  A rotating format's values are rotated
+// back (an fp32 FWHT per token) before they are rounded, so the outputs need
+// no inverse rotation and every output element carries the rounding of one
+// channel's values, as without rotation.
 template <int D>
-__host__ __device__ constexpr int image_bytes(bool lo)
+__host__ __device__ constexpr int image_bytes()
 {
-    return !lo ? 192 * D : D == 256 ? 50 * 1024 : 256 * D;
+    return 192 * D;
 }
 
 // Byte offsets in an image of the K lo half (or a code block's scales and
-// offsets) and of V^T hi and lo (lo: -1 when the block has none; images
-// with lo halves only).  A code block's V^T hi moves only in those.
+// offsets) and of V^T.
 template <int D>
 __host__ __device__ constexpr int klo_at()
 {
@@ -89,15 +83,9 @@ __host__ __device__ constexpr int klo_at()
 }
 
 template <int D>
-__host__ __device__ constexpr int vhi_at(bool lo, bool code)
+__host__ __device__ constexpr int vt_at()
 {
-    return lo && D == 256 && code ? 64 * D + 2048 : 128 * D;
-}
-
-template <int D>
-__host__ __device__ constexpr int vlo_at(bool code)
-{
-    return D == 256 ? (code ? 128 * D + 2048 : -1) : 192 * D;
+    return 128 * D;
 }
 
 // LDS ring depth (block images in flight)
@@ -110,10 +98,10 @@ constexpr int stages()
 // LDS: the ring, or the query / output staging [rows][D] fp32 when larger
 // (both are used by the same workgroup at different times).
 template <int D>
-constexpr size_t attn_lds_bytes(bool lo)
+constexpr size_t attn_lds_bytes()
 {
-    const size_t ring = (size_t)stages<D>() * image_bytes<D>(lo);
-    const size_t rows = (size_t)rows_per_tile<D>() * D * 4;
+    constexpr size_t ring = (size_t)stages<D>() * image_bytes<D>();
+    constexpr size_t rows = (size_t)rows_per_tile<D>() * D * 4;
     return ring > rows ? ring : rows;
 }
 
@@ -194,12 +182,13 @@ __device__ __forceinline__ float half_bits(const uint16_t* row, size_t i)
     return f16_bits_to_f32(row[i]);
 }
 
-// In-place unnormalized FWHT of rows [rows][D] fp32 in LDS, then * c.
-template <int D>
+// In-place unnormalized FWHT of rows [rows][D] fp32 in LDS, then * c, by a
+// workgroup of NTH threads.
+template <int D, int NTH>
 __device__ void fwht_rows(float* x, int rows, float c)
 {
     for (int h = 1; h < D; h <<= 1) {
-        for (int idx = threadIdx.x; idx < rows * (D / 2); idx += kThreads) {
+        for (int idx = threadIdx.x; idx < rows * (D / 2); idx += NTH) {
             const int row = idx / (D / 2), k = idx % (D / 2);
             const int j = (k / h) * 2 * h + (k % h);
             const float a = x[row * D + j], b = x[row * D + j + h];
@@ -208,7 +197,7 @@ __device__ void fwht_rows(float* x, int rows, float c)
         }
         __syncthreads();
     }
-    for (int idx = threadIdx.x; idx < rows * D; idx += kThreads)
+    for (int idx = threadIdx.x; idx < rows * D; idx += NTH)
         x[idx] *= c;
     __syncthreads();
 }
@@ -228,14 +217,17 @@ __device__ __forceinline__ bool code_block(const AttnParams& p, bool sinkblk, in
 // block v of a unit is sink block v for v < pf_nsb, else tail block
 // v - pf_nsb.  Tokens past the end (sink rows beyond n_sink, tail tokens
 // beyond n) are zeros: the causal mask removes them, and zero values keep
-// 0 * v finite.  W8: both code widths are 8 bits.
-template <int D, bool W8>
+// 0 * v finite.  W8: both code widths are 8 bits.  A rotating format's
+// value rows (coded, window and sink rows alike are stored rotated) pass
+// through LDS ([32][D] fp32, dynamic) to be rotated back before they are
+// rounded to fp16 (ROT).
+template <int D, bool W8, bool ROT>
 __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
 {
+    extern __shared__ __attribute__((aligned(16))) float vrows[];
     const int v = blockIdx.x;
     const int unit = p.pf_u0 + blockIdx.y;
-    const bool lo = p.rotate != 0;  // values get lo halves
-    uint8_t* img = p.pf_ws + ((size_t)blockIdx.y * p.pf_nvb + v) * (size_t)image_bytes<D>(lo);
+    uint8_t* img = p.pf_ws + ((size_t)blockIdx.y * p.pf_nvb + v) * (size_t)image_bytes<D>();
     const bool sinkblk = v < p.pf_nsb;
     const int blk = v - p.pf_nsb;
 
@@ -363,20 +355,26 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
                     }
                 }
             }
-            // hi + lo carries ~22 bits: with rotation, a reconstruction
-            // rounded to fp16 alone (11 bits) let outputs near zero (the
-            // inverse rotation cancels large terms) miss the
-            // 2e-3 + 1e-2 |ref| bar
-            const int voff = 64 * d + 16 * (q ^ vswz(d));
-            if (lo) {
-                half8 vhi, vlo;
-                split_half8(x, &vhi, &vlo);
-                *(u32x4*)(img + vhi_at<D>(true, ck) + voff) = __builtin_bit_cast(u32x4, vhi);
-                if (vlo_at<D>(ck) >= 0)
-                    *(u32x4*)(img + vlo_at<D>(ck) + voff) = __builtin_bit_cast(u32x4, vlo);
+            if (ROT) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    vrows[(16 * (e >> 2) + 4 * q + (e & 3)) * D + d] = x[e];
             } else {
-                *(u32x4*)(img + vhi_at<D>(false, ck) + voff) = __builtin_bit_cast(u32x4, pack_half8(x));
+                *(u32x4*)(img + vt_at<D>() + 64 * d + 16 * (q ^ vswz(d))) = __builtin_bit_cast(u32x4, pack_half8(x));
             }
+        }
+    }
+    if (ROT) {
+        __syncthreads();
+        fwht_rows<D, kDqThreads>(vrows, 32, p.rot_c);
+#pragma unroll
+        for (int pc = threadIdx.x; pc < 4 * D; pc += kDqThreads) {
+            const int d = pc >> 2, q = pc & 3;
+            float x[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                x[e] = vrows[(16 * (e >> 2) + 4 * q + (e & 3)) * D + d];
+            *(u32x4*)(img + vt_at<D>() + 64 * d + 16 * (q ^ vswz(d))) = __builtin_bit_cast(u32x4, pack_half8(x));
         }
     }
     // a code block's key scales s[g][t] and offsets z'[g][t] (fp32, in place
@@ -449,19 +447,16 @@ __device__ __forceinline__ void ring_sync(int after)
 
 // KG: 32-channel score steps per key group when the format's keys have
 // per-token groups (code blocks then take exact code operands), 0 otherwise.
-// ROT: a rotating format, whose queries (rotated in fp32) and values carry
-// fp16 lo halves.  The inverse rotation sums the fp16 rounding errors of all
-// D channels of a value into every output element, which can itself be near
-// zero; without rotation an output element is a convex combination of one
-// channel's values, and their fp16 rounding (2^-11 relative) stays well
-// inside the relative part of the error bar.  A bf16 query of a non-rotating
-// format is exact in fp16 once scaled by a power of two, so its score steps
-// take one MFMA per key tile (code blocks) or two (hi and lo keys).
+// ROT: a rotating format, whose queries (rotated in fp32) carry fp16 lo
+// halves; its values come rotated back in the images, so the outputs need
+// no inverse rotation.  A bf16 query of a non-rotating format is exact in
+// fp16 once scaled by a power of two, so its score steps take one MFMA per
+// key tile (code blocks) or two (hi and lo keys).
 template <int D, int KG, bool ROT>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 {
     constexpr int QN = qn<D>(), RT = rows_per_tile<D>(), NKS = D / 32, NCT = D / 16;
-    constexpr int BI = image_bytes<D>(ROT), NST = stages<D>();
+    constexpr int BI = image_bytes<D>(), NST = stages<D>();
     constexpr int WI = BI / 1024;  // 1 KiB wave copies per image
     extern __shared__ __attribute__((aligned(16))) uint8_t plds[];
 
@@ -517,8 +512,8 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
             }
         }
         __syncthreads();
-        if (p.rotate)
-            fwht_rows<D>(xq, RT, p.rot_c);
+        if (ROT)
+            fwht_rows<D, kThreads>(xq, RT, p.rot_c);
 #pragma unroll
         for (int c = 0; c < QN; ++c) {
             const int rr = 16 * (QN * wave + c) + col;
@@ -617,11 +612,7 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         const uint8_t* kh = plds + stg * BI;
         const uint8_t* kl = kh + klo_at<D>();
         const bool codeb = KG > 0 && code_block<D>(p, it < nsb, blk);
-        const uint8_t* vt = kh + vhi_at<D>(ROT, codeb);
-        // V^T lo (D = 256: code blocks only; another block reads its hi
-        // half again, and the products of lo stay zero)
-        const uint8_t* vtl = ROT && vlo_at<D>(codeb) >= 0 ? kh + vlo_at<D>(codeb) : nullptr;
-        const bool vlo = vtl != nullptr;
+        const uint8_t* vt = kh + vt_at<D>();
         // copies of image it + NST - 1 (into the stage image it - 1 used),
         // one per score step so that the wave never waits on a burst of them
         const bool more = it + NST - 1 < nvis;
@@ -750,14 +741,12 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
                 copy16(cbase, (uint32_t)(1024 * (wave + 8 * i) + 16 * lane), cat + 1024 * (wave + 8 * i));
 
         // the first value fragments, read while the softmax runs
-        constexpr int NVP = D == 256 ? 1 : 2;  // value fragments read ahead (hi and lo)
-        half8 vf[NVP], vfl[NVP];
+        constexpr int NVP = D == 256 ? 1 : 2;  // value fragments read ahead
+        half8 vf[NVP];
 #pragma unroll
         for (int t = 0; t < NVP; ++t) {
             const int d = 16 * t + col;
-            const int off = 64 * d + 16 * (qg ^ vswz(d));
-            vf[t] = __builtin_bit_cast(half8, *(const u32x4*)(vt + off));
-            vfl[t] = vlo ? __builtin_bit_cast(half8, *(const u32x4*)(vtl + off)) : half8{};
+            vf[t] = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
         }
 
         // ---- online softmax per query column; P^T operands
@@ -826,30 +815,17 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
 
         // ---- O^T += V^T P^T, 16 channels per tile, keys in the slot order
         // above; fragment t + NVP is read while tile t's MFMAs run
-        auto value_products = [&](auto lo_tag) {
-            constexpr bool VL = decltype(lo_tag)::value;
 #pragma unroll
-            for (int t = 0; t < NCT; ++t) {
-                const half8 av = vf[t % NVP], avl = vfl[t % NVP];
-                if (t + NVP < NCT) {
-                    const int d = 16 * (t + NVP) + col;
-                    const int off = 64 * d + 16 * (qg ^ vswz(d));
-                    vf[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vt + off));
-                    if (VL)
-                        vfl[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vtl + off));
-                }
-#pragma unroll
-                for (int c = 0; c < QN; ++c) {
-                    acc[c][t] = mfma16(av, ph[c], acc[c][t]);
-                    if (VL)
-                        acc[c][t] = mfma16(avl, ph[c], acc[c][t]);
-                }
+        for (int t = 0; t < NCT; ++t) {
+            const half8 av = vf[t % NVP];
+            if (t + NVP < NCT) {
+                const int d = 16 * (t + NVP) + col;
+                vf[t % NVP] = __builtin_bit_cast(half8, *(const u32x4*)(vt + 64 * d + 16 * (qg ^ vswz(d))));
             }
-        };
-        if (vlo)
-            value_products(std::true_type{});
-        else
-            value_products(std::false_type{});
+#pragma unroll
+            for (int c = 0; c < QN; ++c)
+                acc[c][t] = mfma16(av, ph[c], acc[c][t]);
+        }
         // image it + 1 has landed (all of this wave's copies but those of
         // the images after it), and no wave reads stage it any more
         ring_sync(it + NST - 1 < nvis ? cw * (NST - 2) : 0);
@@ -863,38 +839,18 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnParams p)
         const float l = xor_sum16_32(lsum[c]);
         inv[c] = l > 0.0f ? 1.0f / l : 0.0f;
     }
-    if (!p.rotate) {
-#pragma unroll
-        for (int c = 0; c < QN; ++c) {
-            const int R = r0 + 16 * (QN * wave + c) + col;
-            if (R >= rows)
-                continue;
-            const int i = R / G, g = R % G;
-            float* dst = p.out + (((size_t)b * C + i) * p.H_q + (size_t)h * G + g) * D;
-#pragma unroll
-            for (int t = 0; t < NCT; ++t)
-                *(floatx4*)(dst + 16 * t + 4 * qg) = acc[c][t] * inv[c];
-        }
-        return;
-    }
-    float* xo = (float*)plds;  // [RT][D] fp32
+    // (values were rotated back in the images: outputs are in the original
+    // basis for every format)
 #pragma unroll
     for (int c = 0; c < QN; ++c) {
-        const int rr = 16 * (QN * wave + c) + col;
-#pragma unroll
-        for (int t = 0; t < NCT; ++t)
-            *(floatx4*)(xo + rr * D + 16 * t + 4 * qg) = acc[c][t] * inv[c];
-    }
-    __syncthreads();
-    fwht_rows<D>(xo, RT, p.rot_c);
-    for (int idx = threadIdx.x; idx < RT * (D / 4); idx += kThreads) {
-        const int rr = idx / (D / 4), d4 = 4 * (idx % (D / 4));
-        const int R = r0 + rr;
+        const int R = r0 + 16 * (QN * wave + c) + col;
         if (R >= rows)
             continue;
         const int i = R / G, g = R % G;
-        *(floatx4*)(p.out + (((size_t)b * C + i) * p.H_q + (size_t)h * G + g) * D + d4) =
-            *(const floatx4*)(xo + rr * D + d4);
+        float* dst = p.out + (((size_t)b * C + i) * p.H_q + (size_t)h * G + g) * D;
+#pragma unroll
+        for (int t = 0; t < NCT; ++t)
+            *(floatx4*)(dst + 16 * t + 4 * qg) = acc[c][t] * inv[c];
     }
 }
 
@@ -913,19 +869,20 @@ hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
 {
     constexpr int RT = rows_per_tile<D>();
     const int units = p0.B * p0.H;
-    const bool lo = p0.rotate != 0;
-    const size_t per_unit = (size_t)p0.pf_nvb * image_bytes<D>(lo);
+    const bool rot = p0.rotate != 0;
+    const size_t per_unit = (size_t)p0.pf_nvb * image_bytes<D>();
     const int group = (int)(ws_bytes / per_unit < (size_t)units ? ws_bytes / per_unit : (size_t)units);
     if (group < 1)
         return hipErrorInvalidValue;
     const int tiles = (p0.C * p0.G + RT - 1) / RT;
     const bool w8 = p0.k_bits == 8;  // 8-bit codes come as K and V both 8-bit
-    void (*deq)(AttnParams) = w8 ? dequant_kernel<D, true> : dequant_kernel<D, false>;
+    void (*deq)(AttnParams) = w8 ? (rot ? dequant_kernel<D, true, true> : dequant_kernel<D, true, false>)
+                                 : (rot ? dequant_kernel<D, false, true> : dequant_kernel<D, false, false>);
     // per-token key groups of 32 KG channels (a power of two from 32 to D);
     // groups of 32 at D = 256 keep the hi + lo path (the code path's eight
     // group sums per query would spill)
     const int kg = p0.k_axis == KVQ_PER_TOKEN ? p0.k_group / 32 : 0;
-    void (*att)(AttnParams) = lo ? pick<D, true>(kg) : pick<D, false>(kg);
+    void (*att)(AttnParams) = rot ? pick<D, true>(kg) : pick<D, false>(kg);
     if (kg != 0 && kg != 1 && kg != 2 && !(kg == 4 && D >= 128) && !(kg == 8 && D >= 256))
         return hipErrorInvalidValue;
     for (int u0 = 0; u0 < units; u0 += group) {
@@ -933,24 +890,17 @@ hipError_t launch(const AttnParams& p0, size_t ws_bytes, hipStream_t stream)
         p.pf_u0 = u0;
         p.pf_tiles = tiles;
         const int nu = units - u0 < group ? units - u0 : group;
-        launch_kernel(deq, dim3(p.pf_nvb, nu), dim3(kDqThreads), 0, stream, p);
-        launch_kernel(att, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(lo), stream, p);
+        launch_kernel(deq, dim3(p.pf_nvb, nu), dim3(kDqThreads), rot ? (size_t)32 * D * 4 : 0, stream, p);
+        launch_kernel(att, dim3(tiles * nu), dim3(kThreads), attn_lds_bytes<D>(), stream, p);
     }
     return hipGetLastError();
 }
 
 }  // namespace pre
 
-size_t prefill_image_bytes(int D, bool rotate)
+size_t prefill_image_bytes(int D)
 {
-    switch (D) {
-    case 64:
-        return pre::image_bytes<64>(rotate);
-    case 128:
-        return pre::image_bytes<128>(rotate);
-    default:
-        return pre::image_bytes<256>(rotate);
-    }
+    return (size_t)192 * D;
 }
 
 hipError_t launch_prefill(const AttnParams& p, int D, size_t ws_bytes, hipStream_t stream)
