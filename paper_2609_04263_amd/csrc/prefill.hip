@@ -9,10 +9,12 @@
 //      v_hat as fp16 transposed [D][32 key slots].  A block of per-token
 //      key groups whose tokens are all coded (a "code block") keeps the key
 //      codes instead, as exact fp16 values, with the groups' scales and
-//      offsets in place of the lo half.  The image is laid out exactly as
-//      the attention kernel reads it from LDS (16-byte chunks xor-swizzled
-//      by row so that the fragment reads are free of bank conflicts), so it
-//      moves to LDS with plain linear copies.
+//      offsets in place of the lo half.  A rotating format's value rows are
+//      rotated back to the original basis first (an fp32 FWHT per token in
+//      LDS), so the outputs need no inverse rotation.  The image is laid
+//      out exactly as the attention kernel reads it from LDS (16-byte
+//      chunks xor-swizzled by row so that the fragment reads are free of
+//      bank conflicts), so it moves to LDS with plain linear copies.
 //   2. attn_kernel: one workgroup per (unit, tile of query rows); query rows
 //      are the (chunk token, head of the KV group) pairs in token-major
 //      order.  Each of the eight waves owns 16 QN query rows (128 / 256 / 512
@@ -20,27 +22,29 @@
 //      a ring of LDS stages with global_load_lds_dwordx4 (no registers, no
 //      vector work), several blocks ahead, and per block:
 //      - scores S^T = K Q^T with v_mfma_f32_16x16x32_f16 (keys as rows,
-//        query rows as columns; hi x hi + hi x lo + lo x hi), queries
-//        pre-scaled by sm_scale * log2(e) so the softmax runs in base 2,
-//        online per column (the running maximum moves only in steps of more
-//        than 2^8); for a code block S = sum_g s_g (c_g . q_g) + z'_g sum q_g
-//        with exact products c q (q as hi + lo) and one fp32 scaling of
-//        each group's score tile;
-//      - O^T += V^T P^T in fp16 (probabilities in [0, 1] and values each
-//        carry an 11-bit relative rounding, well inside the output bound;
-//        the logits are the precision-critical product).  A lane holds
-//        score rows 4 q + i of the block's two 16-key tiles, which are
-//        exactly the eight k-slots 8 q .. 8 q + 7 its next MFMA operand
-//        needs when the keys of slot 8 q + e are taken as 4 q + e (e < 4)
-//        and 16 + 4 q + e - 4; the image stores V^T in that key order, so
-//        probabilities never cross lanes and a value operand is one read.
+//        query rows as columns).  A bf16 query of a non-rotating format,
+//        scaled by a power of two, is exact in fp16 (K hi x q + K lo x q);
+//        a rotated query (rotated in fp32 in LDS) is split into fp16 hi +
+//        lo (three products).  The softmax runs in base 2, online per
+//        column (the running maximum moves only in steps of more than 2^8);
+//        for a code block S = sum_g s_g (c_g . q_g) + z'_g sum q_g with
+//        exact products c q and one fp32 scaling of each group's score
+//        tile (the offset terms, at D = 256 with four key groups, as one
+//        fp32 MFMA per key tile);
+//      - O^T += V^T P^T in fp16 (probabilities in [0, 2^8] and values each
+//        carry an 11-bit relative rounding; the logits are the
+//        precision-critical product).  A lane holds score rows 4 q + i of
+//        the block's two 16-key tiles, which are exactly the eight k-slots
+//        8 q .. 8 q + 7 its next MFMA operand needs when the keys of slot
+//        8 q + e are taken as 4 q + e (e < 4) and 16 + 4 q + e - 4; the
+//        image stores V^T in that key order, so probabilities never cross
+//        lanes and a value operand is one read.
 // Reconstructing once per unit instead of once per query tile is what the
 // workspace buys: a 2048-token chunk has 4096 query rows per KV head at
 // grouping 2, i.e. 32 tiles that would each rebuild every block.
 // Sink tokens (fp16 rows) come first as blocks of their own, so every query
 // row holds a finite running maximum before the coded tail; fp16 window
 // tokens past the coded ones are copied into the image from the ring.
-// Rotated formats transform the queries (FWHT in LDS) and the outputs back.
 
 #include "kvq_internal.h"
 #include "kvq_device.h"
