@@ -307,12 +307,18 @@ __global__ __launch_bounds__(kDqThreads) void dequant_kernel(AttnParams p)
                     for (int e = 0; e < 8; ++e)
                         x[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), sc, z);
                 } else {
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int mi = 8 * P + e;
-                        x[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), meta(rks, mi, m16),
-                                  kaff ? meta(rkz, mi, m16) : 0.0f);
+                    // per-channel keys: the piece's eight channels' scales
+                    // (and offsets) are consecutive, two vector loads each
+                    float sc[8], zc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                    meta4(rks, 8 * P, m16, sc);
+                    meta4(rks, 8 * P + 4, m16, sc + 4);
+                    if (kaff) {
+                        meta4(rkz, 8 * P, m16, zc);
+                        meta4(rkz, 8 * P + 4, m16, zc + 4);
                     }
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        x[e] = dq(p.k_mode, kbits, code_of(w, kbits, e), sc[e], zc[e]);
                 }
             } else if (row) {
                 const u32x4 rw = *(const u32x4*)(row + 8 * P);
