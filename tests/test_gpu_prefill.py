@@ -18,17 +18,24 @@ import pytest
 import torch
 
 import oracle
-from paper_2609_04263_amd import synth
+from paper_2609_04263_amd import configs, synth
 
 from gpu_util import assert_close, dev_bf16, image
 from test_gpu_append import CASES
 
 pytestmark = pytest.mark.gpu
 
+# Rotating formats at the shapes the shared cases leave out: head size 64
+# (four-wave attention workgroups) and 32-channel key groups at 128.
+EXTRA = {
+    "had_d64_g32": (configs.make_format(4, 4, k_group=32, v_group=32, rotate=64), 64),
+    "had_d128_g32": (configs.make_format(4, 2, k_mode=1, v_mode=1, k_group=32, v_group=32, rotate=128), 128),
+}
+
 
 def run(name, B, H, G, n, C, seed, sm=None, ws_units=None):
     from paper_2609_04263_amd import kvq
-    fmt, D = CASES[name]
+    fmt, D = CASES[name] if name in CASES else EXTRA[name]
     outlier = ("student_t", 3.0) if fmt["rotate"] else ("scale", 4, 20.0)
     K, V = synth.kv_tokens(seed, B, n, H, D, outlier=outlier)
     T = n + 8
@@ -74,6 +81,12 @@ def test_prefill_peaked_and_flat_softmax():
 def test_prefill_workload_shape_chunk():
     # a 256-token chunk at the end of 1280 tokens, D = 256, G = 2 (the 12B layer's shape)
     run("gqa12b", B=1, H=2, G=2, n=1280, C=256, seed=130)
+
+
+@pytest.mark.parametrize("name", list(EXTRA))
+@pytest.mark.parametrize("n,C", [(33, 1), (150, 40), (300, 128)])
+def test_prefill_rotated_other_shapes(name, n, C):
+    run(name, B=2, H=2, G=3, n=n, C=C, seed=160 + n + C)
 
 
 def test_prefill_rotated_outputs_near_zero():
