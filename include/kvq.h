@@ -274,7 +274,7 @@ kvq_status kvq_decode_attn(const kvq_cache* cache, const void* Q, int H_q, float
 kvq_status kvq_decode_attn_noalloc(const kvq_cache* cache, const void* Q, int H_q, float sm_scale, void* O,
                                    void* stream);
 
-/* Chunked prefill attention (Sec. 3.1: evaluation consumes chunks; the
+/* Chunked prefill attention (Sec. 3.1: evaluation runs chunk by chunk; the
  * chunk's states are coded and appended first, then the reconstruction of
  * everything stored feeds attention).  The chunk is the newest C tokens of
  * the cache (1 <= C <= n); query i of the chunk, at position n - C + i,

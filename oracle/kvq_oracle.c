@@ -23,7 +23,7 @@
  *                     KVarN's fp16 sink tokens (the first S tokens).
  *   orc_dequant       Sec. 3.2: the reconstruction presented to attention.
  *   orc_decode_attn   Sec. 3.1-3.2: attention over that reconstruction, fp64.
- *   orc_prefill_attn  Sec. 3.1 "Evaluation consumes 128-token chunks": the
+ *   orc_prefill_attn  Sec. 3.1, chunked evaluation (128-token chunks): the
  *                     chunk's queries attend causally over the
  *                     reconstruction after the chunk has been appended.
  *
@@ -270,7 +270,7 @@ void orc_quant_sym(const float* x, int g, int bits, uint8_t* codes, float* s_out
     *s_out = s;
 }
 
-/* fp16 metadata (Sec. 3.1 stores "an FP16 scale, and an FP16 offset").
+/* fp16 metadata (Sec. 3.1 keeps each group's scale and offset in fp16).
  * Reading: the scale and offset are computed in fp32 exactly as above, then
  * rounded to fp16 (nearest, ties to even), the scale first clamped to
  * [2^-24, 65504] (the 1e-8 floor lies below fp16's smallest subnormal) and
@@ -953,7 +953,7 @@ int orc_decode_attn(const orc_format* f, int B, int H, int D, int T_max, const u
     return nomem ? ORC_ERR_NOMEM : ORC_OK;
 }
 
-/* Chunked prefill attention (Sec. 3.1: evaluation consumes chunks; the
+/* Chunked prefill attention (Sec. 3.1: evaluation runs chunk by chunk; the
  * chunk's states are coded and appended, then the reconstruction feeds
  * attention).  The cache holds n tokens, the last C of which are the
  * chunk; Q is bf16 [B][C][H_q][D] for positions n - C .. n - 1 and O is fp64

@@ -1,5 +1,5 @@
 // Chunked prefill attention over the packed cache (Sec. 3.1: evaluation
-// consumes chunks; the chunk's states are coded and appended, then its
+// runs chunk by chunk; the chunk's states are coded and appended, then its
 // queries attend causally over the reconstruction of everything stored).
 //
 // Two launches per group of (sequence, KV head) units:

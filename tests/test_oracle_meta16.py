@@ -1,5 +1,5 @@
-"""Pins of the oracle's fp16 metadata (Sec. 3.1 stores an FP16 scale and an
-FP16 offset; the rounding rule is a reading: fp32 statistics rounded to
+"""Pins of the oracle's fp16 metadata (Sec. 3.1 keeps each group's scale and
+offset in fp16; the rounding rule is a reading: fp32 statistics rounded to
 nearest fp16, scale clamped to [2^-24, 65504], codes from the rounded values).
 
 * hand-worked groups whose statistics are exact in fp16 give the same codes

@@ -1,5 +1,5 @@
-"""Pins of the oracle's chunked prefill attention (Sec. 3.1: evaluation consumes
-chunks; the chunk's states are appended, then its queries attend over the
+"""Pins of the oracle's chunked prefill attention (Sec. 3.1: evaluation runs chunk
+by chunk; the chunk's states are appended, then its queries attend over the
 reconstruction, causally).
 
 * Agrees with torch's scaled_dot_product_attention (fp64, grouped-query mode,
